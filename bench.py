@@ -1,0 +1,202 @@
+#!/usr/bin/env python3
+"""Benchmark: paged MoE decode tokens/s at a fixed VRAM expert budget, one MI355X.
+
+Workload (default): Qwen3-30B-A3B-shaped paged decode — 48 MoE layers, d=2048, 128 bf16 experts
+per layer (SwiGLU, I=768, 9,437,184-byte blobs), top-8 softmax-then-renormalise routing, batch 1,
+AR(1) hidden states, expert budget 25% of the 6144 experts (C = 32 slots per layer), LRU paging
+from pinned host masters.  A step is one decode token through all 48 layers: router + top-k,
+slot lookup and fault list, host->device fills of the faults, slot-indirected SwiGLU FFN and
+combine, layer after layer.  Inputs (weights in pinned host memory, hidden states in HBM) are in
+place before the timed region; every step starts from the slot contents the previous one left.
+
+Reported beside the throughput:
+  roofline       the expert gate/up GEMV kernel (the largest share of HBM bytes): algorithmic
+                 bytes per launch / average launch time from HIP events over the timed region,
+                 against the 8 TB/s HBM peak;
+  path_roofline  the whole path against T_roof = sum over layer-steps of HBM bytes / 8 TB/s +
+                 fault bytes / measured host-link bandwidth (exact fault counts of the run);
+  cpu_baseline   the fp64 CPU oracle (fully resident layer) on a bounded sample of the same
+                 workload, on this host's cores.
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def measure_hbm_copy(torch, wisp, nbytes=1 << 30, reps=5):
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    s = torch.cuda.Stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    rates = []
+    with torch.cuda.stream(s):
+        wisp.hbm_copy(src, dst, nbytes, s)
+        for _ in range(reps):
+            ev0.record(s)
+            wisp.hbm_copy(src, dst, nbytes, s)
+            ev1.record(s)
+            ev1.synchronize()
+            rates.append(2 * nbytes / (ev0.elapsed_time(ev1) * 1e-3) / 1e9)
+    del src, dst
+    rates.sort()
+    return rates[len(rates) // 2]
+
+
+def cpu_baseline(run, wl, start_step, max_tokens=24, budget_s=15.0):
+    """The oracle as it stands: fully resident fp64 layer, all layers of consecutive decode steps."""
+    import oracle
+    threads = oracle.num_threads()
+    t0 = time.perf_counter()
+    tokens = 0
+    s = start_step
+    while tokens < max_tokens and s < run.x_host.shape[1]:
+        for l in range(wl.L):
+            oracle.moe_layer(wl.route, run.master_ptrs(l), run.wr_host[l], run.x_host[l, s], wl.k, wl.I, wl.w_dtype,
+                             run.shared_ptr(l), wl.n_groups, wl.topk_groups)
+        tokens += wl.T
+        s += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return dict(value=tokens / dt, unit="tokens/s", cores=threads, kind="oracle",
+                sample=f"{tokens // wl.T} decode step(s) x {wl.L} layers x batch {wl.T} "
+                       f"(fully resident fp64 layer, weights read from the same pinned host masters), {dt:.1f} s")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed decode steps (default: the run length minus warmup)")
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true", help="skip the per-kernel HIP events")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); the paged "
+              f"MoE layer here runs per GPU and has no multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_21868_amd import wisp
+    from paper_2606_21868_amd.workloads import BENCH_WORKLOAD, DTYPE_NAMES, WORKLOADS
+
+    wl = WORKLOADS[args.workload or BENCH_WORKLOAD]
+    if wl.prefill:
+        raise SystemExit("prefill workloads are benchmarked by their own tests, not by this decode benchmark")
+    warmup = max(0, args.warmup)
+    steps = args.steps if args.steps is not None else wl.steps - warmup
+    if steps < 1:
+        raise SystemExit("need at least one timed step")
+    total = warmup + steps
+    log(f"workload {wl.name}: {warmup} warmup + {steps} timed steps, cap {wl.cap}")
+
+    run = wisp.DecodeRun(wl, device=0, steps=total)
+    t0 = time.time()
+    run.generate()
+    log(f"generated {wl.L * wl.N} expert blobs ({wl.L * wl.N * wl.blob / 1e9:.1f} GB pinned) and inputs in "
+        f"{time.time() - t0:.1f} s")
+    n_probe = max(1, math.ceil(2e9 / wl.blob))
+    link = run.ctx.probe_h2d(n_probe, 5)
+    hbm_copy = measure_hbm_copy(torch, wisp)
+    log(f"host->device {link:.1f} GB/s (median of 5 x {n_probe} blobs); device copy {hbm_copy:.0f} GB/s")
+    assert run.set_cap(wl.cap) == wl.cap
+
+    tw = time.perf_counter()
+    if warmup:
+        run.decode(record=False, steps=warmup, start=0)
+    tw = time.perf_counter() - tw
+    run.ctx.reset_stats()
+    run.ctx.reset_kernel_times()
+    run.ctx.set_profiling(0 if args.no_kernel_timing else 1)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    out = run.decode(record=False, steps=steps, start=warmup)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t1
+    run.ctx.set_profiling(0)
+    tok_s = wl.T * steps / elapsed
+    log(f"timed {steps} steps in {elapsed:.3f} s -> {tok_s:.2f} tokens/s (warmup {tw:.2f} s)")
+
+    # path roofline from the exact counts of the timed steps
+    hits, misses = out["hits"], out["misses"]
+    distinct = hits + misses
+    router_bytes = wl.N * wl.d * 4
+    hbm_bytes = float(distinct.sum()) * wl.blob + router_bytes * wl.L * steps
+    link_bytes = float(misses.sum()) * wl.blob
+    t_roof = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (link * 1e9)
+    path = dict(t_roof_s=t_roof, t_measured_s=elapsed, frac=t_roof / elapsed, roofline_tokens_per_s=wl.T * steps / t_roof,
+                link_GBps_measured=link, hbm_peak_GBps=HBM_PEAK_GBPS, device_copy_GBps_measured=hbm_copy,
+                hbm_bytes_per_token=hbm_bytes / (wl.T * steps), link_bytes_per_token=link_bytes / (wl.T * steps),
+                faults_per_token=float(misses.sum()) / (wl.T * steps),
+                fault_rate=float(misses.sum()) / float(distinct.sum()))
+
+    kernels = {}
+    for kc, name in enumerate(wisp.KERNEL_CLASS_NAMES):
+        t = run.ctx.kernel_times(kc)
+        if t["launches"]:
+            avg_us = t["total_ms"] * 1e3 / t["launches"]
+            kernels[name] = dict(launches=t["launches"], avg_us=avg_us, total_ms=t["total_ms"],
+                                 bytes_per_launch=t["bytes"] / t["launches"],
+                                 GBps=t["bytes"] / (t["total_ms"] * 1e-3) / 1e9 if t["total_ms"] > 0 else None)
+    roof = None
+    if "ffn_gateup" in kernels:
+        g = kernels["ffn_gateup"]
+        roof = dict(bound="hbm", achieved=g["GBps"], peak=HBM_PEAK_GBPS, unit="GB/s", frac=g["GBps"] / HBM_PEAK_GBPS,
+                    traffic=None, kernel="ffn_rows<bf16, gate/up> (expert GEMV, W1+W3 rows)",
+                    avg_launch_us=g["avg_us"], bytes_per_launch=g["bytes_per_launch"])
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        cpu = cpu_baseline(run, wl, warmup)
+        log(f"cpu oracle {cpu['value']:.3f} tokens/s on {cpu['cores']} threads")
+
+    result = {
+        "metric": "paged MoE decode tokens/s at fixed VRAM expert budget",
+        "value": tok_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": elapsed / steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": DTYPE_NAMES[wl.w_dtype],
+        "data": "synthetic (seeded N(0,0.02) weights, AR(1) rho=0.9 hidden states)",
+        "config": {"workload": wl.description, "layers": wl.L, "d_model": wl.d, "d_ff": wl.I, "experts": wl.N,
+                   "top_k": wl.k, "batch": wl.T, "expert_budget_bytes": wl.budget_bytes, "cap_per_layer": wl.cap,
+                   "expert_blob_bytes": wl.blob, "decode_steps": total},
+        "roofline": roof,
+        "path_roofline": path,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+        "kernel_timing": not args.no_kernel_timing,
+    }
+    run.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

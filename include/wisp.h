@@ -1,0 +1,206 @@
+/*
+ * wisp.h — C ABI of the paged MoE layer for AMD MI355X (gfx950).
+ *
+ * Implements the per-layer decode step of WiSP (arXiv 2606.21868): a routing-aware expert pager
+ * over a slot-indirected expert FFN.  One layer-step is
+ *   1. router scoring and top-k                    wisp_route_topk   (Sec. 3.1, selection of R)
+ *   2. slot lookup, fault list, LRU victims        wisp_page_in      (Algorithm 1, faults/victims/assign)
+ *   3. async host->device fills of the faults      wisp_page_in      (Algorithm 1, copy_async + map update)
+ *   4. slot-indirected SwiGLU FFN + combine        wisp_moe_forward  (Algorithm 1, final FusedMoE call)
+ * and the expert budget is set or resized with wisp_set_budget (cap C = B_exp / (L * M_e),
+ * Sec. 3.1; resize at a drained barrier, keeping the prior state on failure, Sec. 3.5 and App. B).
+ *
+ * Conventions
+ *  - Every call returns a wisp_status and never throws.  On error nothing has changed: arguments
+ *    are validated before any state is touched, and resizes are transactional.  The message of
+ *    the last error on the calling thread is returned by wisp_last_error().
+ *  - A context is one model; it is not thread-safe.  All device pointers must belong to the
+ *    device that was current at wisp_create.  `stream` arguments are hipStream_t handles passed
+ *    as void* (NULL = the legacy default stream; a non-blocking stream is recommended).
+ *  - The caller owns x, idx, w, y, the router weights and the streams.  The library owns the
+ *    pinned host masters of every expert, the device expert slots, its internal side stream and
+ *    events, and its scratch buffers.
+ *  - Expert blob format (the unit that is paged; one contiguous blob per expert):
+ *      W1 [I, d] row-major | W3 [I, d] row-major | W2 [d, I] row-major
+ *    fp32 / bf16 store the elements; WISP_FP8E4M3_B128 stores OCP E4M3FN codes and appends
+ *    bf16 scales S1 [I/128, d/128] | S3 [I/128, d/128] | S2 [d/128, I/128] (one per 128x128
+ *    block); a weight is code * scale.  The expert computes o = W2 (silu(W1 x) * (W3 x)).
+ */
+#ifndef WISP_H
+#define WISP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct wisp_ctx wisp_ctx;
+
+typedef enum {
+  WISP_OK = 0,
+  WISP_E_INVAL = -1,        /* bad argument (range, shape, null pointer) */
+  WISP_E_NOMEM = -2,        /* host or device allocation failed; state unchanged */
+  WISP_E_HIP = -3,          /* a HIP runtime call failed */
+  WISP_E_NOT_RESIDENT = -4, /* a routed expert is not resident when the FFN would run */
+  WISP_E_STATE = -5         /* call out of order (no budget set, no pending page-in, ...) */
+} wisp_status;
+
+typedef enum {
+  WISP_ROUTE_SOFTMAX_RENORM = 0, /* p = softmax(z) over all N, top-k of p, g = p_R / sum p_R */
+  WISP_ROUTE_TOPK_SOFTMAX = 1,   /* top-k of z, g = softmax(z_R) */
+  WISP_ROUTE_SIGMOID_GROUP = 2   /* s = sigmoid(z); groups of N/n_groups ids scored by their two
+                                    largest s; keep topk_groups groups; top-k s; g = s_R / sum s_R */
+} wisp_route;
+
+typedef enum { WISP_F32 = 0, WISP_BF16 = 1, WISP_FP8E4M3_B128 = 2 } wisp_dtype;
+
+typedef struct {
+  int32_t n_layers;    /* L */
+  int32_t d_model;     /* d */
+  int32_t d_ff;        /* I, expert intermediate width */
+  int32_t n_experts;   /* N routed experts per layer (<= 256) */
+  int32_t top_k;       /* k (<= 8) */
+  int32_t n_groups;    /* WISP_ROUTE_SIGMOID_GROUP only, else 1 */
+  int32_t topk_groups; /* WISP_ROUTE_SIGMOID_GROUP only, else 1 */
+  int32_t has_shared;  /* 1: every layer has one always-resident shared expert (weight 1) */
+  int32_t route;       /* wisp_route */
+  int32_t w_dtype;     /* wisp_dtype of expert weights */
+  int32_t x_dtype;     /* WISP_F32 or WISP_BF16 hidden states */
+  int32_t max_tokens;  /* largest T passed to route / forward */
+} wisp_model_desc;
+
+typedef struct {
+  uint32_t hits;      /* distinct routed experts already resident */
+  uint32_t misses;    /* faults: experts copied host -> device */
+  uint32_t chunks;    /* Algorithm 1 steps taken (more than one when the union exceeds C) */
+  uint32_t steps;     /* layer-steps counted (cumulative statistics) */
+  uint64_t h2d_bytes; /* misses * M_e */
+} wisp_page_stats;
+
+/* Bytes M_e of one expert blob for a description (weights + fp8 scales). */
+wisp_status wisp_expert_bytes(const wisp_model_desc* desc, uint64_t* bytes);
+
+/* Create a context on the current device: pinned host masters for every expert (and the shared
+ * experts), the side stream and events, and scratch sized by max_tokens.  No expert slots exist
+ * until wisp_set_budget.  The masters are uninitialised: fill them through wisp_expert_host_ptr
+ * and then call wisp_masters_ready.  (Masters in pinned host memory: App. C.) */
+wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out);
+
+/* Wait for all outstanding work of the context and free everything it owns. */
+wisp_status wisp_destroy(wisp_ctx* ctx);
+
+/* Host address and size of expert `expert` of `layer` in the pinned masters (expert = -1: the
+ * shared expert).  The caller writes the blob there before wisp_masters_ready. */
+wisp_status wisp_expert_host_ptr(wisp_ctx* ctx, int32_t layer, int32_t expert, void** ptr, uint64_t* bytes);
+
+/* Declare the masters final: copies the shared experts to their fixed device slab and drops every
+ * resident expert so later faults re-read the masters.  Synchronous. */
+wisp_status wisp_masters_ready(wisp_ctx* ctx);
+
+/* Router weights of `layer`: device pointer to W_r [N, d] fp32 row-major, caller-owned, valid
+ * for the life of the context. */
+wisp_status wisp_router_weights(wisp_ctx* ctx, int32_t layer, const float* w_r_dev);
+
+/* Set the VRAM expert budget B_exp (bytes).  The per-layer cap becomes C = floor(B_exp / (L * M_e))
+ * (Sec. 3.1); it must satisfy 1 <= C <= N.  Runs at a drained barrier: waits for every
+ * outstanding fill and FFN of the context; fails with WISP_E_STATE if a page-in is pending.
+ * Shrink keeps each layer's C most recently used experts (largest LRU tick, ties to the lower
+ * slot), renumbers them in slot order and frees the rest first; grow allocates new empty slots.
+ * Device footprint never exceeds max(old, new).  On failure (WISP_E_NOMEM) every layer keeps its
+ * previous slots, tables and contents.  cap_out (optional) receives C. */
+wisp_status wisp_set_budget(wisp_ctx* ctx, uint64_t expert_bytes, int32_t* cap_out);
+
+/* Make experts 0 .. C-1 of every layer resident (one Algorithm 1 step per layer over those ids)
+ * and wait for the copies.  With C = N this is the fully resident mode in which a run takes no
+ * faults.  Not counted in the statistics. */
+wisp_status wisp_preload(wisp_ctx* ctx);
+
+/* Route T tokens of `layer`: x_dev [T, d] (x_dtype) -> idx_dev [T, k] int32 and w_dev [T, k] fp32
+ * on `stream`, ranks ordered (score desc, expert id asc).  If idx_host is not NULL the call
+ * waits for the indices and copies them there (T*k int32): this is the one device->host
+ * synchronisation of a layer-step, needed because the pager runs on the host. */
+wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int32_t T, int32_t* idx_dev,
+                            float* w_dev, int32_t* idx_host, void* stream);
+
+/* Algorithm 1 lines for faults, victims, assignment, fills, map update and ticks, for the routing
+ * ids_host [T, k] of `layer`.  The reference set is the union of the T selections.  If it fits
+ * in C it is one step; otherwise it is split into chunks of C (resident ids ascending, then the
+ * rest ascending), whose fills are issued by wisp_moe_forward between chunk computations.  Fills
+ * are hipMemcpyAsync copies of whole blobs from the pinned masters on the library's side stream,
+ * ordered after the layer's previous FFN (write-after-read on victim slots).  Asynchronous.
+ * st (optional) receives this step's counts.  Must be followed by wisp_moe_forward for the
+ * same layer and T before the next page-in of that layer. */
+wisp_status wisp_page_in(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, int32_t T, wisp_page_stats* st);
+
+/* The FFN over the routing given to the preceding wisp_page_in of `layer`: for every token t and
+ * rank j, o_tj = W2 (silu(W1 x_t) * (W3 x_t)) with the weights of expert idx[t,j] read from its
+ * slot, then y_t = sum_j w_dev[t,j] o_tj in rank order (+ the shared expert's output).  Experts
+ * that were resident start at once; faulted ones wait for their fill.  x_dev [T, d], w_dev [T, k]
+ * fp32, y_dev [T, d] fp32, on `stream`.  Returns WISP_E_NOT_RESIDENT if a routed expert is not
+ * resident (exactness invariant, Sec. 3.2).  st (optional) receives the step's counts. */
+wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, int32_t T, const float* w_dev,
+                             float* y_dev, void* stream, wisp_page_stats* st);
+
+/* One decode step over all layers in order (route, page-in, forward per layer): x_dev [L, T, d],
+ * idx_dev [L, T, k], w_dev [L, T, k], y_dev [L, T, d].  Layer l+1 is routed only after layer l's
+ * FFN has been issued.  st (optional) receives [L] per-layer counts. */
+wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_t* idx_dev, float* w_dev,
+                             float* y_dev, void* stream, wisp_page_stats* st);
+
+/* Cumulative counts of `layer` since creation or the last wisp_reset_stats. */
+wisp_status wisp_get_stats(wisp_ctx* ctx, int32_t layer, wisp_page_stats* cumulative);
+wisp_status wisp_reset_stats(wisp_ctx* ctx);
+
+/* Current cap C (0 before the first wisp_set_budget). */
+wisp_status wisp_get_cap(wisp_ctx* ctx, int32_t* cap);
+
+/* Slot of `expert` in `layer` (-1 if not resident), and the expert held by `slot` (-1 if empty). */
+wisp_status wisp_slot_of(wisp_ctx* ctx, int32_t layer, int32_t expert, int32_t* slot);
+wisp_status wisp_expert_in_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, int32_t* expert);
+
+/* Copy the device bytes of `slot` of `layer` to host memory dst (M_e bytes); synchronous. */
+wisp_status wisp_read_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, void* dst);
+
+/* Kernel timing.  When on, every kernel launch and every fill batch is bracketed by HIP events
+ * on its own stream; durations are accumulated per class.  Classes: */
+typedef enum {
+  WISP_K_ROUTER_LOGITS = 0, WISP_K_ROUTER_SELECT = 1, WISP_K_FFN_GATEUP = 2, WISP_K_FFN_DOWN = 3,
+  WISP_K_COMBINE = 4, WISP_K_H2D_FILL = 5, WISP_K_GROUPED_GATEUP = 6, WISP_K_GROUPED_DOWN = 7,
+  WISP_K_PERMUTE = 8, WISP_K_NUM = 9
+} wisp_kernel_class;
+wisp_status wisp_set_profiling(wisp_ctx* ctx, int32_t on);
+/* Waits for outstanding timed work, then returns the accumulated total milliseconds, number of
+ * launches, and algorithmic HBM bytes (weights and activations each read or written once) of a
+ * class. */
+wisp_status wisp_kernel_times(wisp_ctx* ctx, int32_t kclass, double* total_ms, uint64_t* launches,
+                              uint64_t* bytes);
+wisp_status wisp_reset_kernel_times(wisp_ctx* ctx);
+
+/* Measure host->device bandwidth of the expert path: `reps` rounds, each copying `count` expert
+ * blobs (M_e each) from the pinned masters to a scratch device buffer on the side stream; returns
+ * the median GB/s (1e9 bytes/s).  Allocates and frees the scratch buffer itself. */
+wisp_status wisp_probe_h2d(wisp_ctx* ctx, int32_t count, int32_t reps, double* gbps);
+
+/* A plain device copy kernel (16-byte loads and stores) of `bytes` from src to dst on `stream`:
+ * the reference for HBM counters and for measured copy bandwidth.  bytes must be a multiple of
+ * 16 and both pointers 16-byte aligned. */
+wisp_status wisp_hbm_copy(const void* src, void* dst, uint64_t bytes, void* stream);
+
+/* Decode n fp8 E4M3 codes to fp32 on the device with the same conversion the FFN kernels use
+ * (for checking the hardware conversion against the format definition). */
+wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n, void* stream);
+
+/* Fault injection for tests of the transactional resize: the next `n`-th device slot allocation
+ * (counting from 1, across later wisp_set_budget calls) fails as if out of memory.  0 = off. */
+wisp_status wisp_debug_fail_slot_alloc(wisp_ctx* ctx, int32_t n);
+
+/* Message of the last error on this thread ("" if none). */
+const char* wisp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WISP_H */

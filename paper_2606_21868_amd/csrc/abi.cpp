@@ -1,0 +1,844 @@
+// C ABI of the paged MoE layer: context, pinned expert masters, the expert pager (Algorithm 1 of
+// WiSP, arXiv 2606.21868, Sec. 3.2) and the launch sequence of one layer-step.
+//
+// Streams and ordering.  The caller's stream carries the router, the FFN kernels and the combine.
+// The library's side stream (non-blocking, default priority) carries the host->device fills.
+// Per layer: the side stream waits for the layer's last FFN before overwriting victim slots
+// (write-after-read), and the caller's stream waits for the fill event before the FFN of the
+// faulted experts (read-after-write).  Resident experts' FFN is issued before that wait, so it
+// overlaps the fills.  When the union of a layer-step exceeds C, chunk i+1's fills wait for
+// chunk i's FFN.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "slot_table.hpp"
+#include "wisp.h"
+
+using namespace wisp;
+
+namespace {
+
+thread_local std::string g_err;
+
+wisp_status fail(wisp_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+#define WISP_HIP(expr, what)                                                               \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess) return fail(WISP_E_HIP, std::string(what) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr size_t kMasterAlign = 4096;
+
+struct TimedPair {
+  hipEvent_t a, b;
+  int kclass;
+  uint64_t bytes;
+};
+
+struct LayerState {
+  std::unique_ptr<SlotTable> table;
+  std::vector<uint8_t*> slot_mem;
+  const float* wr = nullptr;
+  uint8_t* shared_dev = nullptr;
+  hipEvent_t use_ev = nullptr;
+  bool use_ev_recorded = false;
+  std::vector<hipEvent_t> fill_ev;
+  std::vector<hipEvent_t> chunk_ev;
+  bool pending = false;
+  int32_t T = 0;
+  std::vector<int32_t> ids;
+  StepPlan plan;
+  std::vector<std::vector<const uint8_t*>> chunk_ptrs;
+  wisp_page_stats cum{};
+};
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+}  // namespace
+
+struct wisp_ctx {
+  wisp_model_desc desc{};
+  int device = 0;
+  BlobLayout blob;
+  FfnShape shape;
+  size_t master_stride = 0;
+  std::vector<uint8_t*> masters;
+  std::vector<uint8_t*> shared_master;
+  int32_t cap = 0;
+  std::vector<LayerState> layers;
+  hipStream_t side = nullptr;
+  hipEvent_t route_ev = nullptr;
+  float* logits = nullptr;
+  void* h = nullptr;
+  float* buf = nullptr;
+  int32_t* idx_pinned = nullptr;
+  std::vector<int32_t> ids_scratch;
+  bool profiling = false;
+  std::vector<TimedPair> timed;
+  std::vector<hipEvent_t> ev_pool;
+  double k_ms[WISP_K_NUM] = {};
+  uint64_t k_n[WISP_K_NUM] = {};
+  uint64_t k_bytes[WISP_K_NUM] = {};
+  int32_t fail_alloc_at = 0;
+  int32_t alloc_counter = 0;
+
+  uint8_t* master(int l, int e) const { return masters[l] + static_cast<size_t>(e) * master_stride; }
+  int k() const { return desc.top_k; }
+  size_t h_elem() const { return shape.h_dtype == DT_F32 ? 4 : 2; }
+  size_t x_elem() const { return desc.x_dtype == DT_F32 ? 4 : 2; }
+};
+
+namespace {
+
+// ------------------------------------------------------------------------------------------
+// profiling
+// ------------------------------------------------------------------------------------------
+hipEvent_t pool_event(wisp_ctx* c) {
+  if (!c->ev_pool.empty()) {
+    hipEvent_t e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+LaunchTiming timing_begin(wisp_ctx* c) {
+  LaunchTiming t;
+  if (c->profiling) {
+    t.start = pool_event(c);
+    t.stop = pool_event(c);
+  }
+  return t;
+}
+
+void timing_end(wisp_ctx* c, const LaunchTiming& t, int kclass, uint64_t bytes) {
+  if (!c->profiling || !t.start || !t.stop) return;
+  c->timed.push_back({t.start, t.stop, kclass, bytes});
+}
+
+// Accumulate every finished timed pair; with wait, first wait for all of them.
+void harvest(wisp_ctx* c, bool wait) {
+  size_t keep = 0;
+  for (size_t i = 0; i < c->timed.size(); ++i) {
+    TimedPair& p = c->timed[i];
+    if (wait) hipEventSynchronize(p.b);
+    if (hipEventQuery(p.b) != hipSuccess) {
+      c->timed[keep++] = p;
+      continue;
+    }
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
+      c->k_ms[p.kclass] += ms;
+      c->k_n[p.kclass] += 1;
+      c->k_bytes[p.kclass] += p.bytes;
+    }
+    c->ev_pool.push_back(p.a);
+    c->ev_pool.push_back(p.b);
+  }
+  c->timed.resize(keep);
+}
+
+// ------------------------------------------------------------------------------------------
+// validation helpers
+// ------------------------------------------------------------------------------------------
+wisp_status check_desc(const wisp_model_desc* d) {
+  if (!d) return fail(WISP_E_INVAL, "desc is NULL");
+  if (d->n_layers < 1 || d->d_model < 1 || d->d_ff < 1) return fail(WISP_E_INVAL, "non-positive shape");
+  if (d->n_experts < 1 || d->n_experts > 256) return fail(WISP_E_INVAL, "n_experts must be in [1, 256]");
+  if (d->top_k < 1 || d->top_k > 8 || d->top_k > d->n_experts) return fail(WISP_E_INVAL, "top_k must be in [1, min(8, N)]");
+  if (d->max_tokens < 1) return fail(WISP_E_INVAL, "max_tokens must be >= 1");
+  if (d->route < 0 || d->route > 2) return fail(WISP_E_INVAL, "unknown route");
+  if (d->route == WISP_ROUTE_SIGMOID_GROUP) {
+    if (d->n_groups < 1 || d->n_groups > 32 || d->n_experts % d->n_groups)
+      return fail(WISP_E_INVAL, "n_groups must divide N and be <= 32");
+    if (d->topk_groups < 1 || d->topk_groups > d->n_groups ||
+        d->topk_groups * (d->n_experts / d->n_groups) < d->top_k)
+      return fail(WISP_E_INVAL, "topk_groups too small for top_k");
+  }
+  const bool ok_pair = (d->w_dtype == WISP_F32 && d->x_dtype == WISP_F32) ||
+                       (d->w_dtype == WISP_BF16 && d->x_dtype == WISP_BF16) ||
+                       (d->w_dtype == WISP_FP8E4M3_B128 && d->x_dtype == WISP_BF16);
+  if (!ok_pair) return fail(WISP_E_INVAL, "supported (weights, inputs): (f32, f32), (bf16, bf16), (fp8, bf16)");
+  if (d->d_model % 16 || d->d_ff % 16) return fail(WISP_E_INVAL, "d_model and d_ff must be multiples of 16");
+  if (d->w_dtype == WISP_FP8E4M3_B128 && (d->d_model % 128 || d->d_ff % 128))
+    return fail(WISP_E_INVAL, "fp8 blocks need d_model and d_ff multiples of 128");
+  const int epl = d->w_dtype == WISP_F32 ? 4 : d->w_dtype == WISP_BF16 ? 8 : 16;
+  if ((d->d_model / epl) % 8 || (d->d_ff / epl) % 8)
+    return fail(WISP_E_INVAL, "d_model and d_ff must be multiples of 8 x 16-byte chunks");
+  if (d->has_shared != 0 && d->has_shared != 1) return fail(WISP_E_INVAL, "has_shared must be 0 or 1");
+  return WISP_OK;
+}
+
+wisp_status check_ctx(wisp_ctx* c) {
+  if (!c) return fail(WISP_E_INVAL, "ctx is NULL");
+  hipError_t e = hipSetDevice(c->device);
+  if (e != hipSuccess) return fail(WISP_E_HIP, std::string("hipSetDevice: ") + hipGetErrorString(e));
+  return WISP_OK;
+}
+
+wisp_status check_layer(wisp_ctx* c, int32_t l) {
+  if (l < 0 || l >= c->desc.n_layers) return fail(WISP_E_INVAL, "layer out of range");
+  return WISP_OK;
+}
+
+void free_ctx(wisp_ctx* c) {
+  if (!c) return;
+  if (c->side) hipStreamSynchronize(c->side);
+  for (auto& L : c->layers) {
+    if (L.use_ev_recorded) hipEventSynchronize(L.use_ev);
+  }
+  hipDeviceSynchronize();
+  for (auto& L : c->layers) {
+    for (auto* p : L.slot_mem) if (p) hipFree(p);
+    if (L.shared_dev) hipFree(L.shared_dev);
+    if (L.use_ev) hipEventDestroy(L.use_ev);
+    for (auto e : L.fill_ev) hipEventDestroy(e);
+    for (auto e : L.chunk_ev) hipEventDestroy(e);
+  }
+  for (auto* p : c->masters) if (p) hipHostFree(p);
+  for (auto* p : c->shared_master) if (p) hipHostFree(p);
+  for (auto& t : c->timed) { hipEventDestroy(t.a); hipEventDestroy(t.b); }
+  for (auto e : c->ev_pool) hipEventDestroy(e);
+  if (c->route_ev) hipEventDestroy(c->route_ev);
+  if (c->side) hipStreamDestroy(c->side);
+  if (c->logits) hipFree(c->logits);
+  if (c->h) hipFree(c->h);
+  if (c->buf) hipFree(c->buf);
+  if (c->idx_pinned) hipHostFree(c->idx_pinned);
+  delete c;
+}
+
+wisp_status ensure_events(std::vector<hipEvent_t>& v, size_t n) {
+  while (v.size() < n) {
+    hipEvent_t e = nullptr;
+    WISP_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreateWithFlags");
+    v.push_back(e);
+  }
+  return WISP_OK;
+}
+
+// Drained barrier: every fill and every FFN of the context has finished.
+wisp_status drain(wisp_ctx* c) {
+  WISP_HIP(hipStreamSynchronize(c->side), "hipStreamSynchronize(side)");
+  for (auto& L : c->layers)
+    if (L.use_ev_recorded) WISP_HIP(hipEventSynchronize(L.use_ev), "hipEventSynchronize(layer)");
+  return WISP_OK;
+}
+
+// Enqueue the fills of chunk ci of `layer`'s pending plan on the side stream.
+wisp_status issue_fills(wisp_ctx* c, int32_t layer, size_t ci) {
+  LayerState& L = c->layers[layer];
+  const ChunkPlan& cp = L.plan.chunks[ci];
+  if (cp.n_faults == 0) return WISP_OK;
+  if (ci == 0) {
+    if (L.use_ev_recorded) WISP_HIP(hipStreamWaitEvent(c->side, L.use_ev, 0), "hipStreamWaitEvent(use)");
+  } else {
+    WISP_HIP(hipStreamWaitEvent(c->side, L.chunk_ev[ci - 1], 0), "hipStreamWaitEvent(chunk)");
+  }
+  LaunchTiming tm = timing_begin(c);
+  if (tm.start) WISP_HIP(hipEventRecord(tm.start, c->side), "hipEventRecord");
+  for (size_t i = 0; i < cp.experts.size(); ++i) {
+    if (!cp.fault[i]) continue;
+    WISP_HIP(hipMemcpyAsync(L.slot_mem[cp.slots[i]], c->master(layer, cp.experts[i]), c->blob.bytes,
+                            hipMemcpyHostToDevice, c->side),
+             "hipMemcpyAsync(fill)");
+  }
+  if (tm.stop) WISP_HIP(hipEventRecord(tm.stop, c->side), "hipEventRecord");
+  timing_end(c, tm, WISP_K_H2D_FILL, static_cast<uint64_t>(cp.n_faults) * c->blob.bytes);
+  WISP_HIP(hipEventRecord(L.fill_ev[ci], c->side), "hipEventRecord(fill)");
+  return WISP_OK;
+}
+
+uint64_t ffn_bytes(const wisp_ctx* c, const FfnBatch& b, bool gateup) {
+  const BlobLayout& B = c->blob;
+  const uint64_t n = static_cast<uint64_t>(B.d) * B.I;
+  const uint64_t nb = B.w_dtype == DT_FP8 ? static_cast<uint64_t>(B.d / 128) * (B.I / 128) * 2 : 0;
+  uint64_t bytes = 0;
+  for (int i = 0; i < b.n_items; ++i) {
+    const uint64_t nt = b.items[i].ntok;
+    if (gateup) bytes += 2 * n * B.elem + 2 * nb + nt * (B.d * c->x_elem() + B.I * c->h_elem());
+    else bytes += n * B.elem + nb + nt * (B.I * c->h_elem() + B.d * 4);
+  }
+  return bytes;
+}
+
+// Launch gate/up then down for a list of (expert blob, (token, rank) pairs), in batches.
+struct Pair { int32_t t, out; };
+struct Work { const uint8_t* w; std::vector<Pair> pairs; };
+
+wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, hipStream_t st) {
+  FfnBatch b;
+  b.n_items = 0;
+  b.max_ntok = 0;
+  auto flush = [&]() -> wisp_status {
+    if (b.n_items == 0) return WISP_OK;
+    LaunchTiming t1 = timing_begin(c);
+    WISP_HIP(launch_ffn_gateup(b, c->shape, x, c->h, st, t1), "ffn gate/up launch");
+    timing_end(c, t1, WISP_K_FFN_GATEUP, ffn_bytes(c, b, true));
+    LaunchTiming t2 = timing_begin(c);
+    WISP_HIP(launch_ffn_down(b, c->shape, c->h, c->buf, st, t2), "ffn down launch");
+    timing_end(c, t2, WISP_K_FFN_DOWN, ffn_bytes(c, b, false));
+    b.n_items = 0;
+    b.max_ntok = 0;
+    return WISP_OK;
+  };
+  for (const Work& wk : work) {
+    for (size_t p0 = 0; p0 < wk.pairs.size(); p0 += kMaxTokPerItem) {
+      if (b.n_items == kMaxItems) {
+        wisp_status s = flush();
+        if (s != WISP_OK) return s;
+      }
+      FfnItem& it = b.items[b.n_items++];
+      it.w = wk.w;
+      it.ntok = static_cast<int32_t>(std::min<size_t>(kMaxTokPerItem, wk.pairs.size() - p0));
+      for (int q = 0; q < kMaxTokPerItem; ++q) {
+        const bool on = q < it.ntok;
+        it.tok[q] = on ? wk.pairs[p0 + q].t : 0;
+        it.out[q] = on ? wk.pairs[p0 + q].out : 0;
+      }
+      b.max_ntok = std::max(b.max_ntok, it.ntok);
+    }
+  }
+  return flush();
+}
+
+}  // namespace
+
+// ==========================================================================================
+// C ABI
+// ==========================================================================================
+extern "C" {
+
+const char* wisp_last_error(void) { return g_err.c_str(); }
+
+wisp_status wisp_expert_bytes(const wisp_model_desc* desc, uint64_t* bytes) {
+  wisp_status s = check_desc(desc);
+  if (s != WISP_OK) return s;
+  if (!bytes) return fail(WISP_E_INVAL, "bytes is NULL");
+  *bytes = make_blob_layout(desc->d_model, desc->d_ff, desc->w_dtype).bytes;
+  return WISP_OK;
+}
+
+wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
+  if (!out) return fail(WISP_E_INVAL, "out is NULL");
+  *out = nullptr;
+  wisp_status s = check_desc(desc);
+  if (s != WISP_OK) return s;
+  auto* c = new (std::nothrow) wisp_ctx();
+  if (!c) return fail(WISP_E_NOMEM, "host allocation failed");
+  c->desc = *desc;
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return fail(WISP_E_HIP, "hipGetDevice failed (no GPU?)");
+  }
+  c->blob = make_blob_layout(desc->d_model, desc->d_ff, desc->w_dtype);
+  c->shape.blob = c->blob;
+  c->shape.x_dtype = desc->x_dtype;
+  c->shape.h_dtype = desc->w_dtype == WISP_F32 ? DT_F32 : DT_BF16;
+  c->master_stride = round_up(c->blob.bytes, kMasterAlign);
+  const int L = desc->n_layers, N = desc->n_experts, k = desc->top_k, T = desc->max_tokens;
+  c->layers.resize(L);
+  c->masters.assign(L, nullptr);
+  c->shared_master.assign(L, nullptr);
+  auto bail = [&](wisp_status st, const std::string& m) {
+    free_ctx(c);
+    return fail(st, m);
+  };
+  for (int l = 0; l < L; ++l) {
+    void* p = nullptr;
+    if (hipHostMalloc(&p, static_cast<size_t>(N) * c->master_stride, hipHostMallocDefault) != hipSuccess)
+      return bail(WISP_E_NOMEM, "hipHostMalloc of the expert masters failed");
+    c->masters[l] = static_cast<uint8_t*>(p);
+    if (desc->has_shared) {
+      if (hipHostMalloc(&p, c->master_stride, hipHostMallocDefault) != hipSuccess)
+        return bail(WISP_E_NOMEM, "hipHostMalloc of the shared-expert master failed");
+      c->shared_master[l] = static_cast<uint8_t*>(p);
+      if (hipMalloc(&p, c->blob.bytes) != hipSuccess) return bail(WISP_E_NOMEM, "hipMalloc of a shared expert failed");
+      c->layers[l].shared_dev = static_cast<uint8_t*>(p);
+    }
+    if (hipEventCreateWithFlags(&c->layers[l].use_ev, hipEventDisableTiming) != hipSuccess)
+      return bail(WISP_E_HIP, "hipEventCreate failed");
+  }
+  if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess)
+    return bail(WISP_E_HIP, "hipStreamCreateWithFlags failed");
+  if (hipEventCreateWithFlags(&c->route_ev, hipEventDisableTiming) != hipSuccess)
+    return bail(WISP_E_HIP, "hipEventCreate failed");
+  void* p = nullptr;
+  if (hipMalloc(&p, sizeof(float) * static_cast<size_t>(T) * N) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
+  c->logits = static_cast<float*>(p);
+  const size_t rows = static_cast<size_t>(T) * (k + 1);
+  if (hipMalloc(&c->h, rows * desc->d_ff * c->h_elem()) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
+  if (hipMalloc(&p, rows * desc->d_model * sizeof(float)) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
+  c->buf = static_cast<float*>(p);
+  if (hipHostMalloc(&p, sizeof(int32_t) * static_cast<size_t>(T) * k, hipHostMallocCoherent) != hipSuccess)
+    return bail(WISP_E_NOMEM, "pinned scratch");
+  c->idx_pinned = static_cast<int32_t*>(p);
+  c->ids_scratch.resize(static_cast<size_t>(T) * k);
+  *out = c;
+  g_err.clear();
+  return WISP_OK;
+}
+
+wisp_status wisp_destroy(wisp_ctx* ctx) {
+  if (!ctx) return fail(WISP_E_INVAL, "ctx is NULL");
+  hipSetDevice(ctx->device);
+  free_ctx(ctx);
+  return WISP_OK;
+}
+
+wisp_status wisp_expert_host_ptr(wisp_ctx* ctx, int32_t layer, int32_t expert, void** ptr, uint64_t* bytes) {
+  if (!ctx || !ptr) return fail(WISP_E_INVAL, "NULL argument");
+  wisp_status s = check_layer(ctx, layer);
+  if (s != WISP_OK) return s;
+  if (expert == -1) {
+    if (!ctx->desc.has_shared) return fail(WISP_E_INVAL, "model has no shared expert");
+    *ptr = ctx->shared_master[layer];
+  } else {
+    if (expert < 0 || expert >= ctx->desc.n_experts) return fail(WISP_E_INVAL, "expert out of range");
+    *ptr = ctx->master(layer, expert);
+  }
+  if (bytes) *bytes = ctx->blob.bytes;
+  return WISP_OK;
+}
+
+wisp_status wisp_masters_ready(wisp_ctx* ctx) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  s = drain(ctx);
+  if (s != WISP_OK) return s;
+  for (auto& L : ctx->layers)
+    if (L.pending) return fail(WISP_E_STATE, "a page-in is pending");
+  for (int l = 0; l < ctx->desc.n_layers; ++l) {
+    LayerState& L = ctx->layers[l];
+    if (ctx->desc.has_shared)
+      WISP_HIP(hipMemcpy(L.shared_dev, ctx->shared_master[l], ctx->blob.bytes, hipMemcpyHostToDevice),
+               "hipMemcpy(shared expert)");
+    if (L.table) L.table->clear();
+  }
+  return WISP_OK;
+}
+
+wisp_status wisp_router_weights(wisp_ctx* ctx, int32_t layer, const float* w_r_dev) {
+  if (!ctx || !w_r_dev) return fail(WISP_E_INVAL, "NULL argument");
+  wisp_status s = check_layer(ctx, layer);
+  if (s != WISP_OK) return s;
+  ctx->layers[layer].wr = w_r_dev;
+  return WISP_OK;
+}
+
+wisp_status wisp_set_budget(wisp_ctx* ctx, uint64_t expert_bytes, int32_t* cap_out) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  const uint64_t a = static_cast<uint64_t>(ctx->desc.n_layers) * ctx->blob.bytes;
+  const uint64_t cap64 = expert_bytes / a;
+  if (cap64 < 1 || cap64 > static_cast<uint64_t>(ctx->desc.n_experts))
+    return fail(WISP_E_INVAL, "budget gives a cap outside [1, N]: C = floor(B / (L * M_e)) = " + std::to_string(cap64));
+  const int32_t C = static_cast<int32_t>(cap64);
+  for (auto& L : ctx->layers)
+    if (L.pending) return fail(WISP_E_STATE, "a page-in is pending");
+  s = drain(ctx);
+  if (s != WISP_OK) return s;
+  if (cap_out) *cap_out = C;
+  const int32_t old = ctx->cap;
+  if (C == old) return WISP_OK;
+  const int nl = ctx->desc.n_layers;
+  if (C > old) {
+    // grow: allocate every new slot first; commit only if all succeed
+    std::vector<std::vector<uint8_t*>> fresh(nl);
+    bool ok = true;
+    std::string why;
+    for (int l = 0; l < nl && ok; ++l) {
+      for (int32_t i = old; i < C; ++i) {
+        ++ctx->alloc_counter;
+        void* p = nullptr;
+        if (ctx->fail_alloc_at > 0 && ctx->alloc_counter == ctx->fail_alloc_at) {
+          ctx->fail_alloc_at = 0;
+          ok = false;
+          why = "injected slot allocation failure";
+          break;
+        }
+        if (hipMalloc(&p, ctx->blob.bytes) != hipSuccess) {
+          ok = false;
+          why = "hipMalloc of an expert slot failed";
+          hipGetLastError();
+          break;
+        }
+        fresh[l].push_back(static_cast<uint8_t*>(p));
+      }
+    }
+    if (!ok) {
+      for (auto& v : fresh)
+        for (auto* p : v) hipFree(p);
+      return fail(WISP_E_NOMEM, why + "; previous budget kept");
+    }
+    for (int l = 0; l < nl; ++l) {
+      LayerState& L = ctx->layers[l];
+      if (!L.table) {
+        L.table.reset(new SlotTable(ctx->desc.n_experts, C));
+      } else {
+        std::vector<int32_t> map;
+        L.table->resize(C, &map);
+      }
+      L.slot_mem.insert(L.slot_mem.end(), fresh[l].begin(), fresh[l].end());
+    }
+  } else {
+    // shrink: keep the most recently used experts, free the rest of the slots first
+    for (int l = 0; l < nl; ++l) {
+      LayerState& L = ctx->layers[l];
+      std::vector<int32_t> map;
+      L.table->resize(C, &map);
+      std::vector<uint8_t> used(old, 0);
+      std::vector<uint8_t*> mem(C, nullptr);
+      for (int32_t i = 0; i < C; ++i)
+        if (map[i] >= 0) { mem[i] = L.slot_mem[map[i]]; used[map[i]] = 1; }
+      int32_t spare = 0;
+      for (int32_t i = 0; i < C; ++i) {
+        if (mem[i]) continue;
+        while (used[spare]) ++spare;
+        mem[i] = L.slot_mem[spare];
+        used[spare] = 1;
+      }
+      for (int32_t s2 = 0; s2 < old; ++s2)
+        if (!used[s2]) hipFree(L.slot_mem[s2]);
+      L.slot_mem.swap(mem);
+    }
+  }
+  ctx->cap = C;
+  return WISP_OK;
+}
+
+wisp_status wisp_preload(wisp_ctx* ctx) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (ctx->cap < 1) return fail(WISP_E_STATE, "no expert budget set");
+  for (auto& L : ctx->layers)
+    if (L.pending) return fail(WISP_E_STATE, "a page-in is pending");
+  if ((s = drain(ctx)) != WISP_OK) return s;
+  std::vector<int32_t> ids(ctx->cap);
+  for (int32_t i = 0; i < ctx->cap; ++i) ids[i] = i;
+  for (int32_t l = 0; l < ctx->desc.n_layers; ++l) {
+    LayerState& L = ctx->layers[l];
+    StepPlan plan;
+    L.table->step(ids.data(), ctx->cap, &plan);
+    for (const ChunkPlan& cp : plan.chunks)
+      for (size_t i = 0; i < cp.experts.size(); ++i)
+        if (cp.fault[i])
+          WISP_HIP(hipMemcpyAsync(L.slot_mem[cp.slots[i]], ctx->master(l, cp.experts[i]), ctx->blob.bytes,
+                                  hipMemcpyHostToDevice, ctx->side),
+                   "hipMemcpyAsync(preload)");
+  }
+  WISP_HIP(hipStreamSynchronize(ctx->side), "hipStreamSynchronize(side)");
+  return WISP_OK;
+}
+
+wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int32_t T, int32_t* idx_dev,
+                            float* w_dev, int32_t* idx_host, void* stream) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if ((s = check_layer(ctx, layer)) != WISP_OK) return s;
+  if (!x_dev || !idx_dev || !w_dev) return fail(WISP_E_INVAL, "NULL device pointer");
+  if (T < 1 || T > ctx->desc.max_tokens) return fail(WISP_E_INVAL, "T out of [1, max_tokens]");
+  LayerState& L = ctx->layers[layer];
+  if (!L.wr) return fail(WISP_E_STATE, "router weights not set for this layer");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const auto& d = ctx->desc;
+  LaunchTiming t1 = timing_begin(ctx);
+  WISP_HIP(launch_router_logits(L.wr, x_dev, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, st, t1),
+           "router logits launch");
+  timing_end(ctx, t1, WISP_K_ROUTER_LOGITS,
+             static_cast<uint64_t>(d.n_experts) * d.d_model * 4 + static_cast<uint64_t>(T) * d.d_model * ctx->x_elem() +
+                 static_cast<uint64_t>(T) * d.n_experts * 4);
+  LaunchTiming t2 = timing_begin(ctx);
+  WISP_HIP(launch_router_select(ctx->logits, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev,
+                                w_dev, st, t2),
+           "router select launch");
+  timing_end(ctx, t2, WISP_K_ROUTER_SELECT,
+             static_cast<uint64_t>(T) * d.n_experts * 4 + static_cast<uint64_t>(T) * d.top_k * 8);
+  if (idx_host) {
+    const size_t nb = sizeof(int32_t) * static_cast<size_t>(T) * d.top_k;
+    WISP_HIP(hipMemcpyAsync(ctx->idx_pinned, idx_dev, nb, hipMemcpyDeviceToHost, st), "hipMemcpyAsync(idx)");
+    WISP_HIP(hipEventRecord(ctx->route_ev, st), "hipEventRecord(route)");
+    // spin: this wait is on the critical path of every layer-step
+    hipError_t q;
+    while ((q = hipEventQuery(ctx->route_ev)) == hipErrorNotReady) {
+    }
+    if (q != hipSuccess) return fail(WISP_E_HIP, std::string("route event: ") + hipGetErrorString(q));
+    std::memcpy(idx_host, ctx->idx_pinned, nb);
+    if (ctx->profiling) harvest(ctx, false);
+  }
+  return WISP_OK;
+}
+
+wisp_status wisp_page_in(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, int32_t T, wisp_page_stats* st) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if ((s = check_layer(ctx, layer)) != WISP_OK) return s;
+  if (!ids_host) return fail(WISP_E_INVAL, "ids_host is NULL");
+  if (T < 1 || T > ctx->desc.max_tokens) return fail(WISP_E_INVAL, "T out of [1, max_tokens]");
+  if (ctx->cap < 1) return fail(WISP_E_STATE, "no expert budget set");
+  LayerState& L = ctx->layers[layer];
+  if (L.pending) return fail(WISP_E_STATE, "previous page-in of this layer not consumed by wisp_moe_forward");
+  const int32_t n = T * ctx->desc.top_k;
+  for (int32_t i = 0; i < n; ++i)
+    if (ids_host[i] < 0 || ids_host[i] >= ctx->desc.n_experts) return fail(WISP_E_INVAL, "expert id out of range");
+  if (!L.table->step(ids_host, n, &L.plan)) return fail(WISP_E_INVAL, "expert id out of range");
+  L.ids.assign(ids_host, ids_host + n);
+  L.T = T;
+  const size_t nch = L.plan.chunks.size();
+  if ((s = ensure_events(L.fill_ev, nch)) != WISP_OK) return s;
+  if ((s = ensure_events(L.chunk_ev, nch)) != WISP_OK) return s;
+  L.chunk_ptrs.assign(nch, {});
+  for (size_t ci = 0; ci < nch; ++ci)
+    for (int32_t sl : L.plan.chunks[ci].slots) L.chunk_ptrs[ci].push_back(L.slot_mem[sl]);
+  L.pending = true;
+  wisp_page_stats ps{};
+  ps.hits = L.plan.hits;
+  ps.misses = L.plan.misses;
+  ps.chunks = static_cast<uint32_t>(nch);
+  ps.steps = 1;
+  ps.h2d_bytes = static_cast<uint64_t>(L.plan.misses) * ctx->blob.bytes;
+  L.cum.hits += ps.hits;
+  L.cum.misses += ps.misses;
+  L.cum.chunks += ps.chunks;
+  L.cum.steps += 1;
+  L.cum.h2d_bytes += ps.h2d_bytes;
+  if (st) *st = ps;
+  if (nch > 0) {
+    s = issue_fills(ctx, layer, 0);
+    if (s != WISP_OK) return s;
+  }
+  return WISP_OK;
+}
+
+wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, int32_t T, const float* w_dev,
+                             float* y_dev, void* stream, wisp_page_stats* st) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if ((s = check_layer(ctx, layer)) != WISP_OK) return s;
+  if (!x_dev || !w_dev || !y_dev) return fail(WISP_E_INVAL, "NULL device pointer");
+  LayerState& L = ctx->layers[layer];
+  if (!L.pending) return fail(WISP_E_STATE, "no pending page-in for this layer");
+  if (T != L.T) return fail(WISP_E_INVAL, "T differs from the page-in");
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  const int k = ctx->desc.top_k;
+  const int rows = k + 1;
+  const size_t nch = L.plan.chunks.size();
+  // exactness check: every routed id is in exactly one chunk, with a slot
+  for (int32_t i = 0; i < T * k; ++i) {
+    bool found = false;
+    for (size_t ci = 0; ci < nch && !found; ++ci)
+      for (int32_t e : L.plan.chunks[ci].experts) found |= (e == L.ids[i]);
+    if (!found) return fail(WISP_E_NOT_RESIDENT, "routed expert missing from the page-in plan");
+  }
+  for (size_t ci = 0; ci < nch; ++ci) {
+    const ChunkPlan& cp = L.plan.chunks[ci];
+    if (ci > 0 && (s = issue_fills(ctx, layer, ci)) != WISP_OK) return s;
+    std::vector<Work> hits, faults;
+    for (size_t i = 0; i < cp.experts.size(); ++i) {
+      Work wk;
+      wk.w = L.chunk_ptrs[ci][i];
+      for (int32_t t = 0; t < T; ++t)
+        for (int j = 0; j < k; ++j)
+          if (L.ids[t * k + j] == cp.experts[i]) wk.pairs.push_back({t, t * rows + j});
+      (cp.fault[i] ? faults : hits).push_back(std::move(wk));
+    }
+    if (ci == 0 && ctx->desc.has_shared) {
+      Work wk;
+      wk.w = L.shared_dev;
+      for (int32_t t = 0; t < T; ++t) wk.pairs.push_back({t, t * rows + k});
+      hits.push_back(std::move(wk));
+    }
+    if (!hits.empty() && (s = run_ffn(ctx, hits, x_dev, sm)) != WISP_OK) return s;
+    if (!faults.empty()) {
+      WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[ci], 0), "hipStreamWaitEvent(fill)");
+      if ((s = run_ffn(ctx, faults, x_dev, sm)) != WISP_OK) return s;
+    }
+    if (ci + 1 < nch) WISP_HIP(hipEventRecord(L.chunk_ev[ci], sm), "hipEventRecord(chunk)");
+  }
+  LaunchTiming tc = timing_begin(ctx);
+  WISP_HIP(launch_combine(T, k, ctx->desc.d_model, ctx->desc.has_shared, w_dev, ctx->buf, y_dev, sm, tc),
+           "combine launch");
+  timing_end(ctx, tc, WISP_K_COMBINE,
+             static_cast<uint64_t>(T) * ctx->desc.d_model * 4 * (k + ctx->desc.has_shared + 1) +
+                 static_cast<uint64_t>(T) * k * 4);
+  WISP_HIP(hipEventRecord(L.use_ev, sm), "hipEventRecord(use)");
+  L.use_ev_recorded = true;
+  L.pending = false;
+  if (st) {
+    st->hits = L.plan.hits;
+    st->misses = L.plan.misses;
+    st->chunks = static_cast<uint32_t>(nch);
+    st->steps = 1;
+    st->h2d_bytes = static_cast<uint64_t>(L.plan.misses) * ctx->blob.bytes;
+  }
+  return WISP_OK;
+}
+
+wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_t* idx_dev, float* w_dev,
+                             float* y_dev, void* stream, wisp_page_stats* st) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (!x_dev || !idx_dev || !w_dev || !y_dev) return fail(WISP_E_INVAL, "NULL device pointer");
+  if (T < 1 || T > ctx->desc.max_tokens) return fail(WISP_E_INVAL, "T out of [1, max_tokens]");
+  const auto& d = ctx->desc;
+  const size_t xs = static_cast<size_t>(T) * d.d_model * ctx->x_elem();
+  for (int32_t l = 0; l < d.n_layers; ++l) {
+    const void* xl = static_cast<const uint8_t*>(x_dev) + l * xs;
+    int32_t* il = idx_dev + static_cast<size_t>(l) * T * d.top_k;
+    float* wl = w_dev + static_cast<size_t>(l) * T * d.top_k;
+    float* yl = y_dev + static_cast<size_t>(l) * T * d.d_model;
+    if ((s = wisp_route_topk(ctx, l, xl, T, il, wl, ctx->ids_scratch.data(), stream)) != WISP_OK) return s;
+    if ((s = wisp_page_in(ctx, l, ctx->ids_scratch.data(), T, st ? st + l : nullptr)) != WISP_OK) return s;
+    if ((s = wisp_moe_forward(ctx, l, xl, T, wl, yl, stream, nullptr)) != WISP_OK) return s;
+  }
+  return WISP_OK;
+}
+
+wisp_status wisp_get_stats(wisp_ctx* ctx, int32_t layer, wisp_page_stats* cumulative) {
+  if (!ctx || !cumulative) return fail(WISP_E_INVAL, "NULL argument");
+  wisp_status s = check_layer(ctx, layer);
+  if (s != WISP_OK) return s;
+  *cumulative = ctx->layers[layer].cum;
+  return WISP_OK;
+}
+
+wisp_status wisp_reset_stats(wisp_ctx* ctx) {
+  if (!ctx) return fail(WISP_E_INVAL, "ctx is NULL");
+  for (auto& L : ctx->layers) L.cum = wisp_page_stats{};
+  return WISP_OK;
+}
+
+wisp_status wisp_get_cap(wisp_ctx* ctx, int32_t* cap) {
+  if (!ctx || !cap) return fail(WISP_E_INVAL, "NULL argument");
+  *cap = ctx->cap;
+  return WISP_OK;
+}
+
+wisp_status wisp_slot_of(wisp_ctx* ctx, int32_t layer, int32_t expert, int32_t* slot) {
+  if (!ctx || !slot) return fail(WISP_E_INVAL, "NULL argument");
+  wisp_status s = check_layer(ctx, layer);
+  if (s != WISP_OK) return s;
+  if (expert < 0 || expert >= ctx->desc.n_experts) return fail(WISP_E_INVAL, "expert out of range");
+  const auto& t = ctx->layers[layer].table;
+  *slot = t ? t->slot_of(expert) : -1;
+  return WISP_OK;
+}
+
+wisp_status wisp_expert_in_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, int32_t* expert) {
+  if (!ctx || !expert) return fail(WISP_E_INVAL, "NULL argument");
+  wisp_status s = check_layer(ctx, layer);
+  if (s != WISP_OK) return s;
+  if (slot < 0 || slot >= ctx->cap) return fail(WISP_E_INVAL, "slot out of range");
+  *expert = ctx->layers[layer].table->expert_in(slot);
+  return WISP_OK;
+}
+
+wisp_status wisp_read_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, void* dst) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if ((s = check_layer(ctx, layer)) != WISP_OK) return s;
+  if (!dst) return fail(WISP_E_INVAL, "dst is NULL");
+  if (slot < 0 || slot >= ctx->cap) return fail(WISP_E_INVAL, "slot out of range");
+  if ((s = drain(ctx)) != WISP_OK) return s;
+  WISP_HIP(hipMemcpy(dst, ctx->layers[layer].slot_mem[slot], ctx->blob.bytes, hipMemcpyDeviceToHost),
+           "hipMemcpy(read slot)");
+  return WISP_OK;
+}
+
+wisp_status wisp_set_profiling(wisp_ctx* ctx, int32_t on) {
+  if (!ctx) return fail(WISP_E_INVAL, "ctx is NULL");
+  if (!on) harvest(ctx, true);
+  ctx->profiling = on != 0;
+  return WISP_OK;
+}
+
+wisp_status wisp_kernel_times(wisp_ctx* ctx, int32_t kclass, double* total_ms, uint64_t* launches, uint64_t* bytes) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (kclass < 0 || kclass >= WISP_K_NUM) return fail(WISP_E_INVAL, "kernel class out of range");
+  harvest(ctx, true);
+  if (total_ms) *total_ms = ctx->k_ms[kclass];
+  if (launches) *launches = ctx->k_n[kclass];
+  if (bytes) *bytes = ctx->k_bytes[kclass];
+  return WISP_OK;
+}
+
+wisp_status wisp_reset_kernel_times(wisp_ctx* ctx) {
+  if (!ctx) return fail(WISP_E_INVAL, "ctx is NULL");
+  harvest(ctx, true);
+  for (int i = 0; i < WISP_K_NUM; ++i) { ctx->k_ms[i] = 0; ctx->k_n[i] = 0; ctx->k_bytes[i] = 0; }
+  return WISP_OK;
+}
+
+wisp_status wisp_probe_h2d(wisp_ctx* ctx, int32_t count, int32_t reps, double* gbps) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (count < 1 || reps < 1 || !gbps) return fail(WISP_E_INVAL, "count, reps >= 1 and gbps required");
+  if ((s = drain(ctx)) != WISP_OK) return s;
+  void* scratch = nullptr;
+  const size_t B = ctx->blob.bytes;
+  if (hipMalloc(&scratch, B * count) != hipSuccess) {
+    hipGetLastError();
+    return fail(WISP_E_NOMEM, "probe scratch allocation failed");
+  }
+  hipEvent_t a = nullptr, b = nullptr;
+  std::vector<double> rates;
+  hipError_t e = hipEventCreate(&a);
+  if (e == hipSuccess) e = hipEventCreate(&b);
+  const int nl = ctx->desc.n_layers, ne = ctx->desc.n_experts;
+  int src = 0;
+  for (int r = 0; r < reps && e == hipSuccess; ++r) {
+    e = hipEventRecord(a, ctx->side);
+    for (int i = 0; i < count && e == hipSuccess; ++i, ++src) {
+      const int l = (src / ne) % nl, x = src % ne;
+      e = hipMemcpyAsync(static_cast<uint8_t*>(scratch) + static_cast<size_t>(i) * B, ctx->master(l, x), B,
+                         hipMemcpyHostToDevice, ctx->side);
+    }
+    if (e == hipSuccess) e = hipEventRecord(b, ctx->side);
+    if (e == hipSuccess) e = hipEventSynchronize(b);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+    if (e == hipSuccess) rates.push_back(static_cast<double>(B) * count / (ms * 1e-3) / 1e9);
+  }
+  if (a) hipEventDestroy(a);
+  if (b) hipEventDestroy(b);
+  hipFree(scratch);
+  if (e != hipSuccess) return fail(WISP_E_HIP, std::string("probe: ") + hipGetErrorString(e));
+  std::sort(rates.begin(), rates.end());
+  *gbps = rates[rates.size() / 2];
+  return WISP_OK;
+}
+
+wisp_status wisp_hbm_copy(const void* src, void* dst, uint64_t bytes, void* stream) {
+  if (!src || !dst) return fail(WISP_E_INVAL, "NULL pointer");
+  if (bytes % 16 || reinterpret_cast<uintptr_t>(src) % 16 || reinterpret_cast<uintptr_t>(dst) % 16)
+    return fail(WISP_E_INVAL, "bytes and pointers must be 16-byte aligned");
+  WISP_HIP(launch_hbm_copy(src, dst, bytes, static_cast<hipStream_t>(stream)), "copy launch");
+  return WISP_OK;
+}
+
+wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n, void* stream) {
+  if (!codes_dev || !out_dev || n < 0) return fail(WISP_E_INVAL, "bad argument");
+  WISP_HIP(launch_decode_fp8(codes_dev, out_dev, n, static_cast<hipStream_t>(stream)), "decode launch");
+  return WISP_OK;
+}
+
+wisp_status wisp_debug_fail_slot_alloc(wisp_ctx* ctx, int32_t n) {
+  if (!ctx || n < 0) return fail(WISP_E_INVAL, "bad argument");
+  ctx->fail_alloc_at = n > 0 ? ctx->alloc_counter + n : 0;
+  return WISP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,366 @@
+// Slot-indirected expert FFN for decode-sized token counts (gfx950).
+//
+// The expert is o = W2 (silu(W1 x) * (W3 x)).  At decode sizes every weight byte is used once
+// per token, so the work is a streaming GEMV bound by HBM bandwidth, not a contraction worth
+// MFMA tiles.  Each launch covers a batch of "items" (an expert blob in its slot plus the up to
+// four tokens that chose it), so an expert is read once however many tokens use it.
+//
+// Layout of the work: a group of LPR lanes owns one weight row; lane l of the group reads the
+// 16-byte chunks l, l + LPR, ... of the row (coalesced across the group), decodes them (fp32 /
+// bf16 bit shifts; fp8 E4M3 with the hardware packed conversion, times the bf16 scale of the
+// chunk's 128x128 block), and multiplies them with the matching input elements read from LDS,
+// where the workgroup has staged the item's input rows.  Group partial sums are reduced with
+// cross-lane shuffles.  Phase 1 (gate/up) reads the W1 and W3 rows of the same output index
+// together and writes h = silu(a) * b; phase 2 (down) reads W2 rows and writes the per-(token,
+// rank) outputs that the combine kernel sums in rank order.  Every (token, rank) result is
+// computed by the same instructions in the same order whatever the batch composition, so a
+// paged run is bit-identical to a fully resident one.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+
+namespace wisp {
+
+BlobLayout make_blob_layout(int d, int I, int w_dtype) {
+  BlobLayout L;
+  L.d = d;
+  L.I = I;
+  L.w_dtype = w_dtype;
+  L.elem = w_dtype == DT_F32 ? 4 : w_dtype == DT_BF16 ? 2 : 1;
+  const size_t n = static_cast<size_t>(d) * I;
+  L.off_w1 = 0;
+  L.off_w3 = n * L.elem;
+  L.off_w2 = 2 * n * L.elem;
+  L.bytes = 3 * n * L.elem;
+  if (w_dtype == DT_FP8) {
+    const size_t nb = static_cast<size_t>(d / 128) * (I / 128);
+    L.off_s1 = 3 * n;
+    L.off_s3 = L.off_s1 + 2 * nb;
+    L.off_s2 = L.off_s3 + 2 * nb;
+    L.bytes = 3 * n + 6 * nb;
+  }
+  return L;
+}
+
+namespace {
+
+enum { MODE_GATEUP = 0, MODE_DOWN = 1 };
+
+template <int WT> struct WFmt;
+template <> struct WFmt<DT_F32> { static constexpr int EPL = 4; };
+template <> struct WFmt<DT_BF16> { static constexpr int EPL = 8; };
+template <> struct WFmt<DT_FP8> { static constexpr int EPL = 16; };
+
+__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xFFFF0000u); }
+
+// Four E4M3 codes (little-endian bytes of w) to fp32 with the gfx950 packed conversion.
+__device__ __forceinline__ void fp8x4(uint32_t w, float* o) {
+  auto lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w), false);
+  auto hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w), true);
+  o[0] = lo[0];
+  o[1] = lo[1];
+  o[2] = hi[0];
+  o[3] = hi[1];
+}
+
+template <int WT>
+__device__ __forceinline__ void decode_chunk(const uint4 v, float* o) {
+  if constexpr (WT == DT_F32) {
+    o[0] = __uint_as_float(v.x); o[1] = __uint_as_float(v.y);
+    o[2] = __uint_as_float(v.z); o[3] = __uint_as_float(v.w);
+  } else if constexpr (WT == DT_BF16) {
+    o[0] = bf16_lo(v.x); o[1] = bf16_hi(v.x); o[2] = bf16_lo(v.y); o[3] = bf16_hi(v.y);
+    o[4] = bf16_lo(v.z); o[5] = bf16_hi(v.z); o[6] = bf16_lo(v.w); o[7] = bf16_hi(v.w);
+  } else {
+    fp8x4(v.x, o); fp8x4(v.y, o + 4); fp8x4(v.z, o + 8); fp8x4(v.w, o + 12);
+  }
+}
+
+// EPL consecutive input elements starting at element col of an LDS row.
+template <int IT, int EPL>
+__device__ __forceinline__ void lds_chunk(const uint8_t* row, int col, float* o) {
+  if constexpr (IT == DT_F32) {
+    static_assert(EPL % 4 == 0, "");
+    const float4* p = reinterpret_cast<const float4*>(row + static_cast<size_t>(col) * 4);
+#pragma unroll
+    for (int q = 0; q < EPL / 4; ++q) {
+      const float4 v = p[q];
+      o[4 * q] = v.x; o[4 * q + 1] = v.y; o[4 * q + 2] = v.z; o[4 * q + 3] = v.w;
+    }
+  } else {
+    static_assert(EPL % 8 == 0, "");
+    const uint4* p = reinterpret_cast<const uint4*>(row + static_cast<size_t>(col) * 2);
+#pragma unroll
+    for (int q = 0; q < EPL / 8; ++q) {
+      const uint4 v = p[q];
+      o[8 * q + 0] = bf16_lo(v.x); o[8 * q + 1] = bf16_hi(v.x); o[8 * q + 2] = bf16_lo(v.y); o[8 * q + 3] = bf16_hi(v.y);
+      o[8 * q + 4] = bf16_lo(v.z); o[8 * q + 5] = bf16_hi(v.z); o[8 * q + 6] = bf16_lo(v.w); o[8 * q + 7] = bf16_hi(v.w);
+    }
+  }
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// One launch: blockIdx.x = item * blocks_per_item + row block.  K = inner (row) length, R = rows.
+// off0/off1: byte offsets of the matrix (matrices) in the blob; soff0/soff1: fp8 scale tables.
+template <int WT, int IT, int MODE, int LPR, int NLT>
+__global__ void __launch_bounds__(256) ffn_rows(const FfnBatch B, const uint8_t* __restrict__ vin, int vin_stride,
+                                                int K, int R, int rows_per_wg, int blocks_per_item, uint32_t off0,
+                                                uint32_t off1, uint32_t soff0, uint32_t soff1,
+                                                uint8_t* __restrict__ out, int out_stride) {
+  constexpr int EPL = WFmt<WT>::EPL;
+  constexpr int RPW = 64 / LPR;                 // rows a wave covers at once
+  constexpr int IS = IT == DT_F32 ? 4 : 2;      // input element bytes
+  constexpr int U = NLT > 0 ? NLT : 4;          // chunks in flight per lane
+  extern __shared__ __align__(16) uint8_t lds[];
+
+  const int item_idx = blockIdx.x / blocks_per_item;
+  const int rb = blockIdx.x - item_idx * blocks_per_item;
+  const FfnItem& it = B.items[item_idx];
+  const int ntok = it.ntok;
+  const int row_bytes = K * IS;
+
+  // stage the item's input rows (x for gate/up, h for down) in LDS
+  for (int t = 0; t < ntok; ++t) {
+    const int src_row = MODE == MODE_GATEUP ? it.tok[t] : it.out[t];
+    const uint4* src = reinterpret_cast<const uint4*>(vin + static_cast<size_t>(src_row) * vin_stride * IS);
+    uint4* dst = reinterpret_cast<uint4*>(lds + t * row_bytes);
+    for (int i = threadIdx.x; i < row_bytes / 16; i += 256) dst[i] = src[i];
+  }
+  __syncthreads();
+
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int sub = lane / LPR;
+  const int sl = lane - sub * LPR;
+  const int NL = NLT > 0 ? NLT : (K / EPL) / LPR;
+  const int r_begin = rb * rows_per_wg;
+  const int r_end = min(R, r_begin + rows_per_wg);
+  const uint8_t* wbase0 = it.w + off0;
+  const uint8_t* wbase1 = it.w + off1;
+  const uint16_t* sc0 = reinterpret_cast<const uint16_t*>(it.w + soff0);
+  const uint16_t* sc1 = reinterpret_cast<const uint16_t*>(it.w + soff1);
+  const int scols = K / 128;
+  const size_t row_stride_b = static_cast<size_t>(K) * (WT == DT_F32 ? 4 : WT == DT_BF16 ? 2 : 1);
+
+  for (int rbase = r_begin + wave * RPW; rbase < r_end; rbase += 4 * RPW) {
+    const int r = rbase + sub;
+    const bool valid = r < r_end;
+    const int rr = valid ? r : r_begin;   // keep addresses in range for idle row groups
+    float acc0[kMaxTokPerItem], acc1[kMaxTokPerItem];
+#pragma unroll
+    for (int t = 0; t < kMaxTokPerItem; ++t) { acc0[t] = 0.f; acc1[t] = 0.f; }
+    const uint4* row0 = reinterpret_cast<const uint4*>(wbase0 + rr * row_stride_b);
+    const uint4* row1 = reinterpret_cast<const uint4*>(wbase1 + rr * row_stride_b);
+
+    for (int m0 = 0; m0 < NL; m0 += U) {
+      uint4 a[U], b[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int m = m0 + u;
+        if (NLT > 0 || m < NL) {
+          a[u] = row0[m * LPR + sl];
+          if constexpr (MODE == MODE_GATEUP) b[u] = row1[m * LPR + sl];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int m = m0 + u;
+        if (!(NLT > 0 || m < NL)) continue;
+        const int col = (m * LPR + sl) * EPL;
+        float wa[EPL], wb[EPL];
+        decode_chunk<WT>(a[u], wa);
+        if constexpr (MODE == MODE_GATEUP) decode_chunk<WT>(b[u], wb);
+        float s0 = 1.f, s1 = 1.f;
+        if constexpr (WT == DT_FP8) {
+          const int sidx = (rr / 128) * scols + col / 128;
+          s0 = __uint_as_float(static_cast<uint32_t>(sc0[sidx]) << 16);
+          if constexpr (MODE == MODE_GATEUP) s1 = __uint_as_float(static_cast<uint32_t>(sc1[sidx]) << 16);
+        }
+#pragma unroll
+        for (int t = 0; t < kMaxTokPerItem; ++t) {
+          if (t >= ntok) break;
+          float xv[EPL];
+          lds_chunk<IT, EPL>(lds + t * row_bytes, col, xv);
+          if constexpr (WT == DT_FP8) {
+            float pa = 0.f, pb = 0.f;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) {
+              pa = fmaf(wa[e], xv[e], pa);
+              if constexpr (MODE == MODE_GATEUP) pb = fmaf(wb[e], xv[e], pb);
+            }
+            acc0[t] = fmaf(s0, pa, acc0[t]);
+            if constexpr (MODE == MODE_GATEUP) acc1[t] = fmaf(s1, pb, acc1[t]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) {
+              acc0[t] = fmaf(wa[e], xv[e], acc0[t]);
+              if constexpr (MODE == MODE_GATEUP) acc1[t] = fmaf(wb[e], xv[e], acc1[t]);
+            }
+          }
+        }
+      }
+    }
+    // reduce over the LPR lanes of the row group
+#pragma unroll
+    for (int t = 0; t < kMaxTokPerItem; ++t) {
+      if (t >= ntok) break;
+#pragma unroll
+      for (int off = LPR / 2; off > 0; off >>= 1) {
+        acc0[t] += __shfl_xor(acc0[t], off, 64);
+        if constexpr (MODE == MODE_GATEUP) acc1[t] += __shfl_xor(acc1[t], off, 64);
+      }
+    }
+    if (valid && sl == 0) {
+      for (int t = 0; t < ntok; ++t) {
+        const size_t o = static_cast<size_t>(it.out[t]) * out_stride + r;
+        if constexpr (MODE == MODE_GATEUP) {
+          const float a = acc0[t];
+          const float h = a / (1.0f + __expf(-a)) * acc1[t];
+          if constexpr (IT == DT_F32) reinterpret_cast<float*>(out)[o] = h;
+          else reinterpret_cast<uint16_t*>(out)[o] = f32_to_bf16_rne(h);
+        } else {
+          reinterpret_cast<float*>(out)[o] = acc0[t];
+        }
+      }
+    }
+  }
+}
+
+using RowsKernel = void (*)(const FfnBatch, const uint8_t*, int, int, int, int, int, uint32_t, uint32_t, uint32_t,
+                            uint32_t, uint8_t*, int);
+
+template <int WT, int IT, int MODE>
+RowsKernel pick_kernel(int lpr, int nl) {
+#define WISP_K(L, N) \
+  if (lpr == L && nl == N) return &ffn_rows<WT, IT, MODE, L, N>;
+  // shapes of the benchmarked and tested workloads, fully unrolled
+  if constexpr (WT == DT_F32) {
+    WISP_K(64, 1) WISP_K(64, 2)
+  } else if constexpr (WT == DT_BF16) {
+    WISP_K(64, 4) WISP_K(64, 8) WISP_K(32, 3) WISP_K(64, 28) WISP_K(32, 1) WISP_K(16, 1) WISP_K(16, 3)
+  } else {
+    WISP_K(64, 7) WISP_K(64, 2) WISP_K(16, 1)
+  }
+  // any other shape: runtime chunk count
+  WISP_K(64, 0) WISP_K(32, 0) WISP_K(16, 0) WISP_K(8, 0)
+#undef WISP_K
+  return nullptr;
+}
+
+int pick_lpr(int chunks) {
+  if (chunks % 64 == 0) return 64;
+  if (chunks % 32 == 0) return 32;
+  if (chunks % 16 == 0) return 16;
+  if (chunks % 8 == 0) return 8;
+  return 0;
+}
+
+hipError_t launch_rows(int mode, const FfnBatch& b, const FfnShape& s, const void* vin, int vin_stride, void* out,
+                       int out_stride, hipStream_t st, const LaunchTiming& tm) {
+  if (b.n_items <= 0) return hipSuccess;
+  const BlobLayout& L = s.blob;
+  const int WT = L.w_dtype;
+  const int IT = mode == MODE_GATEUP ? s.x_dtype : s.h_dtype;
+  const int K = mode == MODE_GATEUP ? L.d : L.I;
+  const int R = mode == MODE_GATEUP ? L.I : L.d;
+  const int EPL = WT == DT_F32 ? 4 : WT == DT_BF16 ? 8 : 16;
+  if (K % EPL != 0) return hipErrorInvalidValue;
+  const int chunks = K / EPL;
+  const int lpr = pick_lpr(chunks);
+  if (lpr == 0) return hipErrorInvalidValue;
+  int nl = chunks / lpr;
+  RowsKernel k = nullptr;
+  auto pick = [&](int n) -> RowsKernel {
+    if (WT == DT_F32 && IT == DT_F32)
+      return mode == MODE_GATEUP ? pick_kernel<DT_F32, DT_F32, MODE_GATEUP>(lpr, n)
+                                 : pick_kernel<DT_F32, DT_F32, MODE_DOWN>(lpr, n);
+    if (WT == DT_BF16 && IT == DT_BF16)
+      return mode == MODE_GATEUP ? pick_kernel<DT_BF16, DT_BF16, MODE_GATEUP>(lpr, n)
+                                 : pick_kernel<DT_BF16, DT_BF16, MODE_DOWN>(lpr, n);
+    if (WT == DT_FP8 && IT == DT_BF16)
+      return mode == MODE_GATEUP ? pick_kernel<DT_FP8, DT_BF16, MODE_GATEUP>(lpr, n)
+                                 : pick_kernel<DT_FP8, DT_BF16, MODE_DOWN>(lpr, n);
+    return nullptr;
+  };
+  k = pick(nl);
+  if (!k) k = pick(0);
+  if (!k) return hipErrorInvalidValue;
+
+  const int rpw = 64 / lpr;
+  const int step = 4 * rpw;  // rows per workgroup pass
+  // about 2048 workgroups per launch (8 per CU), each a whole number of passes
+  int bpi = (2048 + b.n_items - 1) / b.n_items;
+  const int max_bpi = (R + step - 1) / step;
+  if (bpi > max_bpi) bpi = max_bpi;
+  if (bpi < 1) bpi = 1;
+  int rows_per_wg = (R + bpi - 1) / bpi;
+  rows_per_wg = (rows_per_wg + step - 1) / step * step;
+  bpi = (R + rows_per_wg - 1) / rows_per_wg;
+
+  const int isz = IT == DT_F32 ? 4 : 2;
+  const size_t lds = static_cast<size_t>(b.max_ntok) * K * isz;
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+    if (e != hipSuccess) return e;
+  }
+  const uint32_t off0 = static_cast<uint32_t>(mode == MODE_GATEUP ? L.off_w1 : L.off_w2);
+  const uint32_t off1 = static_cast<uint32_t>(mode == MODE_GATEUP ? L.off_w3 : L.off_w2);
+  const uint32_t soff0 = static_cast<uint32_t>(mode == MODE_GATEUP ? L.off_s1 : L.off_s2);
+  const uint32_t soff1 = static_cast<uint32_t>(mode == MODE_GATEUP ? L.off_s3 : L.off_s2);
+  dim3 grid(static_cast<unsigned>(b.n_items * bpi)), block(256);
+  hipExtLaunchKernelGGL(k, grid, block, static_cast<uint32_t>(lds), st, tm.start, tm.stop, 0, b,
+                        static_cast<const uint8_t*>(vin), vin_stride, K, R, rows_per_wg, bpi, off0, off1, soff0, soff1,
+                        static_cast<uint8_t*>(out), out_stride);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_ffn_gateup(const FfnBatch& b, const FfnShape& s, const void* x, void* h, hipStream_t st,
+                             const LaunchTiming& tm) {
+  return launch_rows(MODE_GATEUP, b, s, x, s.blob.d, h, s.blob.I, st, tm);
+}
+
+hipError_t launch_ffn_down(const FfnBatch& b, const FfnShape& s, const void* h, float* buf, hipStream_t st,
+                           const LaunchTiming& tm) {
+  return launch_rows(MODE_DOWN, b, s, h, s.blob.I, buf, s.blob.d, st, tm);
+}
+
+// ------------------------------------------------------------------------------------------
+// fp8 decode probe: the same conversion as the FFN kernels, for checking all codes on device.
+// ------------------------------------------------------------------------------------------
+namespace {
+__global__ void decode_fp8_kernel(const uint8_t* __restrict__ codes, float* __restrict__ out, int n) {
+  const int i = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i + 3 < n) {
+    const uint32_t w = *reinterpret_cast<const uint32_t*>(codes + i);
+    float o[4];
+    fp8x4(w, o);
+    out[i] = o[0]; out[i + 1] = o[1]; out[i + 2] = o[2]; out[i + 3] = o[3];
+  } else {
+    for (int j = i; j < n; ++j) {
+      float o[4];
+      fp8x4(static_cast<uint32_t>(codes[j]), o);
+      out[j] = o[0];
+    }
+  }
+}
+}  // namespace
+
+hipError_t launch_decode_fp8(const uint8_t* codes, float* out, int n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int threads = (n + 3) / 4;
+  hipLaunchKernelGGL(decode_fp8_kernel, dim3((threads + 255) / 256), dim3(256), 0, st, codes, out, n);
+  return hipGetLastError();
+}
+
+}  // namespace wisp

@@ -1,0 +1,77 @@
+// Internal interface between the pager (host C++) and the HIP kernels for gfx950.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace wisp {
+
+// Element formats (same codes as wisp_dtype).
+enum : int { DT_F32 = 0, DT_BF16 = 1, DT_FP8 = 2 };
+
+// Bytes of the expert blob and offsets of its parts (W1 | W3 | W2 [| S1 | S3 | S2]).
+struct BlobLayout {
+  int d = 0, I = 0, w_dtype = 0;
+  size_t elem = 0;          // bytes per stored weight element (4, 2, 1)
+  size_t off_w1 = 0, off_w3 = 0, off_w2 = 0;
+  size_t off_s1 = 0, off_s3 = 0, off_s2 = 0;  // fp8 scales (bf16)
+  size_t bytes = 0;
+};
+BlobLayout make_blob_layout(int d, int I, int w_dtype);
+
+// One unit of expert-FFN work: an expert blob (already in HBM) and up to kMaxTokPerItem tokens
+// that chose it.  out[t] is the row of the h / buf scratch that receives token tok[t]'s result
+// (row = token * (k + 1) + rank; rank k is the shared expert).
+constexpr int kMaxTokPerItem = 4;
+constexpr int kMaxItems = 40;
+
+struct FfnItem {
+  const uint8_t* w;
+  int32_t ntok;
+  int32_t tok[kMaxTokPerItem];
+  int32_t out[kMaxTokPerItem];
+};
+
+// Passed by value as a kernel argument (the device-side expert map of this launch).
+struct FfnBatch {
+  FfnItem items[kMaxItems];
+  int32_t n_items;
+  int32_t max_ntok;
+};
+
+struct FfnShape {
+  BlobLayout blob;
+  int x_dtype;     // DT_F32 or DT_BF16 input rows
+  int h_dtype;     // DT_F32 (fp32 models) or DT_BF16 (h rounded to bf16 between the GEMVs)
+};
+
+// Timing hook: if ev0/ev1 are non-null they bracket the launch (hipExtLaunchKernel events).
+struct LaunchTiming {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
+// Phase 1: h[out] = silu(W1 x[tok]) * (W3 x[tok]) for every item/token; h row stride = I.
+hipError_t launch_ffn_gateup(const FfnBatch& b, const FfnShape& s, const void* x, void* h, hipStream_t st,
+                             const LaunchTiming& tm);
+// Phase 2: buf[out] = W2 h[out]; buf row stride = d (fp32).
+hipError_t launch_ffn_down(const FfnBatch& b, const FfnShape& s, const void* h, float* buf, hipStream_t st,
+                           const LaunchTiming& tm);
+// y[t] = sum_j w[t, j] buf[t*(k+1)+j] (j ascending) + (shared ? buf[t*(k+1)+k] : 0).
+hipError_t launch_combine(int T, int k, int d, int has_shared, const float* w, const float* buf, float* y,
+                          hipStream_t st, const LaunchTiming& tm);
+
+// Router: logits[t, e] = W_r[e] . x[t] (fp32 accumulate).
+hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int T, int N, int d, float* logits,
+                                hipStream_t st, const LaunchTiming& tm);
+// Router selection: idx/w [T, k] by routing variant.
+hipError_t launch_router_select(const float* logits, int T, int N, int k, int route, int n_groups, int topk_groups,
+                                int32_t* idx, float* w, hipStream_t st, const LaunchTiming& tm);
+
+// Diagnostics.
+hipError_t launch_hbm_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
+hipError_t launch_decode_fp8(const uint8_t* codes, float* out, int n, hipStream_t st);
+
+}  // namespace wisp
