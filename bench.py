@@ -86,7 +86,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-kernel-timing", action="store_true", help="skip the per-kernel HIP events")
+    ap.add_argument("--kernel-timing", choices=["gateup", "all", "none"], default="gateup",
+                    help="kernel classes bracketed by HIP events inside the timed region (default: the expert "
+                         "gate/up GEMV, on which the roofline is reported)")
+    ap.add_argument("--census-steps", type=int, default=24,
+                    help="extra decode steps after the timed region with every kernel class timed (0 = skip)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -128,7 +132,8 @@ def main():
     tw = time.perf_counter() - tw
     run.ctx.reset_stats()
     run.ctx.reset_kernel_times()
-    run.ctx.set_profiling(0 if args.no_kernel_timing else 1)
+    mask = {"gateup": 1 << wisp.K_FFN_GATEUP, "all": True, "none": 0}[args.kernel_timing]
+    run.ctx.set_profiling(mask)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     out = run.decode(record=False, steps=steps, start=warmup)
@@ -151,17 +156,30 @@ def main():
                 faults_per_token=float(misses.sum()) / (wl.T * steps),
                 fault_rate=float(misses.sum()) / float(distinct.sum()))
 
-    kernels = {}
-    for kc, name in enumerate(wisp.KERNEL_CLASS_NAMES):
-        t = run.ctx.kernel_times(kc)
-        if t["launches"]:
-            avg_us = t["total_ms"] * 1e3 / t["launches"]
-            kernels[name] = dict(launches=t["launches"], avg_us=avg_us, total_ms=t["total_ms"],
-                                 bytes_per_launch=t["bytes"] / t["launches"],
+    def kernel_table():
+        tab = {}
+        for kc, name in enumerate(wisp.KERNEL_CLASS_NAMES):
+            t = run.ctx.kernel_times(kc)
+            if t["launches"]:
+                tab[name] = dict(launches=t["launches"], avg_us=t["total_ms"] * 1e3 / t["launches"],
+                                 total_ms=t["total_ms"], bytes_per_launch=t["bytes"] / t["launches"],
                                  GBps=t["bytes"] / (t["total_ms"] * 1e-3) / 1e9 if t["total_ms"] > 0 else None)
+        return tab
+
+    timed_kernels = kernel_table()
+    census = {}
+    if args.census_steps > 0 and total < run.x_host.shape[1] + 1:
+        # every class timed, on steps after the timed region (the events slow the path, so these
+        # steps are not part of the throughput)
+        run.ctx.reset_kernel_times()
+        run.ctx.set_profiling(True)
+        n_c = min(args.census_steps, total)
+        run.decode(record=False, steps=n_c, start=0)
+        run.ctx.set_profiling(0)
+        census = kernel_table()
     roof = None
-    if "ffn_gateup" in kernels:
-        g = kernels["ffn_gateup"]
+    if "ffn_gateup" in timed_kernels:
+        g = timed_kernels["ffn_gateup"]
         roof = dict(bound="hbm", achieved=g["GBps"], peak=HBM_PEAK_GBPS, unit="GB/s", frac=g["GBps"] / HBM_PEAK_GBPS,
                     traffic=None, kernel="ffn_rows<bf16, gate/up> (expert GEMV, W1+W3 rows)",
                     avg_launch_us=g["avg_us"], bytes_per_launch=g["bytes_per_launch"])
@@ -191,8 +209,9 @@ def main():
         "roofline": roof,
         "path_roofline": path,
         "cpu_baseline": cpu,
-        "kernels": kernels,
-        "kernel_timing": not args.no_kernel_timing,
+        "kernels_timed_region": timed_kernels,
+        "kernel_census": census,
+        "kernel_timing": args.kernel_timing,
     }
     run.close()
     print(json.dumps(result), flush=True)

@@ -163,14 +163,16 @@ wisp_status wisp_expert_in_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, int3
 /* Copy the device bytes of `slot` of `layer` to host memory dst (M_e bytes); synchronous. */
 wisp_status wisp_read_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, void* dst);
 
-/* Kernel timing.  When on, every kernel launch and every fill batch is bracketed by HIP events
- * on its own stream; durations are accumulated per class.  Classes: */
+/* Kernel timing.  Launches of the classes whose bit is set in class_mask (1 << wisp_kernel_class;
+ * 0 = off) are bracketed by HIP events on their own stream (kernels through the launch's own
+ * start/stop events, fill batches by events on the side stream); durations accumulate per class.
+ * Classes: */
 typedef enum {
   WISP_K_ROUTER_LOGITS = 0, WISP_K_ROUTER_SELECT = 1, WISP_K_FFN_GATEUP = 2, WISP_K_FFN_DOWN = 3,
   WISP_K_COMBINE = 4, WISP_K_H2D_FILL = 5, WISP_K_GROUPED_GATEUP = 6, WISP_K_GROUPED_DOWN = 7,
   WISP_K_PERMUTE = 8, WISP_K_NUM = 9
 } wisp_kernel_class;
-wisp_status wisp_set_profiling(wisp_ctx* ctx, int32_t on);
+wisp_status wisp_set_profiling(wisp_ctx* ctx, int32_t class_mask);
 /* Waits for outstanding timed work, then returns the accumulated total milliseconds, number of
  * launches, and algorithmic HBM bytes (weights and activations each read or written once) of a
  * class. */

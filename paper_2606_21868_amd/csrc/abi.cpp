@@ -81,7 +81,10 @@ struct wisp_ctx {
   float* logits = nullptr;
   void* h = nullptr;
   float* buf = nullptr;
-  int32_t* idx_pinned = nullptr;
+  int32_t* idx_pinned = nullptr;     // pinned staging for the copy-based id transfer
+  uint64_t* idx_tagged = nullptr;    // host-coherent (seq << 32 | id) words written by the router
+  uint32_t route_seq = 0;
+  int32_t profile_mask = 0;          // kernel classes timed when profiling
   std::vector<int32_t> ids_scratch;
   bool profiling = false;
   std::vector<TimedPair> timed;
@@ -114,9 +117,9 @@ hipEvent_t pool_event(wisp_ctx* c) {
   return e;
 }
 
-LaunchTiming timing_begin(wisp_ctx* c) {
+LaunchTiming timing_begin(wisp_ctx* c, int kclass) {
   LaunchTiming t;
-  if (c->profiling) {
+  if (c->profiling && ((c->profile_mask >> kclass) & 1)) {
     t.start = pool_event(c);
     t.stop = pool_event(c);
   }
@@ -247,7 +250,7 @@ wisp_status issue_fills(wisp_ctx* c, int32_t layer, size_t ci) {
   } else {
     WISP_HIP(hipStreamWaitEvent(c->side, L.chunk_ev[ci - 1], 0), "hipStreamWaitEvent(chunk)");
   }
-  LaunchTiming tm = timing_begin(c);
+  LaunchTiming tm = timing_begin(c, WISP_K_H2D_FILL);
   if (tm.start) WISP_HIP(hipEventRecord(tm.start, c->side), "hipEventRecord");
   for (size_t i = 0; i < cp.experts.size(); ++i) {
     if (!cp.fault[i]) continue;
@@ -274,32 +277,31 @@ uint64_t ffn_bytes(const wisp_ctx* c, const FfnBatch& b, bool gateup) {
   return bytes;
 }
 
-// Launch gate/up then down for a list of (expert blob, (token, rank) pairs), in batches.
+// Launch gate/up then down for a list of (expert blob, (token, rank) pairs), in batches of up to
+// kMaxItems items.  If `fin` asks for it, the last batch's down projection also does the combine
+// (when the shape allows the fused kernel); fin->done reports whether it did.
 struct Pair { int32_t t, out; };
 struct Work { const uint8_t* w; std::vector<Pair> pairs; };
+struct Finish {
+  bool want = false;
+  bool done = false;
+  int32_t T = 0;
+  const float* w = nullptr;
+  float* y = nullptr;
+};
 
-wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, hipStream_t st) {
-  FfnBatch b;
-  b.n_items = 0;
-  b.max_ntok = 0;
-  auto flush = [&]() -> wisp_status {
-    if (b.n_items == 0) return WISP_OK;
-    LaunchTiming t1 = timing_begin(c);
-    WISP_HIP(launch_ffn_gateup(b, c->shape, x, c->h, st, t1), "ffn gate/up launch");
-    timing_end(c, t1, WISP_K_FFN_GATEUP, ffn_bytes(c, b, true));
-    LaunchTiming t2 = timing_begin(c);
-    WISP_HIP(launch_ffn_down(b, c->shape, c->h, c->buf, st, t2), "ffn down launch");
-    timing_end(c, t2, WISP_K_FFN_DOWN, ffn_bytes(c, b, false));
-    b.n_items = 0;
-    b.max_ntok = 0;
-    return WISP_OK;
-  };
+wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, hipStream_t st, Finish* fin) {
+  std::vector<FfnBatch> batches(1);
+  batches[0].n_items = 0;
+  batches[0].max_ntok = 0;
   for (const Work& wk : work) {
     for (size_t p0 = 0; p0 < wk.pairs.size(); p0 += kMaxTokPerItem) {
-      if (b.n_items == kMaxItems) {
-        wisp_status s = flush();
-        if (s != WISP_OK) return s;
+      if (batches.back().n_items == kMaxItems) {
+        batches.emplace_back();
+        batches.back().n_items = 0;
+        batches.back().max_ntok = 0;
       }
+      FfnBatch& b = batches.back();
       FfnItem& it = b.items[b.n_items++];
       it.w = wk.w;
       it.ntok = static_cast<int32_t>(std::min<size_t>(kMaxTokPerItem, wk.pairs.size() - p0));
@@ -311,7 +313,51 @@ wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, h
       b.max_ntok = std::max(b.max_ntok, it.ntok);
     }
   }
-  return flush();
+  const int k = c->desc.top_k;
+  for (size_t bi = 0; bi < batches.size(); ++bi) {
+    FfnBatch& b = batches[bi];
+    if (b.n_items == 0) continue;
+    int16_t pairs = 0;
+    std::fill(std::begin(b.src), std::end(b.src), static_cast<int8_t>(-1));
+    for (int i = 0; i < b.n_items; ++i) {
+      b.pair_base[i] = pairs;
+      for (int t = 0; t < b.items[i].ntok; ++t) {
+        const int row = b.items[i].out[t];
+        if (row < kMaxRows) b.src[row] = static_cast<int8_t>(pairs + t);
+      }
+      pairs = static_cast<int16_t>(pairs + b.items[i].ntok);
+    }
+    LaunchTiming t1 = timing_begin(c, WISP_K_FFN_GATEUP);
+    WISP_HIP(launch_ffn_gateup(b, c->shape, x, c->h, st, t1), "ffn gate/up launch");
+    timing_end(c, t1, WISP_K_FFN_GATEUP, ffn_bytes(c, b, true));
+    const bool last = bi + 1 == batches.size();
+    const bool comb = fin && fin->want && last;
+    bool fused_ok = false;
+    if (fin && fin->T * (k + 1) <= kMaxRows) {
+      LaunchTiming t2 = timing_begin(c, WISP_K_FFN_DOWN);
+      hipError_t e = launch_ffn_down_combine(b, c->shape, c->h, c->buf, fin->T, k, c->desc.has_shared, fin->w, fin->y,
+                                             comb, st, t2);
+      if (e == hipSuccess) {
+        fused_ok = true;
+        uint64_t by = ffn_bytes(c, b, false);
+        if (comb)
+          by += static_cast<uint64_t>(fin->T) * c->desc.d_model * 4 * (k + c->desc.has_shared + 1);
+        timing_end(c, t2, WISP_K_FFN_DOWN, by);
+        if (comb) fin->done = true;
+      } else if (e != hipErrorNotSupported) {
+        return fail(WISP_E_HIP, std::string("ffn down launch: ") + hipGetErrorString(e));
+      } else {
+        hipGetLastError();
+        if (t2.start) { c->ev_pool.push_back(t2.start); c->ev_pool.push_back(t2.stop); }
+      }
+    }
+    if (!fused_ok) {
+      LaunchTiming t2 = timing_begin(c, WISP_K_FFN_DOWN);
+      WISP_HIP(launch_ffn_down(b, c->shape, c->h, c->buf, st, t2), "ffn down launch");
+      timing_end(c, t2, WISP_K_FFN_DOWN, ffn_bytes(c, b, false));
+    }
+  }
+  return WISP_OK;
 }
 
 }  // namespace
@@ -382,9 +428,12 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   if (hipMalloc(&c->h, rows * desc->d_ff * c->h_elem()) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
   if (hipMalloc(&p, rows * desc->d_model * sizeof(float)) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
   c->buf = static_cast<float*>(p);
-  if (hipHostMalloc(&p, sizeof(int32_t) * static_cast<size_t>(T) * k, hipHostMallocCoherent) != hipSuccess)
+  const size_t ids_bytes = round_up(sizeof(int32_t) * static_cast<size_t>(T) * k, 256);
+  if (hipHostMalloc(&p, ids_bytes + sizeof(uint64_t) * static_cast<size_t>(T) * k, hipHostMallocCoherent) != hipSuccess)
     return bail(WISP_E_NOMEM, "pinned scratch");
   c->idx_pinned = static_cast<int32_t*>(p);
+  c->idx_tagged = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(p) + ids_bytes);
+  std::memset(c->idx_tagged, 0, sizeof(uint64_t) * static_cast<size_t>(T) * k);
   c->ids_scratch.resize(static_cast<size_t>(T) * k);
   *out = c;
   g_err.clear();
@@ -554,19 +603,41 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
   if (!L.wr) return fail(WISP_E_STATE, "router weights not set for this layer");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const auto& d = ctx->desc;
-  LaunchTiming t1 = timing_begin(ctx);
+  LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_LOGITS);
   WISP_HIP(launch_router_logits(L.wr, x_dev, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, st, t1),
            "router logits launch");
   timing_end(ctx, t1, WISP_K_ROUTER_LOGITS,
              static_cast<uint64_t>(d.n_experts) * d.d_model * 4 + static_cast<uint64_t>(T) * d.d_model * ctx->x_elem() +
                  static_cast<uint64_t>(T) * d.n_experts * 4);
-  LaunchTiming t2 = timing_begin(ctx);
+  // decode: the router publishes tagged ids to host-coherent memory
+  const bool publish = idx_host && T <= 4;
+  const uint32_t seq = publish ? ++ctx->route_seq : 0;
+  LaunchTiming t2 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
   WISP_HIP(launch_router_select(ctx->logits, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev,
-                                w_dev, st, t2),
+                                w_dev, publish ? ctx->idx_tagged : nullptr, seq, st, t2),
            "router select launch");
   timing_end(ctx, t2, WISP_K_ROUTER_SELECT,
              static_cast<uint64_t>(T) * d.n_experts * 4 + static_cast<uint64_t>(T) * d.top_k * 8);
-  if (idx_host) {
+  if (publish) {
+    const int n = T * d.top_k;
+    // spin until every entry carries this call's tag: the wait on the critical path of a layer-step
+    uint64_t spins = 0;
+    for (int i = 0; i < n; ++i) {
+      uint64_t v;
+      while (((v = __atomic_load_n(ctx->idx_tagged + i, __ATOMIC_ACQUIRE)) >> 32) != seq) {
+        __builtin_ia32_pause();
+        if ((++spins & 0xFFFFF) == 0) {
+          hipError_t q = hipStreamQuery(st);
+          if (q != hipSuccess && q != hipErrorNotReady)
+            return fail(WISP_E_HIP, std::string("router stream: ") + hipGetErrorString(q));
+          if (q == hipSuccess && (__atomic_load_n(ctx->idx_tagged + i, __ATOMIC_ACQUIRE) >> 32) != seq)
+            return fail(WISP_E_HIP, "router finished without publishing its indices");
+        }
+      }
+      idx_host[i] = static_cast<int32_t>(v & 0xFFFFFFFFu);
+    }
+    if (ctx->profiling) harvest(ctx, false);
+  } else if (idx_host) {
     const size_t nb = sizeof(int32_t) * static_cast<size_t>(T) * d.top_k;
     WISP_HIP(hipMemcpyAsync(ctx->idx_pinned, idx_dev, nb, hipMemcpyDeviceToHost, st), "hipMemcpyAsync(idx)");
     WISP_HIP(hipEventRecord(ctx->route_ev, st), "hipEventRecord(route)");
@@ -642,6 +713,10 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
       for (int32_t e : L.plan.chunks[ci].experts) found |= (e == L.ids[i]);
     if (!found) return fail(WISP_E_NOT_RESIDENT, "routed expert missing from the page-in plan");
   }
+  Finish fin;
+  fin.T = T;
+  fin.w = w_dev;
+  fin.y = y_dev;
   for (size_t ci = 0; ci < nch; ++ci) {
     const ChunkPlan& cp = L.plan.chunks[ci];
     if (ci > 0 && (s = issue_fills(ctx, layer, ci)) != WISP_OK) return s;
@@ -660,19 +735,24 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
       for (int32_t t = 0; t < T; ++t) wk.pairs.push_back({t, t * rows + k});
       hits.push_back(std::move(wk));
     }
-    if (!hits.empty() && (s = run_ffn(ctx, hits, x_dev, sm)) != WISP_OK) return s;
+    const bool last_chunk = ci + 1 == nch;
+    fin.want = last_chunk && faults.empty();
+    if (!hits.empty() && (s = run_ffn(ctx, hits, x_dev, sm, &fin)) != WISP_OK) return s;
     if (!faults.empty()) {
       WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[ci], 0), "hipStreamWaitEvent(fill)");
-      if ((s = run_ffn(ctx, faults, x_dev, sm)) != WISP_OK) return s;
+      fin.want = last_chunk;
+      if ((s = run_ffn(ctx, faults, x_dev, sm, &fin)) != WISP_OK) return s;
     }
     if (ci + 1 < nch) WISP_HIP(hipEventRecord(L.chunk_ev[ci], sm), "hipEventRecord(chunk)");
   }
-  LaunchTiming tc = timing_begin(ctx);
-  WISP_HIP(launch_combine(T, k, ctx->desc.d_model, ctx->desc.has_shared, w_dev, ctx->buf, y_dev, sm, tc),
-           "combine launch");
-  timing_end(ctx, tc, WISP_K_COMBINE,
-             static_cast<uint64_t>(T) * ctx->desc.d_model * 4 * (k + ctx->desc.has_shared + 1) +
-                 static_cast<uint64_t>(T) * k * 4);
+  if (!fin.done) {
+    LaunchTiming tc = timing_begin(ctx, WISP_K_COMBINE);
+    WISP_HIP(launch_combine(T, k, ctx->desc.d_model, ctx->desc.has_shared, w_dev, ctx->buf, y_dev, sm, tc),
+             "combine launch");
+    timing_end(ctx, tc, WISP_K_COMBINE,
+               static_cast<uint64_t>(T) * ctx->desc.d_model * 4 * (k + ctx->desc.has_shared + 1) +
+                   static_cast<uint64_t>(T) * k * 4);
+  }
   WISP_HIP(hipEventRecord(L.use_ev, sm), "hipEventRecord(use)");
   L.use_ev_recorded = true;
   L.pending = false;
@@ -757,10 +837,11 @@ wisp_status wisp_read_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, void* dst
   return WISP_OK;
 }
 
-wisp_status wisp_set_profiling(wisp_ctx* ctx, int32_t on) {
+wisp_status wisp_set_profiling(wisp_ctx* ctx, int32_t class_mask) {
   if (!ctx) return fail(WISP_E_INVAL, "ctx is NULL");
-  if (!on) harvest(ctx, true);
-  ctx->profiling = on != 0;
+  if (!class_mask) harvest(ctx, true);
+  ctx->profiling = class_mask != 0;
+  ctx->profile_mask = class_mask;
   return WISP_OK;
 }
 

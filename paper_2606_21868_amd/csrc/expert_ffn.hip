@@ -126,15 +126,6 @@ __global__ void __launch_bounds__(256) ffn_rows(const FfnBatch B, const uint8_t*
   const int ntok = it.ntok;
   const int row_bytes = K * IS;
 
-  // stage the item's input rows (x for gate/up, h for down) in LDS
-  for (int t = 0; t < ntok; ++t) {
-    const int src_row = MODE == MODE_GATEUP ? it.tok[t] : it.out[t];
-    const uint4* src = reinterpret_cast<const uint4*>(vin + static_cast<size_t>(src_row) * vin_stride * IS);
-    uint4* dst = reinterpret_cast<uint4*>(lds + t * row_bytes);
-    for (int i = threadIdx.x; i < row_bytes / 16; i += 256) dst[i] = src[i];
-  }
-  __syncthreads();
-
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int sub = lane / LPR;
@@ -149,7 +140,34 @@ __global__ void __launch_bounds__(256) ffn_rows(const FfnBatch B, const uint8_t*
   const int scols = K / 128;
   const size_t row_stride_b = static_cast<size_t>(K) * (WT == DT_F32 ? 4 : WT == DT_BF16 ? 2 : 1);
 
-  for (int rbase = r_begin + wave * RPW; rbase < r_end; rbase += 4 * RPW) {
+  // fully unrolled shapes: the first row pass issues its weight loads before the input rows are
+  // staged, so the HBM fetch overlaps the staging
+  const int rbase0 = r_begin + wave * RPW;
+  uint4 pa[NLT > 0 ? NLT : 1], pb[NLT > 0 ? NLT : 1];
+  if constexpr (NLT > 0) {
+    const int r = rbase0 + sub;
+    const int rr = r < r_end ? r : r_begin;
+    const uint4* row0 = reinterpret_cast<const uint4*>(wbase0 + rr * row_stride_b);
+    const uint4* row1 = reinterpret_cast<const uint4*>(wbase1 + rr * row_stride_b);
+    if (rbase0 < r_end) {
+#pragma unroll
+      for (int m = 0; m < NLT; ++m) {
+        pa[m] = row0[m * LPR + sl];
+        if constexpr (MODE == MODE_GATEUP) pb[m] = row1[m * LPR + sl];
+      }
+    }
+  }
+
+  // stage the item's input rows (x for gate/up, h for down) in LDS
+  for (int t = 0; t < ntok; ++t) {
+    const int src_row = MODE == MODE_GATEUP ? it.tok[t] : it.out[t];
+    const uint4* src = reinterpret_cast<const uint4*>(vin + static_cast<size_t>(src_row) * vin_stride * IS);
+    uint4* dst = reinterpret_cast<uint4*>(lds + t * row_bytes);
+    for (int i = threadIdx.x; i < row_bytes / 16; i += 256) dst[i] = src[i];
+  }
+  __syncthreads();
+
+  for (int rbase = rbase0; rbase < r_end; rbase += 4 * RPW) {
     const int r = rbase + sub;
     const bool valid = r < r_end;
     const int rr = valid ? r : r_begin;   // keep addresses in range for idle row groups
@@ -161,12 +179,20 @@ __global__ void __launch_bounds__(256) ffn_rows(const FfnBatch B, const uint8_t*
 
     for (int m0 = 0; m0 < NL; m0 += U) {
       uint4 a[U], b[U];
+      if (NLT > 0 && rbase == rbase0) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int m = m0 + u;
-        if (NLT > 0 || m < NL) {
-          a[u] = row0[m * LPR + sl];
-          if constexpr (MODE == MODE_GATEUP) b[u] = row1[m * LPR + sl];
+        for (int u = 0; u < U; ++u) {
+          a[u] = pa[NLT > 0 ? u : 0];
+          if constexpr (MODE == MODE_GATEUP) b[u] = pb[NLT > 0 ? u : 0];
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int m = m0 + u;
+          if (NLT > 0 || m < NL) {
+            a[u] = row0[m * LPR + sl];
+            if constexpr (MODE == MODE_GATEUP) b[u] = row1[m * LPR + sl];
+          }
         }
       }
 #pragma unroll
@@ -323,6 +349,152 @@ hipError_t launch_rows(int mode, const FfnBatch& b, const FfnShape& s, const voi
   return hipGetLastError();
 }
 
+// Down projection for all items of a launch, one block of output rows per workgroup, fused with
+// the gate-weighted combine.  Each row group of LPR lanes reads the W2 row of IG items at once
+// (IG * NL 16-byte loads in flight per lane) and dots it with every token's h row (LDS).
+template <int WT, int IT, int LPR, int NL, int IG>
+__global__ void __launch_bounds__(256) ffn_down_combine(const FfnBatch B, const uint8_t* __restrict__ h, int I,
+                                                        int d, int rows_per_wg, uint32_t off2, uint32_t soff2,
+                                                        float* __restrict__ buf, int T, int k, int has_shared,
+                                                        const float* __restrict__ gates, float* __restrict__ y,
+                                                        int combine) {
+  constexpr int EPL = WFmt<WT>::EPL;
+  constexpr int RPW = 64 / LPR;
+  constexpr int IS = IT == DT_F32 ? 4 : 2;
+  constexpr int ES = WT == DT_F32 ? 4 : WT == DT_BF16 ? 2 : 1;
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int n_items = B.n_items;
+  const int n_pairs = B.pair_base[n_items - 1] + B.items[n_items - 1].ntok;
+  const int row_bytes = I * IS;
+  float* outl = reinterpret_cast<float*>(lds + static_cast<size_t>(n_pairs) * row_bytes);  // [pair][local row]
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int sub = lane / LPR, sl = lane - sub * LPR;
+  const int r0 = blockIdx.x * rows_per_wg;
+  const int r1 = min(d, r0 + rows_per_wg);
+  const int scols = I / 128;
+  const int rows = k + 1;
+  const int nr = r1 - r0;
+
+  // before anything waits: the first pass's W2 loads of the first item group, and the combine
+  // inputs produced by earlier launches (one (token, row) per thread: T * nr <= 256)
+  const int rbase0 = r0 + wave * RPW;
+  uint4 pre[IG][NL];
+  {
+    const int r = rbase0 + sub;
+    const int rr = r < r1 ? r : r0;
+    if (rbase0 < r1) {
+#pragma unroll
+      for (int u = 0; u < IG; ++u) {
+        if (u >= n_items) break;
+        const uint4* row = reinterpret_cast<const uint4*>(B.items[u].w + off2 + static_cast<size_t>(rr) * I * ES);
+#pragma unroll
+        for (int m = 0; m < NL; ++m) pre[u][m] = row[m * LPR + sl];
+      }
+    }
+  }
+  float cprev[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float cshared = 0.f;
+  if (combine && static_cast<int>(threadIdx.x) < T * nr) {
+    const int t = threadIdx.x / nr, r = r0 + threadIdx.x % nr;
+    for (int j = 0; j < k; ++j)
+      if (B.src[t * rows + j] < 0) cprev[j] = buf[static_cast<size_t>(t * rows + j) * d + r];
+    if (has_shared && B.src[t * rows + k] < 0) cshared = buf[static_cast<size_t>(t * rows + k) * d + r];
+  }
+
+  // stage every (item, token) h row
+  for (int i = 0; i < n_items; ++i) {
+    const FfnItem& it = B.items[i];
+    for (int t = 0; t < it.ntok; ++t) {
+      const uint4* src = reinterpret_cast<const uint4*>(h + static_cast<size_t>(it.out[t]) * row_bytes);
+      uint4* dst = reinterpret_cast<uint4*>(lds + static_cast<size_t>(B.pair_base[i] + t) * row_bytes);
+      for (int c = threadIdx.x; c < row_bytes / 16; c += 256) dst[c] = src[c];
+    }
+  }
+  __syncthreads();
+
+  for (int rbase = rbase0; rbase < r1; rbase += 4 * RPW) {
+    const int r = rbase + sub;
+    const bool valid = r < r1;
+    const int rr = valid ? r : r0;
+    for (int i0 = 0; i0 < n_items; i0 += IG) {
+      uint4 a[IG][NL];
+      if (rbase == rbase0 && i0 == 0) {
+#pragma unroll
+        for (int u = 0; u < IG; ++u)
+#pragma unroll
+          for (int m = 0; m < NL; ++m) a[u][m] = pre[u][m];
+      } else {
+#pragma unroll
+        for (int u = 0; u < IG; ++u) {
+          if (i0 + u >= n_items) break;
+          const uint4* row = reinterpret_cast<const uint4*>(B.items[i0 + u].w + off2 + static_cast<size_t>(rr) * I * ES);
+#pragma unroll
+          for (int m = 0; m < NL; ++m) a[u][m] = row[m * LPR + sl];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < IG; ++u) {
+        if (i0 + u >= n_items) break;
+        const FfnItem& it = B.items[i0 + u];
+        const uint16_t* sc = reinterpret_cast<const uint16_t*>(it.w + soff2);
+        float acc[kMaxTokPerItem] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int m = 0; m < NL; ++m) {
+          const int col = (m * LPR + sl) * EPL;
+          float wv[EPL];
+          decode_chunk<WT>(a[u][m], wv);
+          float s2 = 1.f;
+          if constexpr (WT == DT_FP8) s2 = __uint_as_float(static_cast<uint32_t>(sc[(rr / 128) * scols + col / 128]) << 16);
+#pragma unroll
+          for (int t = 0; t < kMaxTokPerItem; ++t) {
+            if (t >= it.ntok) break;
+            float xv[EPL];
+            lds_chunk<IT, EPL>(lds + static_cast<size_t>(B.pair_base[i0 + u] + t) * row_bytes, col, xv);
+            if constexpr (WT == DT_FP8) {
+              float p = 0.f;
+#pragma unroll
+              for (int e = 0; e < EPL; ++e) p = fmaf(wv[e], xv[e], p);
+              acc[t] = fmaf(s2, p, acc[t]);
+            } else {
+#pragma unroll
+              for (int e = 0; e < EPL; ++e) acc[t] = fmaf(wv[e], xv[e], acc[t]);
+            }
+          }
+        }
+#pragma unroll
+        for (int t = 0; t < kMaxTokPerItem; ++t) {
+          if (t >= it.ntok) break;
+#pragma unroll
+          for (int off = LPR / 2; off > 0; off >>= 1) acc[t] += __shfl_xor(acc[t], off, 64);
+          if (valid && sl == 0) {
+            if (combine) outl[(B.pair_base[i0 + u] + t) * rows_per_wg + (r - r0)] = acc[t];
+            else buf[static_cast<size_t>(it.out[t]) * d + r] = acc[t];
+          }
+        }
+      }
+    }
+  }
+  if (!combine) return;
+  __syncthreads();
+  if (static_cast<int>(threadIdx.x) < T * nr) {
+    const int t = threadIdx.x / nr, lr = threadIdx.x % nr;
+    float acc = 0.f;
+    for (int j = 0; j < k; ++j) {
+      const int p = B.src[t * rows + j];
+      const float o = p >= 0 ? outl[p * rows_per_wg + lr] : cprev[j];
+      acc = fmaf(gates[t * k + j], o, acc);
+    }
+    if (has_shared) {
+      const int p = B.src[t * rows + k];
+      acc += p >= 0 ? outl[p * rows_per_wg + lr] : cshared;
+    }
+    y[static_cast<size_t>(t) * d + r0 + lr] = acc;
+  }
+}
+
+using DownKernel = void (*)(const FfnBatch, const uint8_t*, int, int, int, uint32_t, uint32_t, float*, int, int, int,
+                            const float*, float*, int);
+
 }  // namespace
 
 hipError_t launch_ffn_gateup(const FfnBatch& b, const FfnShape& s, const void* x, void* h, hipStream_t st,
@@ -333,6 +505,46 @@ hipError_t launch_ffn_gateup(const FfnBatch& b, const FfnShape& s, const void* x
 hipError_t launch_ffn_down(const FfnBatch& b, const FfnShape& s, const void* h, float* buf, hipStream_t st,
                            const LaunchTiming& tm) {
   return launch_rows(MODE_DOWN, b, s, h, s.blob.I, buf, s.blob.d, st, tm);
+}
+
+hipError_t launch_ffn_down_combine(const FfnBatch& b, const FfnShape& s, const void* h, float* buf, int T, int k,
+                                   int has_shared, const float* w, float* y, bool combine, hipStream_t st,
+                                   const LaunchTiming& tm) {
+  if (b.n_items <= 0) return hipSuccess;
+  const BlobLayout& L = s.blob;
+  const int WT = L.w_dtype, IT = s.h_dtype;
+  const int EPL = WT == DT_F32 ? 4 : WT == DT_BF16 ? 8 : 16;
+  const int chunks = L.I / EPL;
+  const int lpr = pick_lpr(chunks);
+  if (lpr == 0) return hipErrorNotSupported;
+  const int nl = chunks / lpr;
+  DownKernel kern = nullptr;
+#define WISP_D(W, X, LP, N, G) \
+  if (WT == W && IT == X && lpr == LP && nl == N) kern = &ffn_down_combine<W, X, LP, N, G>;
+  WISP_D(DT_BF16, DT_BF16, 32, 3, 8)   // I = 768
+  WISP_D(DT_FP8, DT_BF16, 64, 2, 8)    // I = 2048
+  WISP_D(DT_F32, DT_F32, 64, 2, 8)     // I = 512
+  WISP_D(DT_BF16, DT_BF16, 32, 1, 8)   // I = 256
+  WISP_D(DT_BF16, DT_BF16, 16, 1, 8)   // I = 128
+  WISP_D(DT_BF16, DT_BF16, 64, 2, 8)   // I = 1024
+  WISP_D(DT_BF16, DT_BF16, 8, 3, 8)    // I = 192
+  WISP_D(DT_FP8, DT_BF16, 16, 1, 8)    // I = 256
+#undef WISP_D
+  if (!kern) return hipErrorNotSupported;
+  const int isz = IT == DT_F32 ? 4 : 2;
+  const int n_pairs = b.pair_base[b.n_items - 1] + b.items[b.n_items - 1].ntok;
+  const int rpw = 64 / lpr;
+  const int step = 4 * rpw;
+  int rows_per_wg = (L.d + 511) / 512;                  // about 512 workgroups at most
+  rows_per_wg = (rows_per_wg + step - 1) / step * step;
+  const size_t lds = static_cast<size_t>(n_pairs) * L.I * isz + static_cast<size_t>(n_pairs) * rows_per_wg * 4;
+  if (lds > 64 * 1024) return hipErrorNotSupported;
+  if (combine && T * rows_per_wg > 256) return hipErrorNotSupported;
+  const int grid = (L.d + rows_per_wg - 1) / rows_per_wg;
+  hipExtLaunchKernelGGL(kern, dim3(grid), dim3(256), static_cast<uint32_t>(lds), st, tm.start, tm.stop, 0, b,
+                        static_cast<const uint8_t*>(h), L.I, L.d, rows_per_wg, static_cast<uint32_t>(L.off_w2),
+                        static_cast<uint32_t>(L.off_s2), buf, T, k, has_shared, w, y, combine ? 1 : 0);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------------------------------

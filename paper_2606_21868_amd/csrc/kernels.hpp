@@ -35,10 +35,15 @@ struct FfnItem {
 };
 
 // Passed by value as a kernel argument (the device-side expert map of this launch).
+constexpr int kMaxRows = 4 * 9;  // T <= 4 tokens x (k <= 8 ranks + shared)
 struct FfnBatch {
   FfnItem items[kMaxItems];
   int32_t n_items;
   int32_t max_ntok;
+  // for the fused down + combine launch: pair_base[i] = index of item i's first (item, token)
+  // pair; src[row] = the pair holding output row `row` in this launch, or -1 (read the scratch)
+  int16_t pair_base[kMaxItems];
+  int8_t src[kMaxRows];
 };
 
 struct FfnShape {
@@ -59,6 +64,13 @@ hipError_t launch_ffn_gateup(const FfnBatch& b, const FfnShape& s, const void* x
 // Phase 2: buf[out] = W2 h[out]; buf row stride = d (fp32).
 hipError_t launch_ffn_down(const FfnBatch& b, const FfnShape& s, const void* h, float* buf, hipStream_t st,
                            const LaunchTiming& tm);
+// Phase 2 fused with the combine, for decode batches whose h rows fit in LDS: every workgroup owns
+// a block of output rows for all items; y[t] = sum_j w[t, j] o_tj (+ shared) with o_tj from this
+// launch (LDS) or from earlier launches (buf).  With combine = false it only writes buf.
+// Returns hipErrorNotSupported if the shape does not fit; the caller then uses the two kernels.
+hipError_t launch_ffn_down_combine(const FfnBatch& b, const FfnShape& s, const void* h, float* buf, int T, int k,
+                                   int has_shared, const float* w, float* y, bool combine, hipStream_t st,
+                                   const LaunchTiming& tm);
 // y[t] = sum_j w[t, j] buf[t*(k+1)+j] (j ascending) + (shared ? buf[t*(k+1)+k] : 0).
 hipError_t launch_combine(int T, int k, int d, int has_shared, const float* w, const float* buf, float* y,
                           hipStream_t st, const LaunchTiming& tm);
@@ -66,9 +78,11 @@ hipError_t launch_combine(int T, int k, int d, int has_shared, const float* w, c
 // Router: logits[t, e] = W_r[e] . x[t] (fp32 accumulate).
 hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int T, int N, int d, float* logits,
                                 hipStream_t st, const LaunchTiming& tm);
-// Router selection: idx/w [T, k] by routing variant.
+// Router selection: idx/w [T, k] by routing variant.  If idx_host is given, entry t*k+j of it (in
+// host-coherent memory) also receives (seq << 32 | id) as one 64-bit store.
 hipError_t launch_router_select(const float* logits, int T, int N, int k, int route, int n_groups, int topk_groups,
-                                int32_t* idx, float* w, hipStream_t st, const LaunchTiming& tm);
+                                int32_t* idx, float* w, uint64_t* idx_host, uint32_t seq, hipStream_t st,
+                                const LaunchTiming& tm);
 
 // Diagnostics.
 hipError_t launch_hbm_copy(const void* src, void* dst, size_t bytes, hipStream_t st);

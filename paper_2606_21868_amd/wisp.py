@@ -237,8 +237,10 @@ class Context:
         check(lib().wisp_read_slot(self.h, layer, slot, out.ctypes.data), "wisp_read_slot")
         return out
 
-    def set_profiling(self, on):
-        check(lib().wisp_set_profiling(self.h, int(on)), "wisp_set_profiling")
+    def set_profiling(self, class_mask):
+        """class_mask: bit c times kernel class c (1 << K_FFN_GATEUP, ...); True = every class; 0 = off."""
+        mask = (1 << len(KERNEL_CLASS_NAMES)) - 1 if class_mask is True else int(class_mask)
+        check(lib().wisp_set_profiling(self.h, mask), "wisp_set_profiling")
 
     def kernel_times(self, kclass):
         ms = ctypes.c_double()
