@@ -89,6 +89,8 @@ def main():
     ap.add_argument("--kernel-timing", choices=["gateup", "all", "none"], default="gateup",
                     help="kernel classes bracketed by HIP events inside the timed region (default: the expert "
                          "gate/up GEMV, on which the roofline is reported)")
+    ap.add_argument("--pager", choices=["both", "device", "host"], default="both",
+                    help="which pager(s) to time; value is the device pager's when it runs")
     ap.add_argument("--census-steps", type=int, default=24,
                     help="extra decode steps after the timed region with every kernel class timed (0 = skip)")
     args = ap.parse_args()
@@ -126,35 +128,35 @@ def main():
     log(f"host->device {link:.1f} GB/s (median of 5 x {n_probe} blobs); device copy {hbm_copy:.0f} GB/s")
     assert run.set_cap(wl.cap) == wl.cap
 
-    tw = time.perf_counter()
-    if warmup:
-        run.decode(record=False, steps=warmup, start=0)
-    tw = time.perf_counter() - tw
-    run.ctx.reset_stats()
-    run.ctx.reset_kernel_times()
-    mask = {"gateup": 1 << wisp.K_FFN_GATEUP, "all": True, "none": 0}[args.kernel_timing]
-    run.ctx.set_profiling(mask)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    out = run.decode(record=False, steps=steps, start=warmup)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t1
-    run.ctx.set_profiling(0)
-    tok_s = wl.T * steps / elapsed
-    log(f"timed {steps} steps in {elapsed:.3f} s -> {tok_s:.2f} tokens/s (warmup {tw:.2f} s)")
+    def timed_pass(pager, mask):
+        """Cold slot tables, `warmup` untimed steps, then the timed steps; returns (elapsed, stats)."""
+        run.ctx.masters_ready()                       # every slot empty: each pass starts cold
+        run.ctx.set_pager(pager)
+        if warmup:
+            run.decode(record=False, steps=warmup, start=0)
+        run.ctx.reset_stats()
+        run.ctx.reset_kernel_times()
+        run.ctx.set_profiling(mask)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        out = run.decode(record=False, steps=steps, start=warmup)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t1
+        run.ctx.set_profiling(0)
+        return el, out
 
-    # path roofline from the exact counts of the timed steps
-    hits, misses = out["hits"], out["misses"]
-    distinct = hits + misses
-    router_bytes = wl.N * wl.d * 4
-    hbm_bytes = float(distinct.sum()) * wl.blob + router_bytes * wl.L * steps
-    link_bytes = float(misses.sum()) * wl.blob
-    t_roof = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (link * 1e9)
-    path = dict(t_roof_s=t_roof, t_measured_s=elapsed, frac=t_roof / elapsed, roofline_tokens_per_s=wl.T * steps / t_roof,
-                link_GBps_measured=link, hbm_peak_GBps=HBM_PEAK_GBPS, device_copy_GBps_measured=hbm_copy,
-                hbm_bytes_per_token=hbm_bytes / (wl.T * steps), link_bytes_per_token=link_bytes / (wl.T * steps),
-                faults_per_token=float(misses.sum()) / (wl.T * steps),
-                fault_rate=float(misses.sum()) / float(distinct.sum()))
+    def path_roofline(elapsed, out):
+        hits, misses = out["hits"], out["misses"]
+        distinct = hits + misses
+        hbm_bytes = float(distinct.sum()) * wl.blob + wl.N * wl.d * 4 * wl.L * steps
+        link_bytes = float(misses.sum()) * wl.blob
+        t_roof = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (link * 1e9)
+        return dict(t_roof_s=t_roof, t_measured_s=elapsed, frac=t_roof / elapsed,
+                    roofline_tokens_per_s=wl.T * steps / t_roof, link_GBps_measured=link,
+                    hbm_peak_GBps=HBM_PEAK_GBPS, device_copy_GBps_measured=hbm_copy,
+                    hbm_bytes_per_token=hbm_bytes / (wl.T * steps), link_bytes_per_token=link_bytes / (wl.T * steps),
+                    faults_per_token=float(misses.sum()) / (wl.T * steps),
+                    fault_rate=float(misses.sum()) / float(distinct.sum()))
 
     def kernel_table():
         tab = {}
@@ -162,27 +164,50 @@ def main():
             t = run.ctx.kernel_times(kc)
             if t["launches"]:
                 tab[name] = dict(launches=t["launches"], avg_us=t["total_ms"] * 1e3 / t["launches"],
-                                 total_ms=t["total_ms"], bytes_per_launch=t["bytes"] / t["launches"],
-                                 GBps=t["bytes"] / (t["total_ms"] * 1e-3) / 1e9 if t["total_ms"] > 0 else None)
+                                 total_ms=t["total_ms"],
+                                 bytes_per_launch=t["bytes"] / t["launches"] if t["bytes"] else None,
+                                 GBps=t["bytes"] / (t["total_ms"] * 1e-3) / 1e9 if t["bytes"] and t["total_ms"] > 0
+                                 else None)
         return tab
 
-    timed_kernels = kernel_table()
-    census = {}
-    if args.census_steps > 0 and total < run.x_host.shape[1] + 1:
+    def census(pager):
         # every class timed, on steps after the timed region (the events slow the path, so these
-        # steps are not part of the throughput)
+        # steps are not part of any throughput)
+        if args.census_steps <= 0:
+            return {}
+        run.ctx.set_pager(pager)
         run.ctx.reset_kernel_times()
         run.ctx.set_profiling(True)
-        n_c = min(args.census_steps, total)
-        run.decode(record=False, steps=n_c, start=0)
+        run.decode(record=False, steps=min(args.census_steps, total), start=0)
         run.ctx.set_profiling(0)
-        census = kernel_table()
+        return kernel_table()
+
+    mask = {"gateup": 1 << wisp.K_FFN_GATEUP, "all": True, "none": 0}[args.kernel_timing]
+    passes = {}
     roof = None
-    if "ffn_gateup" in timed_kernels:
-        g = timed_kernels["ffn_gateup"]
-        roof = dict(bound="hbm", achieved=g["GBps"], peak=HBM_PEAK_GBPS, unit="GB/s", frac=g["GBps"] / HBM_PEAK_GBPS,
-                    traffic=None, kernel="ffn_rows<bf16, gate/up> (expert GEMV, W1+W3 rows)",
-                    avg_launch_us=g["avg_us"], bytes_per_launch=g["bytes_per_launch"])
+    if args.pager in ("both", "host"):
+        el, out = timed_pass(wisp.PAGER_HOST, mask)
+        tk = kernel_table()
+        passes["host"] = dict(tokens_per_s=wl.T * steps / el, ms_per_step=el / steps * 1e3,
+                              path_roofline=path_roofline(el, out), kernels_timed_region=tk,
+                              kernel_census=census(wisp.PAGER_HOST))
+        log(f"host pager: {steps} steps in {el:.3f} s -> {wl.T * steps / el:.2f} tokens/s, "
+            f"{passes['host']['path_roofline']['frac']:.3f} of the path roofline")
+        if "ffn_gateup" in tk:
+            g = tk["ffn_gateup"]
+            roof = dict(bound="hbm", achieved=g["GBps"], peak=HBM_PEAK_GBPS, unit="GB/s", frac=g["GBps"] / HBM_PEAK_GBPS,
+                        traffic=None, kernel="ffn_rows<bf16,bf16,gate/up> expert GEMV (W1+W3 rows), host-pager pass",
+                        avg_launch_us=g["avg_us"], bytes_per_launch=g["bytes_per_launch"], launches=g["launches"])
+    if args.pager in ("both", "device"):
+        el, out = timed_pass(wisp.PAGER_DEVICE, 0)
+        passes["device"] = dict(tokens_per_s=wl.T * steps / el, ms_per_step=el / steps * 1e3,
+                                path_roofline=path_roofline(el, out), kernel_census=census(wisp.PAGER_DEVICE))
+        log(f"device pager: {steps} steps in {el:.3f} s -> {wl.T * steps / el:.2f} tokens/s, "
+            f"{passes['device']['path_roofline']['frac']:.3f} of the path roofline")
+    main_pass = "device" if "device" in passes else "host"
+    tok_s = passes[main_pass]["tokens_per_s"]
+    elapsed = steps / tok_s * wl.T
+    path = passes[main_pass]["path_roofline"]
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -209,8 +234,8 @@ def main():
         "roofline": roof,
         "path_roofline": path,
         "cpu_baseline": cpu,
-        "kernels_timed_region": timed_kernels,
-        "kernel_census": census,
+        "pager": main_pass,
+        "passes": passes,
         "kernel_timing": args.kernel_timing,
     }
     run.close()

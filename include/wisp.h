@@ -117,6 +117,22 @@ wisp_status wisp_set_budget(wisp_ctx* ctx, uint64_t expert_bytes, int32_t* cap_o
  * faults.  Not counted in the statistics. */
 wisp_status wisp_preload(wisp_ctx* ctx);
 
+/* Where Algorithm 1 runs.
+ * WISP_PAGER_HOST (default): the slot table lives on the host; wisp_route_topk hands the routed
+ *   ids to the host, wisp_page_in decides and issues hipMemcpyAsync fills on the side stream,
+ *   wisp_moe_forward runs the FFN ordered after the fills by events.
+ * WISP_PAGER_DEVICE: the slot table lives in HBM and a one-workgroup kernel runs the same rule
+ *   right after the router, writing the launch plan of the layer's FFN to HBM; the gate/up
+ *   kernel streams each faulted expert from its pinned host master over PCIe (computing with it
+ *   and filling its slot in the same pass), so a decode step (wisp_decode_step) is a fixed kernel
+ *   sequence with no host round trip.  Needs every layer-step to be one Algorithm 1 step
+ *   (C >= max_tokens * k), max_tokens <= 4 and a supported layer shape; wisp_page_in and
+ *   wisp_moe_forward are not available in this mode (WISP_E_STATE).
+ * Switching drains the context and moves the tables; paging decisions and outputs are the same
+ * in both modes. */
+typedef enum { WISP_PAGER_HOST = 0, WISP_PAGER_DEVICE = 1 } wisp_pager;
+wisp_status wisp_set_pager(wisp_ctx* ctx, int32_t pager);
+
 /* Route T tokens of `layer`: x_dev [T, d] (x_dtype) -> idx_dev [T, k] int32 and w_dev [T, k] fp32
  * on `stream`, ranks ordered (score desc, expert id asc).  If idx_host is not NULL the call
  * waits for the indices and copies them there (T*k int32): this is the one device->host

@@ -28,7 +28,7 @@ HIP_FLAGS = [
 ]
 
 HIP_SOURCES = ["abi.cpp", "slot_table.cpp", "router.hip", "expert_ffn.hip", "combine.hip", "probe.hip",
-               "grouped_gemm.hip"]
+               "pager.hip", "grouped_gemm.hip"]
 
 
 def _run(cmd):

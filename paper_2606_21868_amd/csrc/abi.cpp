@@ -94,6 +94,17 @@ struct wisp_ctx {
   uint64_t k_bytes[WISP_K_NUM] = {};
   int32_t fail_alloc_at = 0;
   int32_t alloc_counter = 0;
+  // device pager (WISP_PAGER_DEVICE): the slot tables in HBM are authoritative while it is on
+  int32_t pager = WISP_PAGER_HOST;
+  int32_t dev_cap = 0;               // C the device arrays are sized for
+  int32_t* d_pi = nullptr;           // [L][N]
+  int32_t* d_pinv = nullptr;         // [L][C]
+  uint64_t* d_tau = nullptr;         // [L][C]
+  uint64_t* d_clock = nullptr;       // [L]
+  uint64_t* d_slot_ptr = nullptr;    // [L][C] device addresses of the slots
+  FfnBatch* d_plan = nullptr;        // launch plan written by the device pager
+  uint32_t* d_stats = nullptr;       // [L][2] hits, misses of the current step
+  uint32_t* h_stats = nullptr;       // pinned copy
 
   uint8_t* master(int l, int e) const { return masters[l] + static_cast<size_t>(e) * master_stride; }
   int k() const { return desc.top_k; }
@@ -220,6 +231,11 @@ void free_ctx(wisp_ctx* c) {
   if (c->h) hipFree(c->h);
   if (c->buf) hipFree(c->buf);
   if (c->idx_pinned) hipHostFree(c->idx_pinned);
+  for (void* p : {static_cast<void*>(c->d_pi), static_cast<void*>(c->d_pinv), static_cast<void*>(c->d_tau),
+                  static_cast<void*>(c->d_clock), static_cast<void*>(c->d_slot_ptr), static_cast<void*>(c->d_plan),
+                  static_cast<void*>(c->d_stats)})
+    if (p) hipFree(p);
+  if (c->h_stats) hipHostFree(c->h_stats);
   delete c;
 }
 
@@ -234,10 +250,81 @@ wisp_status ensure_events(std::vector<hipEvent_t>& v, size_t n) {
 
 // Drained barrier: every fill and every FFN of the context has finished.
 wisp_status drain(wisp_ctx* c) {
+  if (c->pager == WISP_PAGER_DEVICE) WISP_HIP(hipDeviceSynchronize(), "hipDeviceSynchronize");
   WISP_HIP(hipStreamSynchronize(c->side), "hipStreamSynchronize(side)");
   for (auto& L : c->layers)
     if (L.use_ev_recorded) WISP_HIP(hipEventSynchronize(L.use_ev), "hipEventSynchronize(layer)");
   return WISP_OK;
+}
+
+// Copy every layer's slot table (and slot addresses) host -> device, resizing the device arrays
+// to the current cap.  Synchronous.
+wisp_status upload_tables(wisp_ctx* c) {
+  const int L = c->desc.n_layers, N = c->desc.n_experts, C = c->cap;
+  if (c->dev_cap != C) {
+    for (void** p : {reinterpret_cast<void**>(&c->d_pinv), reinterpret_cast<void**>(&c->d_tau),
+                     reinterpret_cast<void**>(&c->d_slot_ptr)}) {
+      if (*p) hipFree(*p);
+      *p = nullptr;
+    }
+    c->dev_cap = 0;
+    if (hipMalloc(reinterpret_cast<void**>(&c->d_pinv), sizeof(int32_t) * L * C) != hipSuccess ||
+        hipMalloc(reinterpret_cast<void**>(&c->d_tau), sizeof(uint64_t) * L * C) != hipSuccess ||
+        hipMalloc(reinterpret_cast<void**>(&c->d_slot_ptr), sizeof(uint64_t) * L * C) != hipSuccess)
+      return fail(WISP_E_NOMEM, "device pager tables");
+    c->dev_cap = C;
+  }
+  if (!c->d_pi) {
+    if (hipMalloc(reinterpret_cast<void**>(&c->d_pi), sizeof(int32_t) * L * N) != hipSuccess ||
+        hipMalloc(reinterpret_cast<void**>(&c->d_clock), sizeof(uint64_t) * L) != hipSuccess ||
+        hipMalloc(reinterpret_cast<void**>(&c->d_plan), sizeof(FfnBatch)) != hipSuccess ||
+        hipMalloc(reinterpret_cast<void**>(&c->d_stats), sizeof(uint32_t) * 2 * L) != hipSuccess ||
+        hipHostMalloc(reinterpret_cast<void**>(&c->h_stats), sizeof(uint32_t) * 2 * L, hipHostMallocDefault) != hipSuccess)
+      return fail(WISP_E_NOMEM, "device pager state");
+  }
+  std::vector<int32_t> pi(static_cast<size_t>(L) * N), pinv(static_cast<size_t>(L) * C);
+  std::vector<uint64_t> tau(static_cast<size_t>(L) * C), clk(L), sp(static_cast<size_t>(L) * C);
+  for (int l = 0; l < L; ++l) {
+    c->layers[l].table->export_state(&pi[static_cast<size_t>(l) * N], &pinv[static_cast<size_t>(l) * C],
+                                     &tau[static_cast<size_t>(l) * C], &clk[l]);
+    for (int s = 0; s < C; ++s) sp[static_cast<size_t>(l) * C + s] = reinterpret_cast<uint64_t>(c->layers[l].slot_mem[s]);
+  }
+  WISP_HIP(hipMemcpy(c->d_pi, pi.data(), sizeof(int32_t) * pi.size(), hipMemcpyHostToDevice), "upload pi");
+  WISP_HIP(hipMemcpy(c->d_pinv, pinv.data(), sizeof(int32_t) * pinv.size(), hipMemcpyHostToDevice), "upload pinv");
+  WISP_HIP(hipMemcpy(c->d_tau, tau.data(), sizeof(uint64_t) * tau.size(), hipMemcpyHostToDevice), "upload tau");
+  WISP_HIP(hipMemcpy(c->d_clock, clk.data(), sizeof(uint64_t) * clk.size(), hipMemcpyHostToDevice), "upload clock");
+  WISP_HIP(hipMemcpy(c->d_slot_ptr, sp.data(), sizeof(uint64_t) * sp.size(), hipMemcpyHostToDevice), "upload slots");
+  return WISP_OK;
+}
+
+// Copy the device slot tables back into the host tables.  Synchronous; call after drain().
+wisp_status download_tables(wisp_ctx* c) {
+  const int L = c->desc.n_layers, N = c->desc.n_experts, C = c->cap;
+  std::vector<int32_t> pi(static_cast<size_t>(L) * N), pinv(static_cast<size_t>(L) * C);
+  std::vector<uint64_t> tau(static_cast<size_t>(L) * C), clk(L);
+  WISP_HIP(hipDeviceSynchronize(), "hipDeviceSynchronize");
+  WISP_HIP(hipMemcpy(pi.data(), c->d_pi, sizeof(int32_t) * pi.size(), hipMemcpyDeviceToHost), "download pi");
+  WISP_HIP(hipMemcpy(pinv.data(), c->d_pinv, sizeof(int32_t) * pinv.size(), hipMemcpyDeviceToHost), "download pinv");
+  WISP_HIP(hipMemcpy(tau.data(), c->d_tau, sizeof(uint64_t) * tau.size(), hipMemcpyDeviceToHost), "download tau");
+  WISP_HIP(hipMemcpy(clk.data(), c->d_clock, sizeof(uint64_t) * clk.size(), hipMemcpyDeviceToHost), "download clock");
+  for (int l = 0; l < L; ++l)
+    c->layers[l].table->import_state(&pi[static_cast<size_t>(l) * N], &pinv[static_cast<size_t>(l) * C],
+                                     &tau[static_cast<size_t>(l) * C], clk[l]);
+  return WISP_OK;
+}
+
+// Run `body` on the host tables: with the device pager on, move them down first and back up after.
+template <typename F>
+wisp_status with_host_tables(wisp_ctx* c, F body) {
+  const bool dev = c->pager == WISP_PAGER_DEVICE;
+  wisp_status s;
+  if (dev) {
+    if ((s = drain(c)) != WISP_OK) return s;
+    if ((s = download_tables(c)) != WISP_OK) return s;
+  }
+  wisp_status r = body();
+  if (dev && (s = upload_tables(c)) != WISP_OK) return s;
+  return r;
 }
 
 // Enqueue the fills of chunk ci of `layer`'s pending plan on the side stream.
@@ -278,32 +365,36 @@ uint64_t ffn_bytes(const wisp_ctx* c, const FfnBatch& b, bool gateup) {
 }
 
 // Launch gate/up then down for a list of (expert blob, (token, rank) pairs), in batches of up to
-// kMaxItems items.  If `fin` asks for it, the last batch's down projection also does the combine
-// (when the shape allows the fused kernel); fin->done reports whether it did.
+// kMaxItems items; the per-(token, rank) outputs land in buf.
 struct Pair { int32_t t, out; };
 struct Work { const uint8_t* w; std::vector<Pair> pairs; };
-struct Finish {
-  bool want = false;
-  bool done = false;
-  int32_t T = 0;
-  const float* w = nullptr;
-  float* y = nullptr;
-};
 
-wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, hipStream_t st, Finish* fin) {
-  std::vector<FfnBatch> batches(1);
-  batches[0].n_items = 0;
-  batches[0].max_ntok = 0;
+wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, hipStream_t st) {
+  FfnBatch b;
+  b.n_items = 0;
+  b.max_ntok = 0;
+  auto flush = [&]() -> wisp_status {
+    if (b.n_items == 0) return WISP_OK;
+    LaunchTiming t1 = timing_begin(c, WISP_K_FFN_GATEUP);
+    WISP_HIP(launch_ffn_gateup(b, c->shape, x, c->h, st, t1), "ffn gate/up launch");
+    timing_end(c, t1, WISP_K_FFN_GATEUP, ffn_bytes(c, b, true));
+    LaunchTiming t2 = timing_begin(c, WISP_K_FFN_DOWN);
+    WISP_HIP(launch_ffn_down(b, c->shape, c->h, c->buf, st, t2), "ffn down launch");
+    timing_end(c, t2, WISP_K_FFN_DOWN, ffn_bytes(c, b, false));
+    b.n_items = 0;
+    b.max_ntok = 0;
+    return WISP_OK;
+  };
   for (const Work& wk : work) {
     for (size_t p0 = 0; p0 < wk.pairs.size(); p0 += kMaxTokPerItem) {
-      if (batches.back().n_items == kMaxItems) {
-        batches.emplace_back();
-        batches.back().n_items = 0;
-        batches.back().max_ntok = 0;
+      if (b.n_items == kMaxItems) {
+        wisp_status s = flush();
+        if (s != WISP_OK) return s;
       }
-      FfnBatch& b = batches.back();
       FfnItem& it = b.items[b.n_items++];
       it.w = wk.w;
+      it.src = nullptr;
+      it.fault = 0;
       it.ntok = static_cast<int32_t>(std::min<size_t>(kMaxTokPerItem, wk.pairs.size() - p0));
       for (int q = 0; q < kMaxTokPerItem; ++q) {
         const bool on = q < it.ntok;
@@ -313,51 +404,7 @@ wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, h
       b.max_ntok = std::max(b.max_ntok, it.ntok);
     }
   }
-  const int k = c->desc.top_k;
-  for (size_t bi = 0; bi < batches.size(); ++bi) {
-    FfnBatch& b = batches[bi];
-    if (b.n_items == 0) continue;
-    int16_t pairs = 0;
-    std::fill(std::begin(b.src), std::end(b.src), static_cast<int8_t>(-1));
-    for (int i = 0; i < b.n_items; ++i) {
-      b.pair_base[i] = pairs;
-      for (int t = 0; t < b.items[i].ntok; ++t) {
-        const int row = b.items[i].out[t];
-        if (row < kMaxRows) b.src[row] = static_cast<int8_t>(pairs + t);
-      }
-      pairs = static_cast<int16_t>(pairs + b.items[i].ntok);
-    }
-    LaunchTiming t1 = timing_begin(c, WISP_K_FFN_GATEUP);
-    WISP_HIP(launch_ffn_gateup(b, c->shape, x, c->h, st, t1), "ffn gate/up launch");
-    timing_end(c, t1, WISP_K_FFN_GATEUP, ffn_bytes(c, b, true));
-    const bool last = bi + 1 == batches.size();
-    const bool comb = fin && fin->want && last;
-    bool fused_ok = false;
-    if (fin && fin->T * (k + 1) <= kMaxRows) {
-      LaunchTiming t2 = timing_begin(c, WISP_K_FFN_DOWN);
-      hipError_t e = launch_ffn_down_combine(b, c->shape, c->h, c->buf, fin->T, k, c->desc.has_shared, fin->w, fin->y,
-                                             comb, st, t2);
-      if (e == hipSuccess) {
-        fused_ok = true;
-        uint64_t by = ffn_bytes(c, b, false);
-        if (comb)
-          by += static_cast<uint64_t>(fin->T) * c->desc.d_model * 4 * (k + c->desc.has_shared + 1);
-        timing_end(c, t2, WISP_K_FFN_DOWN, by);
-        if (comb) fin->done = true;
-      } else if (e != hipErrorNotSupported) {
-        return fail(WISP_E_HIP, std::string("ffn down launch: ") + hipGetErrorString(e));
-      } else {
-        hipGetLastError();
-        if (t2.start) { c->ev_pool.push_back(t2.start); c->ev_pool.push_back(t2.stop); }
-      }
-    }
-    if (!fused_ok) {
-      LaunchTiming t2 = timing_begin(c, WISP_K_FFN_DOWN);
-      WISP_HIP(launch_ffn_down(b, c->shape, c->h, c->buf, st, t2), "ffn down launch");
-      timing_end(c, t2, WISP_K_FFN_DOWN, ffn_bytes(c, b, false));
-    }
-  }
-  return WISP_OK;
+  return flush();
 }
 
 }  // namespace
@@ -462,7 +509,7 @@ wisp_status wisp_expert_host_ptr(wisp_ctx* ctx, int32_t layer, int32_t expert, v
   return WISP_OK;
 }
 
-wisp_status wisp_masters_ready(wisp_ctx* ctx) {
+static wisp_status masters_ready_host(wisp_ctx* ctx) {
   wisp_status s = check_ctx(ctx);
   if (s != WISP_OK) return s;
   s = drain(ctx);
@@ -487,7 +534,7 @@ wisp_status wisp_router_weights(wisp_ctx* ctx, int32_t layer, const float* w_r_d
   return WISP_OK;
 }
 
-wisp_status wisp_set_budget(wisp_ctx* ctx, uint64_t expert_bytes, int32_t* cap_out) {
+static wisp_status set_budget_host(wisp_ctx* ctx, uint64_t expert_bytes, int32_t* cap_out) {
   wisp_status s = check_ctx(ctx);
   if (s != WISP_OK) return s;
   const uint64_t a = static_cast<uint64_t>(ctx->desc.n_layers) * ctx->blob.bytes;
@@ -568,7 +615,7 @@ wisp_status wisp_set_budget(wisp_ctx* ctx, uint64_t expert_bytes, int32_t* cap_o
   return WISP_OK;
 }
 
-wisp_status wisp_preload(wisp_ctx* ctx) {
+static wisp_status preload_host(wisp_ctx* ctx) {
   wisp_status s = check_ctx(ctx);
   if (s != WISP_OK) return s;
   if (ctx->cap < 1) return fail(WISP_E_STATE, "no expert budget set");
@@ -589,6 +636,59 @@ wisp_status wisp_preload(wisp_ctx* ctx) {
                    "hipMemcpyAsync(preload)");
   }
   WISP_HIP(hipStreamSynchronize(ctx->side), "hipStreamSynchronize(side)");
+  return WISP_OK;
+}
+
+wisp_status wisp_masters_ready(wisp_ctx* ctx) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (ctx->pager == WISP_PAGER_DEVICE && ctx->cap > 0)
+    return with_host_tables(ctx, [&] { return masters_ready_host(ctx); });
+  return masters_ready_host(ctx);
+}
+
+wisp_status wisp_set_budget(wisp_ctx* ctx, uint64_t expert_bytes, int32_t* cap_out) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (ctx->pager == WISP_PAGER_DEVICE) {
+    const uint64_t C = expert_bytes / (static_cast<uint64_t>(ctx->desc.n_layers) * ctx->blob.bytes);
+    if (C < static_cast<uint64_t>(ctx->desc.max_tokens) * ctx->desc.top_k)
+      return fail(WISP_E_INVAL, "the device pager needs C >= max_tokens * k; switch to the host pager first");
+    return with_host_tables(ctx, [&] { return set_budget_host(ctx, expert_bytes, cap_out); });
+  }
+  return set_budget_host(ctx, expert_bytes, cap_out);
+}
+
+wisp_status wisp_preload(wisp_ctx* ctx) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (ctx->pager == WISP_PAGER_DEVICE) return with_host_tables(ctx, [&] { return preload_host(ctx); });
+  return preload_host(ctx);
+}
+
+wisp_status wisp_set_pager(wisp_ctx* ctx, int32_t pager) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (pager != WISP_PAGER_HOST && pager != WISP_PAGER_DEVICE) return fail(WISP_E_INVAL, "unknown pager");
+  if (pager == ctx->pager) return WISP_OK;
+  for (auto& L : ctx->layers)
+    if (L.pending) return fail(WISP_E_STATE, "a page-in is pending");
+  if (pager == WISP_PAGER_DEVICE) {
+    const auto& d = ctx->desc;
+    if (ctx->cap < 1) return fail(WISP_E_STATE, "no expert budget set");
+    if (d.max_tokens > 4) return fail(WISP_E_INVAL, "the device pager handles max_tokens <= 4");
+    if (ctx->cap < d.max_tokens * d.top_k)
+      return fail(WISP_E_INVAL, "the device pager needs C >= max_tokens * k (one Algorithm 1 step per layer-step)");
+    if (!ffn_dev_supported(ctx->shape, d.max_tokens, d.top_k, d.has_shared))
+      return fail(WISP_E_INVAL, "layer shape not supported by the device-planned FFN kernels");
+    if ((s = drain(ctx)) != WISP_OK) return s;
+    if ((s = upload_tables(ctx)) != WISP_OK) return s;
+    ctx->pager = WISP_PAGER_DEVICE;
+  } else {
+    if ((s = drain(ctx)) != WISP_OK) return s;
+    if ((s = download_tables(ctx)) != WISP_OK) return s;
+    ctx->pager = WISP_PAGER_HOST;
+  }
   return WISP_OK;
 }
 
@@ -659,6 +759,7 @@ wisp_status wisp_page_in(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, 
   if (!ids_host) return fail(WISP_E_INVAL, "ids_host is NULL");
   if (T < 1 || T > ctx->desc.max_tokens) return fail(WISP_E_INVAL, "T out of [1, max_tokens]");
   if (ctx->cap < 1) return fail(WISP_E_STATE, "no expert budget set");
+  if (ctx->pager == WISP_PAGER_DEVICE) return fail(WISP_E_STATE, "the device pager pages inside wisp_decode_step");
   LayerState& L = ctx->layers[layer];
   if (L.pending) return fail(WISP_E_STATE, "previous page-in of this layer not consumed by wisp_moe_forward");
   const int32_t n = T * ctx->desc.top_k;
@@ -699,6 +800,7 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
   if (s != WISP_OK) return s;
   if ((s = check_layer(ctx, layer)) != WISP_OK) return s;
   if (!x_dev || !w_dev || !y_dev) return fail(WISP_E_INVAL, "NULL device pointer");
+  if (ctx->pager == WISP_PAGER_DEVICE) return fail(WISP_E_STATE, "the device pager pages inside wisp_decode_step");
   LayerState& L = ctx->layers[layer];
   if (!L.pending) return fail(WISP_E_STATE, "no pending page-in for this layer");
   if (T != L.T) return fail(WISP_E_INVAL, "T differs from the page-in");
@@ -713,10 +815,6 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
       for (int32_t e : L.plan.chunks[ci].experts) found |= (e == L.ids[i]);
     if (!found) return fail(WISP_E_NOT_RESIDENT, "routed expert missing from the page-in plan");
   }
-  Finish fin;
-  fin.T = T;
-  fin.w = w_dev;
-  fin.y = y_dev;
   for (size_t ci = 0; ci < nch; ++ci) {
     const ChunkPlan& cp = L.plan.chunks[ci];
     if (ci > 0 && (s = issue_fills(ctx, layer, ci)) != WISP_OK) return s;
@@ -735,24 +833,19 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
       for (int32_t t = 0; t < T; ++t) wk.pairs.push_back({t, t * rows + k});
       hits.push_back(std::move(wk));
     }
-    const bool last_chunk = ci + 1 == nch;
-    fin.want = last_chunk && faults.empty();
-    if (!hits.empty() && (s = run_ffn(ctx, hits, x_dev, sm, &fin)) != WISP_OK) return s;
+    if (!hits.empty() && (s = run_ffn(ctx, hits, x_dev, sm)) != WISP_OK) return s;
     if (!faults.empty()) {
       WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[ci], 0), "hipStreamWaitEvent(fill)");
-      fin.want = last_chunk;
-      if ((s = run_ffn(ctx, faults, x_dev, sm, &fin)) != WISP_OK) return s;
+      if ((s = run_ffn(ctx, faults, x_dev, sm)) != WISP_OK) return s;
     }
     if (ci + 1 < nch) WISP_HIP(hipEventRecord(L.chunk_ev[ci], sm), "hipEventRecord(chunk)");
   }
-  if (!fin.done) {
-    LaunchTiming tc = timing_begin(ctx, WISP_K_COMBINE);
-    WISP_HIP(launch_combine(T, k, ctx->desc.d_model, ctx->desc.has_shared, w_dev, ctx->buf, y_dev, sm, tc),
-             "combine launch");
-    timing_end(ctx, tc, WISP_K_COMBINE,
-               static_cast<uint64_t>(T) * ctx->desc.d_model * 4 * (k + ctx->desc.has_shared + 1) +
-                   static_cast<uint64_t>(T) * k * 4);
-  }
+  LaunchTiming tc = timing_begin(ctx, WISP_K_COMBINE);
+  WISP_HIP(launch_combine(T, k, ctx->desc.d_model, ctx->desc.has_shared, w_dev, ctx->buf, y_dev, sm, tc),
+           "combine launch");
+  timing_end(ctx, tc, WISP_K_COMBINE,
+             static_cast<uint64_t>(T) * ctx->desc.d_model * 4 * (k + ctx->desc.has_shared + 1) +
+                 static_cast<uint64_t>(T) * k * 4);
   WISP_HIP(hipEventRecord(L.use_ev, sm), "hipEventRecord(use)");
   L.use_ev_recorded = true;
   L.pending = false;
@@ -774,6 +867,61 @@ wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_
   if (T < 1 || T > ctx->desc.max_tokens) return fail(WISP_E_INVAL, "T out of [1, max_tokens]");
   const auto& d = ctx->desc;
   const size_t xs = static_cast<size_t>(T) * d.d_model * ctx->x_elem();
+  if (ctx->pager == WISP_PAGER_DEVICE) {
+    hipStream_t sm = static_cast<hipStream_t>(stream);
+    const int max_items = T * d.top_k + d.has_shared;
+    const int C = ctx->cap;
+    for (int32_t l = 0; l < d.n_layers; ++l) {
+      LayerState& L = ctx->layers[l];
+      if (!L.wr) return fail(WISP_E_STATE, "router weights not set for this layer");
+      const void* xl = static_cast<const uint8_t*>(x_dev) + l * xs;
+      int32_t* il = idx_dev + static_cast<size_t>(l) * T * d.top_k;
+      float* wl = w_dev + static_cast<size_t>(l) * T * d.top_k;
+      float* yl = y_dev + static_cast<size_t>(l) * T * d.d_model;
+      LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_LOGITS);
+      WISP_HIP(launch_router_logits(L.wr, xl, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, sm, t1),
+               "router logits launch");
+      timing_end(ctx, t1, WISP_K_ROUTER_LOGITS, static_cast<uint64_t>(d.n_experts) * d.d_model * 4);
+      LaunchTiming t2 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
+      WISP_HIP(launch_select_page(ctx->logits, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, il, wl,
+                                  ctx->d_pi + static_cast<size_t>(l) * d.n_experts,
+                                  ctx->d_pinv + static_cast<size_t>(l) * C, ctx->d_tau + static_cast<size_t>(l) * C,
+                                  ctx->d_clock + l, C, ctx->d_slot_ptr + static_cast<size_t>(l) * C, ctx->masters[l],
+                                  ctx->master_stride, L.shared_dev, d.has_shared, ctx->d_plan, ctx->d_stats + 2 * l,
+                                  sm, t2),
+               "device pager launch");
+      timing_end(ctx, t2, WISP_K_ROUTER_SELECT, 0);
+      LaunchTiming t3 = timing_begin(ctx, WISP_K_FFN_GATEUP);
+      LaunchTiming t4 = timing_begin(ctx, WISP_K_FFN_DOWN);
+      WISP_HIP(launch_ffn_dev(ctx->d_plan, max_items, ctx->shape, xl, ctx->h, ctx->buf, sm, t3, t4),
+               "device-planned FFN launch");
+      timing_end(ctx, t3, WISP_K_FFN_GATEUP, 0);
+      timing_end(ctx, t4, WISP_K_FFN_DOWN, 0);
+      LaunchTiming t5 = timing_begin(ctx, WISP_K_COMBINE);
+      WISP_HIP(launch_combine(T, d.top_k, d.d_model, d.has_shared, wl, ctx->buf, yl, sm, t5), "combine launch");
+      timing_end(ctx, t5, WISP_K_COMBINE, 0);
+    }
+    WISP_HIP(hipMemcpyAsync(ctx->h_stats, ctx->d_stats, sizeof(uint32_t) * 2 * d.n_layers, hipMemcpyDeviceToHost, sm),
+             "stats copy");
+    WISP_HIP(hipStreamSynchronize(sm), "hipStreamSynchronize");
+    if (ctx->profiling) harvest(ctx, false);
+    for (int32_t l = 0; l < d.n_layers; ++l) {
+      wisp_page_stats ps{};
+      ps.hits = ctx->h_stats[2 * l];
+      ps.misses = ctx->h_stats[2 * l + 1];
+      ps.chunks = (ps.hits + ps.misses) > 0 ? 1 : 0;
+      ps.steps = 1;
+      ps.h2d_bytes = static_cast<uint64_t>(ps.misses) * ctx->blob.bytes;
+      LayerState& L = ctx->layers[l];
+      L.cum.hits += ps.hits;
+      L.cum.misses += ps.misses;
+      L.cum.chunks += ps.chunks;
+      L.cum.steps += 1;
+      L.cum.h2d_bytes += ps.h2d_bytes;
+      if (st) st[l] = ps;
+    }
+    return WISP_OK;
+  }
   for (int32_t l = 0; l < d.n_layers; ++l) {
     const void* xl = static_cast<const uint8_t*>(x_dev) + l * xs;
     int32_t* il = idx_dev + static_cast<size_t>(l) * T * d.top_k;
@@ -811,6 +959,9 @@ wisp_status wisp_slot_of(wisp_ctx* ctx, int32_t layer, int32_t expert, int32_t* 
   wisp_status s = check_layer(ctx, layer);
   if (s != WISP_OK) return s;
   if (expert < 0 || expert >= ctx->desc.n_experts) return fail(WISP_E_INVAL, "expert out of range");
+  if (ctx->pager == WISP_PAGER_DEVICE) {
+    if ((s = check_ctx(ctx)) != WISP_OK || (s = drain(ctx)) != WISP_OK || (s = download_tables(ctx)) != WISP_OK) return s;
+  }
   const auto& t = ctx->layers[layer].table;
   *slot = t ? t->slot_of(expert) : -1;
   return WISP_OK;
@@ -821,6 +972,9 @@ wisp_status wisp_expert_in_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, int3
   wisp_status s = check_layer(ctx, layer);
   if (s != WISP_OK) return s;
   if (slot < 0 || slot >= ctx->cap) return fail(WISP_E_INVAL, "slot out of range");
+  if (ctx->pager == WISP_PAGER_DEVICE) {
+    if ((s = check_ctx(ctx)) != WISP_OK || (s = drain(ctx)) != WISP_OK || (s = download_tables(ctx)) != WISP_OK) return s;
+  }
   *expert = ctx->layers[layer].table->expert_in(slot);
   return WISP_OK;
 }

@@ -12,7 +12,9 @@
 // where the workgroup has staged the item's input rows.  Group partial sums are reduced with
 // cross-lane shuffles.  Phase 1 (gate/up) reads the W1 and W3 rows of the same output index
 // together and writes h = silu(a) * b; phase 2 (down) reads W2 rows and writes the per-(token,
-// rank) outputs that the combine kernel sums in rank order.  Every (token, rank) result is
+// rank) outputs that the combine kernel sums in rank order.  Both phases give every item its own
+// row blocks (a grid of items x row blocks): many waves with few loads each hide HBM latency
+// better than few waves that each walk every expert.  Every (token, rank) result is
 // computed by the same instructions in the same order whatever the batch composition, so a
 // paged run is bit-identical to a fully resident one.
 #include <hip/hip_ext.h>
@@ -107,22 +109,20 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   return static_cast<uint16_t>(u >> 16);
 }
 
-// One launch: blockIdx.x = item * blocks_per_item + row block.  K = inner (row) length, R = rows.
-// off0/off1: byte offsets of the matrix (matrices) in the blob; soff0/soff1: fp8 scale tables.
+// Rows [r_begin, r_end) of one item, by one workgroup.  Weights and fp8 scales are read from the
+// blob at `rd`; if `wr` is not null every loaded 16-byte chunk is also stored at the same offset
+// of `wr` (a faulted expert streamed from its host master into its slot while being used).
+// K = inner (row) length, R = rows; off0/off1: byte offsets of the matrix (matrices) in the blob;
+// soff0/soff1: fp8 scale tables.  The arithmetic is the same whatever rd / wr are.
 template <int WT, int IT, int MODE, int LPR, int NLT>
-__global__ void __launch_bounds__(256) ffn_rows(const FfnBatch B, const uint8_t* __restrict__ vin, int vin_stride,
-                                                int K, int R, int rows_per_wg, int blocks_per_item, uint32_t off0,
-                                                uint32_t off1, uint32_t soff0, uint32_t soff1,
-                                                uint8_t* __restrict__ out, int out_stride) {
+__device__ __forceinline__ void rows_body(const FfnItem& it, const uint8_t* rd, uint8_t* wr,
+                                          const uint8_t* __restrict__ vin, int vin_stride, int K, int R, int r_begin,
+                                          int r_end, uint32_t off0, uint32_t off1, uint32_t soff0, uint32_t soff1,
+                                          uint8_t* __restrict__ out, int out_stride, uint8_t* lds) {
   constexpr int EPL = WFmt<WT>::EPL;
   constexpr int RPW = 64 / LPR;                 // rows a wave covers at once
   constexpr int IS = IT == DT_F32 ? 4 : 2;      // input element bytes
   constexpr int U = NLT > 0 ? NLT : 4;          // chunks in flight per lane
-  extern __shared__ __align__(16) uint8_t lds[];
-
-  const int item_idx = blockIdx.x / blocks_per_item;
-  const int rb = blockIdx.x - item_idx * blocks_per_item;
-  const FfnItem& it = B.items[item_idx];
   const int ntok = it.ntok;
   const int row_bytes = K * IS;
 
@@ -131,17 +131,15 @@ __global__ void __launch_bounds__(256) ffn_rows(const FfnBatch B, const uint8_t*
   const int sub = lane / LPR;
   const int sl = lane - sub * LPR;
   const int NL = NLT > 0 ? NLT : (K / EPL) / LPR;
-  const int r_begin = rb * rows_per_wg;
-  const int r_end = min(R, r_begin + rows_per_wg);
-  const uint8_t* wbase0 = it.w + off0;
-  const uint8_t* wbase1 = it.w + off1;
-  const uint16_t* sc0 = reinterpret_cast<const uint16_t*>(it.w + soff0);
-  const uint16_t* sc1 = reinterpret_cast<const uint16_t*>(it.w + soff1);
+  const uint8_t* wbase0 = rd + off0;
+  const uint8_t* wbase1 = rd + off1;
+  const uint16_t* sc0 = reinterpret_cast<const uint16_t*>(rd + soff0);
+  const uint16_t* sc1 = reinterpret_cast<const uint16_t*>(rd + soff1);
   const int scols = K / 128;
   const size_t row_stride_b = static_cast<size_t>(K) * (WT == DT_F32 ? 4 : WT == DT_BF16 ? 2 : 1);
 
   // fully unrolled shapes: the first row pass issues its weight loads before the input rows are
-  // staged, so the HBM fetch overlaps the staging
+  // staged, so the weight fetch overlaps the staging
   const int rbase0 = r_begin + wave * RPW;
   uint4 pa[NLT > 0 ? NLT : 1], pb[NLT > 0 ? NLT : 1];
   if constexpr (NLT > 0) {
@@ -192,6 +190,18 @@ __global__ void __launch_bounds__(256) ffn_rows(const FfnBatch B, const uint8_t*
           if (NLT > 0 || m < NL) {
             a[u] = row0[m * LPR + sl];
             if constexpr (MODE == MODE_GATEUP) b[u] = row1[m * LPR + sl];
+          }
+        }
+      }
+      if (wr && valid) {
+        uint4* w0 = reinterpret_cast<uint4*>(wr + off0 + rr * row_stride_b);
+        uint4* w1 = reinterpret_cast<uint4*>(wr + off1 + rr * row_stride_b);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int m = m0 + u;
+          if (NLT > 0 || m < NL) {
+            w0[m * LPR + sl] = a[u];
+            if constexpr (MODE == MODE_GATEUP) w1[m * LPR + sl] = b[u];
           }
         }
       }
@@ -257,6 +267,90 @@ __global__ void __launch_bounds__(256) ffn_rows(const FfnBatch B, const uint8_t*
       }
     }
   }
+}
+
+// Host-planned launch: blockIdx.x = item * blocks_per_item + row block; the items come with the
+// launch (kernel arguments).
+template <int WT, int IT, int MODE, int LPR, int NLT>
+__global__ void __launch_bounds__(256) ffn_rows(const FfnBatch B, const uint8_t* __restrict__ vin, int vin_stride,
+                                                int K, int R, int rows_per_wg, int blocks_per_item, uint32_t off0,
+                                                uint32_t off1, uint32_t soff0, uint32_t soff1,
+                                                uint8_t* __restrict__ out, int out_stride) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int item_idx = blockIdx.x / blocks_per_item;
+  const int rb = blockIdx.x - item_idx * blocks_per_item;
+  const FfnItem& it = B.items[item_idx];
+  const int r_begin = rb * rows_per_wg;
+  rows_body<WT, IT, MODE, LPR, NLT>(it, it.w, nullptr, vin, vin_stride, K, R, r_begin, min(R, r_begin + rows_per_wg),
+                                    off0, off1, soff0, soff1, out, out_stride, lds);
+}
+
+// Device-planned gate/up: the item list was written to HBM by the device pager of this layer.
+// Per item slot, bpi workgroups: a resident expert uses them as row blocks of rows_hit rows; a
+// faulted expert uses fault_wgs of them to stream its W1/W3 rows from the host master (computing
+// h and filling the slot) and copy_wgs more to copy the rest of its blob (W2 and fp8 scales)
+// host -> slot; the others exit.  The PCIe stream needs few workgroups, which leaves the CUs to
+// the resident experts meanwhile.
+template <int WT, int IT, int LPR, int NLT>
+__global__ void __launch_bounds__(256) ffn_gateup_dev(const FfnBatch* __restrict__ P, const uint8_t* __restrict__ vin,
+                                                      int d, int I, int bpi, int rows_hit, int fault_wgs, int copy_wgs,
+                                                      uint32_t off1, uint32_t off3, uint32_t soff1, uint32_t soff3,
+                                                      uint32_t copy_off, uint32_t copy_bytes, uint8_t* __restrict__ h) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  constexpr int RPW = 64 / LPR;
+  const int item_idx = blockIdx.x / bpi;
+  const int j = blockIdx.x - item_idx * bpi;
+  if (item_idx >= P->n_items) return;
+  const FfnItem& it = P->items[item_idx];
+  if (!it.fault) {
+    const int r_begin = j * rows_hit;
+    if (r_begin >= I) return;
+    rows_body<WT, IT, MODE_GATEUP, LPR, NLT>(it, it.w, nullptr, vin, d, d, I, r_begin, min(I, r_begin + rows_hit),
+                                             off1, off3, soff1, soff3, h, I, lds);
+  } else if (j < fault_wgs) {
+    int rows = (I + fault_wgs - 1) / fault_wgs;
+    rows = (rows + 4 * RPW - 1) / (4 * RPW) * (4 * RPW);
+    const int r_begin = j * rows;
+    if (r_begin >= I) return;
+    rows_body<WT, IT, MODE_GATEUP, LPR, NLT>(it, it.src, const_cast<uint8_t*>(it.w), vin, d, d, I, r_begin,
+                                             min(I, r_begin + rows), off1, off3, soff1, soff3, h, I, lds);
+  } else if (j < fault_wgs + copy_wgs) {
+    // copy [copy_off, copy_off + copy_bytes) host -> slot, four 16-byte loads in flight per thread
+    const int q = j - fault_wgs;
+    const size_t n16 = copy_bytes / 16;
+    const size_t per = (n16 + copy_wgs - 1) / copy_wgs;
+    const size_t c0 = static_cast<size_t>(q) * per;
+    const size_t c1 = c0 + per < n16 ? c0 + per : n16;
+    const uint4* src = reinterpret_cast<const uint4*>(it.src + copy_off);
+    uint4* dst = reinterpret_cast<uint4*>(const_cast<uint8_t*>(it.w) + copy_off);
+    size_t i = c0 + threadIdx.x;
+    for (; i + 768 < c1; i += 1024) {
+      const uint4 a = src[i], b = src[i + 256], c = src[i + 512], e = src[i + 768];
+      dst[i] = a; dst[i + 256] = b; dst[i + 512] = c; dst[i + 768] = e;
+    }
+    for (; i < c1; i += 256) dst[i] = src[i];
+    if (q == copy_wgs - 1) {
+      for (size_t b = n16 * 16 + threadIdx.x; b < copy_bytes; b += 256)
+        const_cast<uint8_t*>(it.w)[copy_off + b] = it.src[copy_off + b];
+    }
+  }
+}
+
+// Device-planned down projection: per item slot, row blocks of W2 (every expert of the step is
+// resident by now; faulted ones were filled by the gate/up kernel).
+template <int WT, int IT, int LPR, int NLT>
+__global__ void __launch_bounds__(256) ffn_down_dev(const FfnBatch* __restrict__ P, const uint8_t* __restrict__ h,
+                                                    int d, int I, int bpi, int rows_per_wg, uint32_t off2,
+                                                    uint32_t soff2, float* __restrict__ buf) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int item_idx = blockIdx.x / bpi;
+  const int rb = blockIdx.x - item_idx * bpi;
+  if (item_idx >= P->n_items) return;
+  const FfnItem& it = P->items[item_idx];
+  const int r_begin = rb * rows_per_wg;
+  if (r_begin >= d) return;
+  rows_body<WT, IT, MODE_DOWN, LPR, NLT>(it, it.w, nullptr, h, I, I, d, r_begin, min(d, r_begin + rows_per_wg), off2,
+                                         off2, soff2, soff2, reinterpret_cast<uint8_t*>(buf), d, lds);
 }
 
 using RowsKernel = void (*)(const FfnBatch, const uint8_t*, int, int, int, int, int, uint32_t, uint32_t, uint32_t,
@@ -349,152 +443,6 @@ hipError_t launch_rows(int mode, const FfnBatch& b, const FfnShape& s, const voi
   return hipGetLastError();
 }
 
-// Down projection for all items of a launch, one block of output rows per workgroup, fused with
-// the gate-weighted combine.  Each row group of LPR lanes reads the W2 row of IG items at once
-// (IG * NL 16-byte loads in flight per lane) and dots it with every token's h row (LDS).
-template <int WT, int IT, int LPR, int NL, int IG>
-__global__ void __launch_bounds__(256) ffn_down_combine(const FfnBatch B, const uint8_t* __restrict__ h, int I,
-                                                        int d, int rows_per_wg, uint32_t off2, uint32_t soff2,
-                                                        float* __restrict__ buf, int T, int k, int has_shared,
-                                                        const float* __restrict__ gates, float* __restrict__ y,
-                                                        int combine) {
-  constexpr int EPL = WFmt<WT>::EPL;
-  constexpr int RPW = 64 / LPR;
-  constexpr int IS = IT == DT_F32 ? 4 : 2;
-  constexpr int ES = WT == DT_F32 ? 4 : WT == DT_BF16 ? 2 : 1;
-  extern __shared__ __align__(16) uint8_t lds[];
-  const int n_items = B.n_items;
-  const int n_pairs = B.pair_base[n_items - 1] + B.items[n_items - 1].ntok;
-  const int row_bytes = I * IS;
-  float* outl = reinterpret_cast<float*>(lds + static_cast<size_t>(n_pairs) * row_bytes);  // [pair][local row]
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int sub = lane / LPR, sl = lane - sub * LPR;
-  const int r0 = blockIdx.x * rows_per_wg;
-  const int r1 = min(d, r0 + rows_per_wg);
-  const int scols = I / 128;
-  const int rows = k + 1;
-  const int nr = r1 - r0;
-
-  // before anything waits: the first pass's W2 loads of the first item group, and the combine
-  // inputs produced by earlier launches (one (token, row) per thread: T * nr <= 256)
-  const int rbase0 = r0 + wave * RPW;
-  uint4 pre[IG][NL];
-  {
-    const int r = rbase0 + sub;
-    const int rr = r < r1 ? r : r0;
-    if (rbase0 < r1) {
-#pragma unroll
-      for (int u = 0; u < IG; ++u) {
-        if (u >= n_items) break;
-        const uint4* row = reinterpret_cast<const uint4*>(B.items[u].w + off2 + static_cast<size_t>(rr) * I * ES);
-#pragma unroll
-        for (int m = 0; m < NL; ++m) pre[u][m] = row[m * LPR + sl];
-      }
-    }
-  }
-  float cprev[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  float cshared = 0.f;
-  if (combine && static_cast<int>(threadIdx.x) < T * nr) {
-    const int t = threadIdx.x / nr, r = r0 + threadIdx.x % nr;
-    for (int j = 0; j < k; ++j)
-      if (B.src[t * rows + j] < 0) cprev[j] = buf[static_cast<size_t>(t * rows + j) * d + r];
-    if (has_shared && B.src[t * rows + k] < 0) cshared = buf[static_cast<size_t>(t * rows + k) * d + r];
-  }
-
-  // stage every (item, token) h row
-  for (int i = 0; i < n_items; ++i) {
-    const FfnItem& it = B.items[i];
-    for (int t = 0; t < it.ntok; ++t) {
-      const uint4* src = reinterpret_cast<const uint4*>(h + static_cast<size_t>(it.out[t]) * row_bytes);
-      uint4* dst = reinterpret_cast<uint4*>(lds + static_cast<size_t>(B.pair_base[i] + t) * row_bytes);
-      for (int c = threadIdx.x; c < row_bytes / 16; c += 256) dst[c] = src[c];
-    }
-  }
-  __syncthreads();
-
-  for (int rbase = rbase0; rbase < r1; rbase += 4 * RPW) {
-    const int r = rbase + sub;
-    const bool valid = r < r1;
-    const int rr = valid ? r : r0;
-    for (int i0 = 0; i0 < n_items; i0 += IG) {
-      uint4 a[IG][NL];
-      if (rbase == rbase0 && i0 == 0) {
-#pragma unroll
-        for (int u = 0; u < IG; ++u)
-#pragma unroll
-          for (int m = 0; m < NL; ++m) a[u][m] = pre[u][m];
-      } else {
-#pragma unroll
-        for (int u = 0; u < IG; ++u) {
-          if (i0 + u >= n_items) break;
-          const uint4* row = reinterpret_cast<const uint4*>(B.items[i0 + u].w + off2 + static_cast<size_t>(rr) * I * ES);
-#pragma unroll
-          for (int m = 0; m < NL; ++m) a[u][m] = row[m * LPR + sl];
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < IG; ++u) {
-        if (i0 + u >= n_items) break;
-        const FfnItem& it = B.items[i0 + u];
-        const uint16_t* sc = reinterpret_cast<const uint16_t*>(it.w + soff2);
-        float acc[kMaxTokPerItem] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int m = 0; m < NL; ++m) {
-          const int col = (m * LPR + sl) * EPL;
-          float wv[EPL];
-          decode_chunk<WT>(a[u][m], wv);
-          float s2 = 1.f;
-          if constexpr (WT == DT_FP8) s2 = __uint_as_float(static_cast<uint32_t>(sc[(rr / 128) * scols + col / 128]) << 16);
-#pragma unroll
-          for (int t = 0; t < kMaxTokPerItem; ++t) {
-            if (t >= it.ntok) break;
-            float xv[EPL];
-            lds_chunk<IT, EPL>(lds + static_cast<size_t>(B.pair_base[i0 + u] + t) * row_bytes, col, xv);
-            if constexpr (WT == DT_FP8) {
-              float p = 0.f;
-#pragma unroll
-              for (int e = 0; e < EPL; ++e) p = fmaf(wv[e], xv[e], p);
-              acc[t] = fmaf(s2, p, acc[t]);
-            } else {
-#pragma unroll
-              for (int e = 0; e < EPL; ++e) acc[t] = fmaf(wv[e], xv[e], acc[t]);
-            }
-          }
-        }
-#pragma unroll
-        for (int t = 0; t < kMaxTokPerItem; ++t) {
-          if (t >= it.ntok) break;
-#pragma unroll
-          for (int off = LPR / 2; off > 0; off >>= 1) acc[t] += __shfl_xor(acc[t], off, 64);
-          if (valid && sl == 0) {
-            if (combine) outl[(B.pair_base[i0 + u] + t) * rows_per_wg + (r - r0)] = acc[t];
-            else buf[static_cast<size_t>(it.out[t]) * d + r] = acc[t];
-          }
-        }
-      }
-    }
-  }
-  if (!combine) return;
-  __syncthreads();
-  if (static_cast<int>(threadIdx.x) < T * nr) {
-    const int t = threadIdx.x / nr, lr = threadIdx.x % nr;
-    float acc = 0.f;
-    for (int j = 0; j < k; ++j) {
-      const int p = B.src[t * rows + j];
-      const float o = p >= 0 ? outl[p * rows_per_wg + lr] : cprev[j];
-      acc = fmaf(gates[t * k + j], o, acc);
-    }
-    if (has_shared) {
-      const int p = B.src[t * rows + k];
-      acc += p >= 0 ? outl[p * rows_per_wg + lr] : cshared;
-    }
-    y[static_cast<size_t>(t) * d + r0 + lr] = acc;
-  }
-}
-
-using DownKernel = void (*)(const FfnBatch, const uint8_t*, int, int, int, uint32_t, uint32_t, float*, int, int, int,
-                            const float*, float*, int);
-
 }  // namespace
 
 hipError_t launch_ffn_gateup(const FfnBatch& b, const FfnShape& s, const void* x, void* h, hipStream_t st,
@@ -507,44 +455,97 @@ hipError_t launch_ffn_down(const FfnBatch& b, const FfnShape& s, const void* h, 
   return launch_rows(MODE_DOWN, b, s, h, s.blob.I, buf, s.blob.d, st, tm);
 }
 
-hipError_t launch_ffn_down_combine(const FfnBatch& b, const FfnShape& s, const void* h, float* buf, int T, int k,
-                                   int has_shared, const float* w, float* y, bool combine, hipStream_t st,
-                                   const LaunchTiming& tm) {
-  if (b.n_items <= 0) return hipSuccess;
+namespace {
+// Shapes with a device-planned path: (w dtype, h dtype, d lanes/loads, I lanes/loads).
+struct DevShape { int lpr_g, nl_g, lpr_d, nl_d; };
+bool dev_shape(const FfnShape& s, DevShape* o) {
   const BlobLayout& L = s.blob;
-  const int WT = L.w_dtype, IT = s.h_dtype;
-  const int EPL = WT == DT_F32 ? 4 : WT == DT_BF16 ? 8 : 16;
-  const int chunks = L.I / EPL;
-  const int lpr = pick_lpr(chunks);
-  if (lpr == 0) return hipErrorNotSupported;
-  const int nl = chunks / lpr;
-  DownKernel kern = nullptr;
-#define WISP_D(W, X, LP, N, G) \
-  if (WT == W && IT == X && lpr == LP && nl == N) kern = &ffn_down_combine<W, X, LP, N, G>;
-  WISP_D(DT_BF16, DT_BF16, 32, 3, 8)   // I = 768
-  WISP_D(DT_FP8, DT_BF16, 64, 2, 8)    // I = 2048
-  WISP_D(DT_F32, DT_F32, 64, 2, 8)     // I = 512
-  WISP_D(DT_BF16, DT_BF16, 32, 1, 8)   // I = 256
-  WISP_D(DT_BF16, DT_BF16, 16, 1, 8)   // I = 128
-  WISP_D(DT_BF16, DT_BF16, 64, 2, 8)   // I = 1024
-  WISP_D(DT_BF16, DT_BF16, 8, 3, 8)    // I = 192
-  WISP_D(DT_FP8, DT_BF16, 16, 1, 8)    // I = 256
-#undef WISP_D
-  if (!kern) return hipErrorNotSupported;
-  const int isz = IT == DT_F32 ? 4 : 2;
-  const int n_pairs = b.pair_base[b.n_items - 1] + b.items[b.n_items - 1].ntok;
-  const int rpw = 64 / lpr;
-  const int step = 4 * rpw;
-  int rows_per_wg = (L.d + 511) / 512;                  // about 512 workgroups at most
-  rows_per_wg = (rows_per_wg + step - 1) / step * step;
-  const size_t lds = static_cast<size_t>(n_pairs) * L.I * isz + static_cast<size_t>(n_pairs) * rows_per_wg * 4;
-  if (lds > 64 * 1024) return hipErrorNotSupported;
-  if (combine && T * rows_per_wg > 256) return hipErrorNotSupported;
-  const int grid = (L.d + rows_per_wg - 1) / rows_per_wg;
-  hipExtLaunchKernelGGL(kern, dim3(grid), dim3(256), static_cast<uint32_t>(lds), st, tm.start, tm.stop, 0, b,
-                        static_cast<const uint8_t*>(h), L.I, L.d, rows_per_wg, static_cast<uint32_t>(L.off_w2),
-                        static_cast<uint32_t>(L.off_s2), buf, T, k, has_shared, w, y, combine ? 1 : 0);
+  const int EPL = L.w_dtype == DT_F32 ? 4 : L.w_dtype == DT_BF16 ? 8 : 16;
+  o->lpr_g = pick_lpr(L.d / EPL);
+  o->lpr_d = pick_lpr(L.I / EPL);
+  if (!o->lpr_g || !o->lpr_d) return false;
+  o->nl_g = L.d / EPL / o->lpr_g;
+  o->nl_d = L.I / EPL / o->lpr_d;
+  return true;
+}
+}  // namespace
+
+hipError_t launch_ffn_dev(const FfnBatch* plan, int max_items, const FfnShape& s, const void* x, void* h,
+                          float* buf, hipStream_t st, const LaunchTiming& tm_gateup, const LaunchTiming& tm_down) {
+  const BlobLayout& L = s.blob;
+  DevShape ds;
+  if (!dev_shape(s, &ds)) return hipErrorNotSupported;
+  const int WT = L.w_dtype, XT = s.x_dtype, HT = s.h_dtype;
+  using GK = void (*)(const FfnBatch*, const uint8_t*, int, int, int, int, int, int, uint32_t, uint32_t, uint32_t,
+                      uint32_t, uint32_t, uint32_t, uint8_t*);
+  using DK = void (*)(const FfnBatch*, const uint8_t*, int, int, int, int, uint32_t, uint32_t, float*);
+  GK gk = nullptr;
+  DK dk = nullptr;
+#define WISP_G(W, X, LP, N) \
+  if (WT == W && XT == X && ds.lpr_g == LP && ds.nl_g == N) gk = &ffn_gateup_dev<W, X, LP, N>;
+#define WISP_DD(W, X, LP, N) \
+  if (WT == W && HT == X && ds.lpr_d == LP && ds.nl_d == N) dk = &ffn_down_dev<W, X, LP, N>;
+  WISP_G(DT_BF16, DT_BF16, 64, 4)   // d = 2048
+  WISP_G(DT_BF16, DT_BF16, 32, 1)   // d = 256
+  WISP_G(DT_BF16, DT_BF16, 16, 3)   // d = 384
+  WISP_G(DT_FP8, DT_BF16, 64, 7)    // d = 7168
+  WISP_G(DT_FP8, DT_BF16, 16, 1)    // d = 256
+  WISP_G(DT_F32, DT_F32, 64, 1)     // d = 256
+  WISP_DD(DT_BF16, DT_BF16, 32, 3)  // I = 768
+  WISP_DD(DT_BF16, DT_BF16, 16, 1)  // I = 128
+  WISP_DD(DT_BF16, DT_BF16, 8, 3)   // I = 192
+  WISP_DD(DT_FP8, DT_BF16, 64, 2)   // I = 2048
+  WISP_DD(DT_FP8, DT_BF16, 16, 1)   // I = 256
+  WISP_DD(DT_F32, DT_F32, 64, 2)    // I = 512
+#undef WISP_G
+#undef WISP_DD
+  if (!gk || !dk) return hipErrorNotSupported;
+  // gate/up: per item slot, one row pass per workgroup for resident experts, and at least the
+  // streaming workgroups of a fault
+  const int rows_hit = 4 * (64 / ds.lpr_g);
+  const int fault_wgs = 32, copy_wgs = 16;
+  int bpi = (L.I + rows_hit - 1) / rows_hit;
+  if (bpi < fault_wgs + copy_wgs) bpi = fault_wgs + copy_wgs;
+  const int xs = XT == DT_F32 ? 4 : 2, hs = HT == DT_F32 ? 4 : 2;
+  const size_t lds_g = static_cast<size_t>(kMaxTokPerItem) * L.d * xs;
+  if (lds_g > 64 * 1024) return hipErrorNotSupported;
+  hipExtLaunchKernelGGL(gk, dim3(max_items * bpi), dim3(256), static_cast<uint32_t>(lds_g), st, tm_gateup.start,
+                        tm_gateup.stop, 0, plan, static_cast<const uint8_t*>(x), L.d, L.I, bpi, rows_hit, fault_wgs,
+                        copy_wgs, static_cast<uint32_t>(L.off_w1), static_cast<uint32_t>(L.off_w3),
+                        static_cast<uint32_t>(L.off_s1), static_cast<uint32_t>(L.off_s3),
+                        static_cast<uint32_t>(L.off_w2), static_cast<uint32_t>(L.bytes - L.off_w2),
+                        static_cast<uint8_t*>(h));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // down: per item slot, one row pass per workgroup
+  const int rows_d = 4 * (64 / ds.lpr_d);
+  const int bpi_d = (L.d + rows_d - 1) / rows_d;
+  const size_t lds_d = static_cast<size_t>(kMaxTokPerItem) * L.I * hs;
+  if (lds_d > 64 * 1024) return hipErrorNotSupported;
+  hipExtLaunchKernelGGL(dk, dim3(max_items * bpi_d), dim3(256), static_cast<uint32_t>(lds_d), st, tm_down.start,
+                        tm_down.stop, 0, plan, static_cast<const uint8_t*>(h), L.d, L.I, bpi_d, rows_d,
+                        static_cast<uint32_t>(L.off_w2), static_cast<uint32_t>(L.off_s2), buf);
   return hipGetLastError();
+}
+
+bool ffn_dev_supported(const FfnShape& s, int T, int k, int has_shared) {
+  DevShape ds;
+  if (!dev_shape(s, &ds)) return false;
+  const BlobLayout& L = s.blob;
+  const int WT = L.w_dtype;
+  const bool g = (WT == DT_BF16 && ((ds.lpr_g == 64 && ds.nl_g == 4) || (ds.lpr_g == 32 && ds.nl_g == 1) ||
+                                    (ds.lpr_g == 16 && ds.nl_g == 3))) ||
+                 (WT == DT_FP8 && ((ds.lpr_g == 64 && ds.nl_g == 7) || (ds.lpr_g == 16 && ds.nl_g == 1))) ||
+                 (WT == DT_F32 && ds.lpr_g == 64 && ds.nl_g == 1);
+  const bool dn = (WT == DT_BF16 && ((ds.lpr_d == 32 && ds.nl_d == 3) || (ds.lpr_d == 16 && ds.nl_d == 1) ||
+                                     (ds.lpr_d == 8 && ds.nl_d == 3))) ||
+                  (WT == DT_FP8 && ((ds.lpr_d == 64 && ds.nl_d == 2) || (ds.lpr_d == 16 && ds.nl_d == 1))) ||
+                  (WT == DT_F32 && ds.lpr_d == 64 && ds.nl_d == 2);
+  const int hs = s.h_dtype == DT_F32 ? 4 : 2, xs = s.x_dtype == DT_F32 ? 4 : 2;
+  (void)k;
+  (void)has_shared;
+  return g && dn && T <= kMaxTokPerItem && static_cast<size_t>(kMaxTokPerItem) * L.d * xs <= 64 * 1024 &&
+         static_cast<size_t>(kMaxTokPerItem) * L.I * hs <= 64 * 1024;
 }
 
 // ------------------------------------------------------------------------------------------

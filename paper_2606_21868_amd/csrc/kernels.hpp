@@ -28,22 +28,20 @@ constexpr int kMaxTokPerItem = 4;
 constexpr int kMaxItems = 40;
 
 struct FfnItem {
-  const uint8_t* w;
+  const uint8_t* w;      // the expert's blob in its HBM slot (or the shared expert's slab)
+  const uint8_t* src;    // device-planned launches, faulted expert: its pinned host master
   int32_t ntok;
+  int32_t fault;         // device-planned launches: 1 = stream from src into w while computing
   int32_t tok[kMaxTokPerItem];
   int32_t out[kMaxTokPerItem];
 };
 
-// Passed by value as a kernel argument (the device-side expert map of this launch).
-constexpr int kMaxRows = 4 * 9;  // T <= 4 tokens x (k <= 8 ranks + shared)
+// The device-side expert map of one launch: passed by value as a kernel argument by the host
+// pager, or written to HBM by the device pager.
 struct FfnBatch {
   FfnItem items[kMaxItems];
   int32_t n_items;
   int32_t max_ntok;
-  // for the fused down + combine launch: pair_base[i] = index of item i's first (item, token)
-  // pair; src[row] = the pair holding output row `row` in this launch, or -1 (read the scratch)
-  int16_t pair_base[kMaxItems];
-  int8_t src[kMaxRows];
 };
 
 struct FfnShape {
@@ -64,13 +62,13 @@ hipError_t launch_ffn_gateup(const FfnBatch& b, const FfnShape& s, const void* x
 // Phase 2: buf[out] = W2 h[out]; buf row stride = d (fp32).
 hipError_t launch_ffn_down(const FfnBatch& b, const FfnShape& s, const void* h, float* buf, hipStream_t st,
                            const LaunchTiming& tm);
-// Phase 2 fused with the combine, for decode batches whose h rows fit in LDS: every workgroup owns
-// a block of output rows for all items; y[t] = sum_j w[t, j] o_tj (+ shared) with o_tj from this
-// launch (LDS) or from earlier launches (buf).  With combine = false it only writes buf.
-// Returns hipErrorNotSupported if the shape does not fit; the caller then uses the two kernels.
-hipError_t launch_ffn_down_combine(const FfnBatch& b, const FfnShape& s, const void* h, float* buf, int T, int k,
-                                   int has_shared, const float* w, float* y, bool combine, hipStream_t st,
-                                   const LaunchTiming& tm);
+// Device-planned FFN of one layer-step (plan written to HBM by the device pager): gate/up, with
+// faulted experts streamed from their pinned masters into their slots by the same kernel, then
+// down into buf; the caller launches the combine.  max_items bounds the plan (T*k + shared).
+hipError_t launch_ffn_dev(const FfnBatch* plan, int max_items, const FfnShape& s, const void* x, void* h,
+                          float* buf, hipStream_t st, const LaunchTiming& tm_gateup, const LaunchTiming& tm_down);
+bool ffn_dev_supported(const FfnShape& s, int T, int k, int has_shared);
+
 // y[t] = sum_j w[t, j] buf[t*(k+1)+j] (j ascending) + (shared ? buf[t*(k+1)+k] : 0).
 hipError_t launch_combine(int T, int k, int d, int has_shared, const float* w, const float* buf, float* y,
                           hipStream_t st, const LaunchTiming& tm);
@@ -83,6 +81,14 @@ hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int
 hipError_t launch_router_select(const float* logits, int T, int N, int k, int route, int n_groups, int topk_groups,
                                 int32_t* idx, float* w, uint64_t* idx_host, uint32_t seq, hipStream_t st,
                                 const LaunchTiming& tm);
+
+// Device pager: selection of T <= 4 tokens + Algorithm 1 on the layer's slot table in HBM + the
+// launch plan of the layer's FFN (one workgroup).  Requires T * k <= C.
+hipError_t launch_select_page(const float* logits, int T, int N, int k, int route, int n_groups, int topk_groups,
+                              int32_t* idx, float* w, int32_t* pi, int32_t* pinv, uint64_t* tau, uint64_t* clock,
+                              int C, const uint64_t* slot_ptr, const uint8_t* master_base, uint64_t master_stride,
+                              const uint8_t* shared_dev, int has_shared, FfnBatch* plan, uint32_t* stats,
+                              hipStream_t st, const LaunchTiming& tm);
 
 // Diagnostics.
 hipError_t launch_hbm_copy(const void* src, void* dst, size_t bytes, hipStream_t st);

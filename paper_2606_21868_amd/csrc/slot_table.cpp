@@ -19,6 +19,20 @@ void SlotTable::clear() {
   std::fill(tau_.begin(), tau_.end(), 0);
 }
 
+void SlotTable::export_state(int32_t* pi, int32_t* pinv, uint64_t* tau, uint64_t* clock) const {
+  std::copy(pi_.begin(), pi_.end(), pi);
+  std::copy(pinv_.begin(), pinv_.end(), pinv);
+  std::copy(tau_.begin(), tau_.end(), tau);
+  *clock = clock_;
+}
+
+void SlotTable::import_state(const int32_t* pi, const int32_t* pinv, const uint64_t* tau, uint64_t clock) {
+  std::copy(pi, pi + N_, pi_.begin());
+  std::copy(pinv, pinv + C_, pinv_.begin());
+  std::copy(tau, tau + C_, tau_.begin());
+  clock_ = clock;
+}
+
 // One step on the distinct ids G (|G| <= C): faults in ascending id take the victims with the
 // smallest (tick, slot) among slots whose occupant is not in G; then every id of G gets the new
 // tick (all experts of a step share it).

@@ -42,6 +42,10 @@ class SlotTable {
   // Drop every resident expert (all slots empty, ticks 0); the clock keeps counting.
   void clear();
 
+  // Raw state, for moving the table to and from the device pager.
+  void export_state(int32_t* pi, int32_t* pinv, uint64_t* tau, uint64_t* clock) const;
+  void import_state(const int32_t* pi, const int32_t* pinv, const uint64_t* tau, uint64_t clock);
+
  private:
   void alg1(const int32_t* G, int32_t g, ChunkPlan* cp);
 

@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libwisp.so")
 OK, E_INVAL, E_NOMEM, E_HIP, E_NOT_RESIDENT, E_STATE = 0, -1, -2, -3, -4, -5
 STATUS_NAMES = {0: "OK", -1: "E_INVAL", -2: "E_NOMEM", -3: "E_HIP", -4: "E_NOT_RESIDENT", -5: "E_STATE"}
 F32, BF16, FP8 = 0, 1, 2
+PAGER_HOST, PAGER_DEVICE = 0, 1
 (K_ROUTER_LOGITS, K_ROUTER_SELECT, K_FFN_GATEUP, K_FFN_DOWN, K_COMBINE, K_H2D_FILL, K_GROUPED_GATEUP,
  K_GROUPED_DOWN, K_PERMUTE) = range(9)
 KERNEL_CLASS_NAMES = ["router_logits", "router_select", "ffn_gateup", "ffn_down", "combine", "h2d_fill",
@@ -64,6 +65,7 @@ _SIGS = {
     "wisp_router_weights": [_P, _I, _P],
     "wisp_set_budget": [_P, _U64, ctypes.POINTER(_I)],
     "wisp_preload": [_P],
+    "wisp_set_pager": [_P, _I],
     "wisp_route_topk": [_P, _I, _P, _I, _P, _P, _P, _P],
     "wisp_page_in": [_P, _I, _P, _I, ctypes.POINTER(PageStats)],
     "wisp_moe_forward": [_P, _I, _P, _I, _P, _P, _P, ctypes.POINTER(PageStats)],
@@ -188,6 +190,10 @@ class Context:
 
     def preload(self):
         check(lib().wisp_preload(self.h), "wisp_preload")
+
+    def set_pager(self, pager):
+        """PAGER_HOST (host slot table, hipMemcpyAsync fills) or PAGER_DEVICE (slot table in HBM)."""
+        check(lib().wisp_set_pager(self.h, int(pager)), "wisp_set_pager")
 
     def route_topk(self, layer, x, T, idx, w, idx_host=None, stream=None):
         check(lib().wisp_route_topk(self.h, layer, _ptr(x), T, _ptr(idx), _ptr(w), _ptr(idx_host), _stream(stream)),

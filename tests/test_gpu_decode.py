@@ -54,6 +54,23 @@ def _run_case(wl, cap, steps, sample_points=None, check_all_outputs=False):
         worst, worst_el = check_outputs(run, out["y"], points, ora_idx)
         log(f"  worst row-relative error {worst:.3e} (elementwise {worst_el:.3e}); total misses "
             f"{int(out['misses'].sum())} of {int(out['hits'].sum() + out['misses'].sum())} references")
+        tables = [[run.ctx.slot_of(l, e) for e in range(wl.N)] for l in range(wl.L)]
+        # the device pager: same trace from cold -> same decisions, same slots, same bits
+        device_ok = cap >= wl.T * wl.k and wl.T <= 4
+        run.ctx.masters_ready()            # drops every resident expert
+        run.ctx.reset_stats()
+        if device_ok:
+            run.ctx.set_pager(wisp.PAGER_DEVICE)
+            dev = run.decode(record=True)
+            assert np.array_equal(dev["idx"], out["idx"])
+            assert np.array_equal(dev["hits"], out["hits"]) and np.array_equal(dev["misses"], out["misses"])
+            assert [[run.ctx.slot_of(l, e) for e in range(wl.N)] for l in range(wl.L)] == tables
+            assert np.array_equal(dev["y"].view(np.uint32), out["y"].view(np.uint32)), "device pager changed bits"
+            log("  device pager: same routing, faults, slot tables and output bits as the host pager")
+        else:
+            with pytest.raises(wisp.WispError) as ei:
+                run.ctx.set_pager(wisp.PAGER_DEVICE)
+            assert ei.value.status == wisp.E_INVAL
         # fully resident: C = N, preloaded, same kernels -> bit-identical, no faults
         assert run.set_cap(wl.N) == wl.N
         run.ctx.preload()
@@ -62,7 +79,7 @@ def _run_case(wl, cap, steps, sample_points=None, check_all_outputs=False):
         assert int(res["misses"].sum()) == 0
         assert np.array_equal(res["idx"], out["idx"])
         assert np.array_equal(res["y"].view(np.uint32), out["y"].view(np.uint32)), "paged != resident bits"
-        log("  paged output bit-identical to the fully resident run")
+        log(f"  paged output bit-identical to the fully resident run ({'device' if device_ok else 'host'} pager)")
         return out
     finally:
         run.close()
@@ -100,6 +117,13 @@ def test_qwen3_decode_full_size_sampled():
     pts = sorted({(int(s), int(l)) for s, l in zip(rng.integers(0, wl.steps, 24), rng.integers(0, wl.L, 24))})
     pts += [(0, 0), (wl.steps - 1, wl.L - 1)]
     _run_case(wl, wl.cap, wl.steps, sample_points=pts)
+
+
+def test_deepseek_shaped_fp8_reduced():
+    # fp8 E4M3 weights with 128x128 block scales, sigmoid group-limited routing, shared expert:
+    # the DeepSeek-V3 layer shape (d=7168, I=2048, 256 experts, 8 groups) at 2 layers x 12 steps
+    wl = WORKLOADS["deepseek-v3-16l-decode"].with_(L=2)
+    _run_case(wl, 56, 12, check_all_outputs=True)
 
 
 def test_fp8_conversion_all_codes():
