@@ -103,6 +103,25 @@ __device__ __forceinline__ void lds_chunk(const uint8_t* row, int col, float* o)
   }
 }
 
+// The same EPL input elements from 16-byte chunks held in registers.
+template <int IT, int EPL>
+__device__ __forceinline__ void reg_chunk(const uint4* q, float* o) {
+  if constexpr (IT == DT_F32) {
+#pragma unroll
+    for (int c = 0; c < EPL / 4; ++c) {
+      o[4 * c] = __uint_as_float(q[c].x); o[4 * c + 1] = __uint_as_float(q[c].y);
+      o[4 * c + 2] = __uint_as_float(q[c].z); o[4 * c + 3] = __uint_as_float(q[c].w);
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < EPL / 8; ++c) {
+      o[8 * c + 0] = bf16_lo(q[c].x); o[8 * c + 1] = bf16_hi(q[c].x); o[8 * c + 2] = bf16_lo(q[c].y);
+      o[8 * c + 3] = bf16_hi(q[c].y); o[8 * c + 4] = bf16_lo(q[c].z); o[8 * c + 5] = bf16_hi(q[c].z);
+      o[8 * c + 6] = bf16_lo(q[c].w); o[8 * c + 7] = bf16_hi(q[c].w);
+    }
+  }
+}
+
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
   u += 0x7FFFu + ((u >> 16) & 1u);
@@ -138,32 +157,31 @@ __device__ __forceinline__ void rows_body(const FfnItem& it, const uint8_t* rd, 
   const int scols = K / 128;
   const size_t row_stride_b = static_cast<size_t>(K) * (WT == DT_F32 ? 4 : WT == DT_BF16 ? 2 : 1);
 
-  // fully unrolled shapes: the first row pass issues its weight loads before the input rows are
-  // staged, so the weight fetch overlaps the staging
+  // Single-token items of the unrolled shapes keep the lane's slice of the input row in registers:
+  // a lane reads the same columns of every row it processes, so the slice is loaded once, before
+  // the weights, and no LDS staging or barrier is needed.  Other items stage their input rows in
+  // LDS.  The multiply-add sequence is the same either way.
+  constexpr int XQ = NLT > 0 ? EPL * IS / 16 : 1;          // 16-byte input chunks per weight chunk
+  const bool xreg = NLT > 0 && ntok == 1;
+  uint4 xr[NLT > 0 ? NLT * XQ : 1];
   const int rbase0 = r_begin + wave * RPW;
-  uint4 pa[NLT > 0 ? NLT : 1], pb[NLT > 0 ? NLT : 1];
-  if constexpr (NLT > 0) {
-    const int r = rbase0 + sub;
-    const int rr = r < r_end ? r : r_begin;
-    const uint4* row0 = reinterpret_cast<const uint4*>(wbase0 + rr * row_stride_b);
-    const uint4* row1 = reinterpret_cast<const uint4*>(wbase1 + rr * row_stride_b);
-    if (rbase0 < r_end) {
+  if (xreg) {
+    const uint8_t* xrow = vin + static_cast<size_t>(MODE == MODE_GATEUP ? it.tok[0] : it.out[0]) * vin_stride * IS;
 #pragma unroll
-      for (int m = 0; m < NLT; ++m) {
-        pa[m] = row0[m * LPR + sl];
-        if constexpr (MODE == MODE_GATEUP) pb[m] = row1[m * LPR + sl];
-      }
+    for (int m = 0; m < (NLT > 0 ? NLT : 1); ++m)
+#pragma unroll
+      for (int q = 0; q < XQ; ++q)
+        xr[m * XQ + q] = reinterpret_cast<const uint4*>(xrow + static_cast<size_t>((m * LPR + sl) * EPL) * IS)[q];
+  } else {
+    // stage the item's input rows (x for gate/up, h for down) in LDS
+    for (int t = 0; t < ntok; ++t) {
+      const int src_row = MODE == MODE_GATEUP ? it.tok[t] : it.out[t];
+      const uint4* src = reinterpret_cast<const uint4*>(vin + static_cast<size_t>(src_row) * vin_stride * IS);
+      uint4* dst = reinterpret_cast<uint4*>(lds + t * row_bytes);
+      for (int i = threadIdx.x; i < row_bytes / 16; i += 256) dst[i] = src[i];
     }
+    __syncthreads();
   }
-
-  // stage the item's input rows (x for gate/up, h for down) in LDS
-  for (int t = 0; t < ntok; ++t) {
-    const int src_row = MODE == MODE_GATEUP ? it.tok[t] : it.out[t];
-    const uint4* src = reinterpret_cast<const uint4*>(vin + static_cast<size_t>(src_row) * vin_stride * IS);
-    uint4* dst = reinterpret_cast<uint4*>(lds + t * row_bytes);
-    for (int i = threadIdx.x; i < row_bytes / 16; i += 256) dst[i] = src[i];
-  }
-  __syncthreads();
 
   for (int rbase = rbase0; rbase < r_end; rbase += 4 * RPW) {
     const int r = rbase + sub;
@@ -177,20 +195,12 @@ __device__ __forceinline__ void rows_body(const FfnItem& it, const uint8_t* rd, 
 
     for (int m0 = 0; m0 < NL; m0 += U) {
       uint4 a[U], b[U];
-      if (NLT > 0 && rbase == rbase0) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          a[u] = pa[NLT > 0 ? u : 0];
-          if constexpr (MODE == MODE_GATEUP) b[u] = pb[NLT > 0 ? u : 0];
-        }
-      } else {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int m = m0 + u;
-          if (NLT > 0 || m < NL) {
-            a[u] = row0[m * LPR + sl];
-            if constexpr (MODE == MODE_GATEUP) b[u] = row1[m * LPR + sl];
-          }
+      for (int u = 0; u < U; ++u) {
+        const int m = m0 + u;
+        if (NLT > 0 || m < NL) {
+          a[u] = row0[m * LPR + sl];
+          if constexpr (MODE == MODE_GATEUP) b[u] = row1[m * LPR + sl];
         }
       }
       if (wr && valid) {
@@ -223,7 +233,8 @@ __device__ __forceinline__ void rows_body(const FfnItem& it, const uint8_t* rd, 
         for (int t = 0; t < kMaxTokPerItem; ++t) {
           if (t >= ntok) break;
           float xv[EPL];
-          lds_chunk<IT, EPL>(lds + t * row_bytes, col, xv);
+          if (xreg) reg_chunk<IT, EPL>(&xr[(NLT > 0 ? m : 0) * XQ], xv);
+          else lds_chunk<IT, EPL>(lds + t * row_bytes, col, xv);
           if constexpr (WT == DT_FP8) {
             float pa = 0.f, pb = 0.f;
 #pragma unroll
