@@ -33,6 +33,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "ffn_gateup_qwen3-30b-a3b-decode_hbm_traffic.txt")
+FFN_SOURCE = os.path.join(ROOT, "paper_2606_21868_amd", "csrc", "expert_ffn.hip")
 
 
 def log(msg):
@@ -56,6 +58,30 @@ def measure_hbm_copy(torch, wisp, nbytes=1 << 30, reps=5):
     del src, dst
     rates.sort()
     return rates[len(rates) // 2]
+
+
+def measured_traffic(workload):
+    """HBM bytes per gate/up launch from the committed FETCH_SIZE/WRITE_SIZE counter summary (scaled by
+    the copy-kernel calibration it records), or None when there is none for this workload or the kernel
+    source has changed since the counters were taken."""
+    import hashlib
+    if workload != "qwen3-30b-a3b-decode" or not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    fields = {}
+    for line in open(TRAFFIC_SUMMARY):
+        parts = line.split()
+        if len(parts) >= 2 and parts[0].startswith("traffic_"):
+            fields[parts[0]] = float(parts[1])
+        elif parts[:2] == ["kernel_source", "expert_ffn.hip"] and len(parts) == 4:
+            fields["sha256"] = parts[3]
+    with open(FFN_SOURCE, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != fields.get("sha256"):
+            return None
+    if "traffic_bytes_per_launch" not in fields:
+        return None
+    return dict(bytes_per_launch=fields["traffic_bytes_per_launch"],
+                algorithmic_bytes_per_launch=fields.get("traffic_algorithmic_bytes_per_launch"),
+                source=os.path.relpath(TRAFFIC_SUMMARY, ROOT))
 
 
 def cpu_baseline(run, wl, start_step, max_tokens=24, budget_s=15.0):
@@ -195,8 +221,10 @@ def main():
             f"{passes['host']['path_roofline']['frac']:.3f} of the path roofline")
         if "ffn_gateup" in tk:
             g = tk["ffn_gateup"]
+            tr = measured_traffic(wl.name)
             roof = dict(bound="hbm", achieved=g["GBps"], peak=HBM_PEAK_GBPS, unit="GB/s", frac=g["GBps"] / HBM_PEAK_GBPS,
-                        traffic=None, kernel="ffn_rows<bf16,bf16,gate/up> expert GEMV (W1+W3 rows), host-pager pass",
+                        traffic=tr["bytes_per_launch"] if tr else None,
+                        traffic_detail=tr, kernel="ffn_rows<bf16,bf16,gate/up> expert GEMV (W1+W3 rows), host-pager pass",
                         avg_launch_us=g["avg_us"], bytes_per_launch=g["bytes_per_launch"], launches=g["launches"])
     if args.pager in ("both", "device"):
         el, out = timed_pass(wisp.PAGER_DEVICE, 0)
