@@ -190,10 +190,11 @@ typedef enum {
 } wisp_kernel_class;
 wisp_status wisp_set_profiling(wisp_ctx* ctx, int32_t class_mask);
 /* Waits for outstanding timed work, then returns the accumulated total milliseconds, number of
- * launches, and algorithmic HBM bytes (weights and activations each read or written once) of a
- * class. */
+ * launches, algorithmic HBM bytes (weights and activations each read or written once) and
+ * algorithmic floating-point operations (2 per multiply-add; counted for the grouped GEMM classes)
+ * of a class.  Any output pointer may be NULL. */
 wisp_status wisp_kernel_times(wisp_ctx* ctx, int32_t kclass, double* total_ms, uint64_t* launches,
-                              uint64_t* bytes);
+                              uint64_t* bytes, uint64_t* flops);
 wisp_status wisp_reset_kernel_times(wisp_ctx* ctx);
 
 /* Measure host->device bandwidth of the expert path: `reps` rounds, each copying `count` expert

@@ -43,6 +43,7 @@ struct TimedPair {
   hipEvent_t a, b;
   int kclass;
   uint64_t bytes;
+  uint64_t flops;
 };
 
 struct LayerState {
@@ -92,6 +93,15 @@ struct wisp_ctx {
   double k_ms[WISP_K_NUM] = {};
   uint64_t k_n[WISP_K_NUM] = {};
   uint64_t k_bytes[WISP_K_NUM] = {};
+  uint64_t k_flops[WISP_K_NUM] = {};
+  // token batches: the routed ids on the device and their expert-sorted order
+  int32_t* ids_up = nullptr;         // pinned staging of the ids for the upload
+  int32_t* d_ids = nullptr;          // [max_tokens * k]
+  int32_t* d_perm = nullptr;         // [max_tokens * k]
+  hipEvent_t ids_ev = nullptr;       // the last upload has been read
+  bool ids_ev_recorded = false;
+  std::vector<int32_t> e_cnt, e_off; // pairs per expert and their first sorted row
+  std::vector<int32_t> pair_order;   // pairs sorted by expert (host copy, for the per-item path)
   int32_t fail_alloc_at = 0;
   int32_t alloc_counter = 0;
   // device pager (WISP_PAGER_DEVICE): the slot tables in HBM are authoritative while it is on
@@ -137,9 +147,9 @@ LaunchTiming timing_begin(wisp_ctx* c, int kclass) {
   return t;
 }
 
-void timing_end(wisp_ctx* c, const LaunchTiming& t, int kclass, uint64_t bytes) {
+void timing_end(wisp_ctx* c, const LaunchTiming& t, int kclass, uint64_t bytes, uint64_t flops = 0) {
   if (!c->profiling || !t.start || !t.stop) return;
-  c->timed.push_back({t.start, t.stop, kclass, bytes});
+  c->timed.push_back({t.start, t.stop, kclass, bytes, flops});
 }
 
 // Accumulate every finished timed pair; with wait, first wait for all of them.
@@ -157,6 +167,7 @@ void harvest(wisp_ctx* c, bool wait) {
       c->k_ms[p.kclass] += ms;
       c->k_n[p.kclass] += 1;
       c->k_bytes[p.kclass] += p.bytes;
+      c->k_flops[p.kclass] += p.flops;
     }
     c->ev_pool.push_back(p.a);
     c->ev_pool.push_back(p.b);
@@ -231,6 +242,10 @@ void free_ctx(wisp_ctx* c) {
   if (c->h) hipFree(c->h);
   if (c->buf) hipFree(c->buf);
   if (c->idx_pinned) hipHostFree(c->idx_pinned);
+  if (c->ids_up) hipHostFree(c->ids_up);
+  if (c->d_ids) hipFree(c->d_ids);
+  if (c->d_perm) hipFree(c->d_perm);
+  if (c->ids_ev) hipEventDestroy(c->ids_ev);
   for (void* p : {static_cast<void*>(c->d_pi), static_cast<void*>(c->d_pinv), static_cast<void*>(c->d_tau),
                   static_cast<void*>(c->d_clock), static_cast<void*>(c->d_slot_ptr), static_cast<void*>(c->d_plan),
                   static_cast<void*>(c->d_stats)})
@@ -482,6 +497,18 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   c->idx_tagged = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(p) + ids_bytes);
   std::memset(c->idx_tagged, 0, sizeof(uint64_t) * static_cast<size_t>(T) * k);
   c->ids_scratch.resize(static_cast<size_t>(T) * k);
+  const size_t pairs_bytes = sizeof(int32_t) * static_cast<size_t>(T) * k;
+  if (hipHostMalloc(&p, pairs_bytes, hipHostMallocDefault) != hipSuccess) return bail(WISP_E_NOMEM, "pinned scratch");
+  c->ids_up = static_cast<int32_t*>(p);
+  if (hipMalloc(&p, pairs_bytes) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
+  c->d_ids = static_cast<int32_t*>(p);
+  if (hipMalloc(&p, pairs_bytes) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
+  c->d_perm = static_cast<int32_t*>(p);
+  if (hipEventCreateWithFlags(&c->ids_ev, hipEventDisableTiming) != hipSuccess)
+    return bail(WISP_E_HIP, "hipEventCreate failed");
+  c->e_cnt.assign(N, 0);
+  c->e_off.assign(N + 1, 0);
+  c->pair_order.resize(static_cast<size_t>(T) * k);
   *out = c;
   g_err.clear();
   return WISP_OK;
@@ -806,37 +833,112 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
   if (T != L.T) return fail(WISP_E_INVAL, "T differs from the page-in");
   hipStream_t sm = static_cast<hipStream_t>(stream);
   const int k = ctx->desc.top_k;
+  const int N = ctx->desc.n_experts;
   const int rows = k + 1;
+  const int32_t n_pairs = T * k;
   const size_t nch = L.plan.chunks.size();
-  // exactness check: every routed id is in exactly one chunk, with a slot
-  for (int32_t i = 0; i < T * k; ++i) {
-    bool found = false;
-    for (size_t ci = 0; ci < nch && !found; ++ci)
-      for (int32_t e : L.plan.chunks[ci].experts) found |= (e == L.ids[i]);
-    if (!found) return fail(WISP_E_NOT_RESIDENT, "routed expert missing from the page-in plan");
+  // pairs per expert, and the pairs in (expert, pair) order
+  std::vector<int32_t>& cnt = ctx->e_cnt;
+  std::vector<int32_t>& off = ctx->e_off;
+  std::fill(cnt.begin(), cnt.end(), 0);
+  for (int32_t p = 0; p < n_pairs; ++p) ++cnt[L.ids[p]];
+  off[0] = 0;
+  for (int e = 0; e < N; ++e) off[e + 1] = off[e] + cnt[e];
+  {
+    std::vector<int32_t> fill(off.begin(), off.end() - 1);
+    for (int32_t p = 0; p < n_pairs; ++p) ctx->pair_order[fill[L.ids[p]]++] = p;
   }
+  // exactness check: every routed id is in a chunk of the plan, with a slot
+  {
+    std::vector<uint8_t> planned(N, 0);
+    for (size_t ci = 0; ci < nch; ++ci)
+      for (int32_t e : L.plan.chunks[ci].experts) planned[e] = 1;
+    for (int e = 0; e < N; ++e)
+      if (cnt[e] > 0 && !planned[e]) return fail(WISP_E_NOT_RESIDENT, "routed expert missing from the page-in plan");
+  }
+  const bool grouped = T >= kGroupedMinTokens && grouped_supported(ctx->shape, ctx->desc.has_shared);
+  if (grouped) {
+    // the ids go to the device once; the permutation kernel orders the pairs by expert there
+    if (ctx->ids_ev_recorded) WISP_HIP(hipEventSynchronize(ctx->ids_ev), "hipEventSynchronize(ids)");
+    std::memcpy(ctx->ids_up, L.ids.data(), sizeof(int32_t) * n_pairs);
+    WISP_HIP(hipMemcpyAsync(ctx->d_ids, ctx->ids_up, sizeof(int32_t) * n_pairs, hipMemcpyHostToDevice, sm),
+             "hipMemcpyAsync(ids)");
+    WISP_HIP(hipEventRecord(ctx->ids_ev, sm), "hipEventRecord(ids)");
+    ctx->ids_ev_recorded = true;
+    LaunchTiming tp = timing_begin(ctx, WISP_K_PERMUTE);
+    WISP_HIP(launch_permute_pairs(ctx->d_ids, n_pairs, N, ctx->d_perm, sm, tp), "permute launch");
+    timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(n_pairs) * 8);
+  }
+  const BlobLayout& B = ctx->blob;
+  const uint64_t dI = static_cast<uint64_t>(B.d) * B.I;
+  // grouped GEMMs over a list of (expert, slot) in launches of up to kMaxGroups experts
+  auto run_grouped = [&](const std::vector<std::pair<int32_t, const uint8_t*>>& list) -> wisp_status {
+    for (size_t g0 = 0; g0 < list.size(); g0 += kMaxGroups) {
+      GroupedBatch gb;
+      gb.n_groups = static_cast<int32_t>(std::min<size_t>(kMaxGroups, list.size() - g0));
+      int32_t tiles = 0;
+      uint64_t nrows = 0;
+      for (int g = 0; g < gb.n_groups; ++g) {
+        const int32_t e = list[g0 + g].first;
+        gb.w[g] = list[g0 + g].second;
+        gb.row_off[g] = off[e];
+        gb.rows[g] = cnt[e];
+        tiles += grouped_row_tiles(cnt[e]);
+        gb.tile_end[g] = tiles;
+        nrows += static_cast<uint64_t>(cnt[e]);
+      }
+      for (int g = gb.n_groups; g < kMaxGroups; ++g) {
+        gb.w[g] = nullptr;
+        gb.row_off[g] = gb.rows[g] = 0;
+        gb.tile_end[g] = tiles;
+      }
+      const uint64_t ng = static_cast<uint64_t>(gb.n_groups);
+      LaunchTiming t1 = timing_begin(ctx, WISP_K_GROUPED_GATEUP);
+      WISP_HIP(launch_grouped_gateup(gb, ctx->shape, x_dev, ctx->d_perm, k, ctx->h, sm, t1), "grouped gate/up launch");
+      timing_end(ctx, t1, WISP_K_GROUPED_GATEUP, ng * 2 * dI * B.elem + nrows * (B.d + B.I) * 2,
+                 nrows * 2 * 2 * dI);
+      LaunchTiming t2 = timing_begin(ctx, WISP_K_GROUPED_DOWN);
+      WISP_HIP(launch_grouped_down(gb, ctx->shape, ctx->h, ctx->d_perm, k, ctx->buf, sm, t2), "grouped down launch");
+      timing_end(ctx, t2, WISP_K_GROUPED_DOWN, ng * dI * B.elem + nrows * (B.I * 2 + B.d * 4), nrows * 2 * dI);
+    }
+    return WISP_OK;
+  };
+  auto work_of = [&](int32_t e, const uint8_t* w) {
+    Work wk;
+    wk.w = w;
+    for (int32_t q = off[e]; q < off[e + 1]; ++q) {
+      const int32_t p = ctx->pair_order[q];
+      wk.pairs.push_back({p / k, (p / k) * rows + p % k});
+    }
+    return wk;
+  };
   for (size_t ci = 0; ci < nch; ++ci) {
     const ChunkPlan& cp = L.plan.chunks[ci];
     if (ci > 0 && (s = issue_fills(ctx, layer, ci)) != WISP_OK) return s;
-    std::vector<Work> hits, faults;
-    for (size_t i = 0; i < cp.experts.size(); ++i) {
-      Work wk;
-      wk.w = L.chunk_ptrs[ci][i];
-      for (int32_t t = 0; t < T; ++t)
-        for (int j = 0; j < k; ++j)
-          if (L.ids[t * k + j] == cp.experts[i]) wk.pairs.push_back({t, t * rows + j});
-      (cp.fault[i] ? faults : hits).push_back(std::move(wk));
-    }
-    if (ci == 0 && ctx->desc.has_shared) {
-      Work wk;
-      wk.w = L.shared_dev;
-      for (int32_t t = 0; t < T; ++t) wk.pairs.push_back({t, t * rows + k});
-      hits.push_back(std::move(wk));
-    }
-    if (!hits.empty() && (s = run_ffn(ctx, hits, x_dev, sm)) != WISP_OK) return s;
-    if (!faults.empty()) {
-      WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[ci], 0), "hipStreamWaitEvent(fill)");
-      if ((s = run_ffn(ctx, faults, x_dev, sm)) != WISP_OK) return s;
+    if (grouped) {
+      std::vector<std::pair<int32_t, const uint8_t*>> hits, faults;
+      for (size_t i = 0; i < cp.experts.size(); ++i)
+        (cp.fault[i] ? faults : hits).push_back({cp.experts[i], L.chunk_ptrs[ci][i]});
+      if (!hits.empty() && (s = run_grouped(hits)) != WISP_OK) return s;
+      if (!faults.empty()) {
+        WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[ci], 0), "hipStreamWaitEvent(fill)");
+        if ((s = run_grouped(faults)) != WISP_OK) return s;
+      }
+    } else {
+      std::vector<Work> hits, faults;
+      for (size_t i = 0; i < cp.experts.size(); ++i)
+        (cp.fault[i] ? faults : hits).push_back(work_of(cp.experts[i], L.chunk_ptrs[ci][i]));
+      if (ci == 0 && ctx->desc.has_shared) {
+        Work wk;
+        wk.w = L.shared_dev;
+        for (int32_t t = 0; t < T; ++t) wk.pairs.push_back({t, t * rows + k});
+        hits.push_back(std::move(wk));
+      }
+      if (!hits.empty() && (s = run_ffn(ctx, hits, x_dev, sm)) != WISP_OK) return s;
+      if (!faults.empty()) {
+        WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[ci], 0), "hipStreamWaitEvent(fill)");
+        if ((s = run_ffn(ctx, faults, x_dev, sm)) != WISP_OK) return s;
+      }
     }
     if (ci + 1 < nch) WISP_HIP(hipEventRecord(L.chunk_ev[ci], sm), "hipEventRecord(chunk)");
   }
@@ -999,7 +1101,8 @@ wisp_status wisp_set_profiling(wisp_ctx* ctx, int32_t class_mask) {
   return WISP_OK;
 }
 
-wisp_status wisp_kernel_times(wisp_ctx* ctx, int32_t kclass, double* total_ms, uint64_t* launches, uint64_t* bytes) {
+wisp_status wisp_kernel_times(wisp_ctx* ctx, int32_t kclass, double* total_ms, uint64_t* launches, uint64_t* bytes,
+                              uint64_t* flops) {
   wisp_status s = check_ctx(ctx);
   if (s != WISP_OK) return s;
   if (kclass < 0 || kclass >= WISP_K_NUM) return fail(WISP_E_INVAL, "kernel class out of range");
@@ -1007,13 +1110,14 @@ wisp_status wisp_kernel_times(wisp_ctx* ctx, int32_t kclass, double* total_ms, u
   if (total_ms) *total_ms = ctx->k_ms[kclass];
   if (launches) *launches = ctx->k_n[kclass];
   if (bytes) *bytes = ctx->k_bytes[kclass];
+  if (flops) *flops = ctx->k_flops[kclass];
   return WISP_OK;
 }
 
 wisp_status wisp_reset_kernel_times(wisp_ctx* ctx) {
   if (!ctx) return fail(WISP_E_INVAL, "ctx is NULL");
   harvest(ctx, true);
-  for (int i = 0; i < WISP_K_NUM; ++i) { ctx->k_ms[i] = 0; ctx->k_n[i] = 0; ctx->k_bytes[i] = 0; }
+  for (int i = 0; i < WISP_K_NUM; ++i) { ctx->k_ms[i] = 0; ctx->k_n[i] = 0; ctx->k_bytes[i] = 0; ctx->k_flops[i] = 0; }
   return WISP_OK;
 }
 

@@ -1,0 +1,285 @@
+// Token-batch (prefill) expert FFN: grouped GEMMs on the bf16 matrix cores of gfx950 over
+// slot-indirected experts (the FusedMoE call of WiSP Algorithm 1 for large token batches).
+//
+// With thousands of tokens per layer each expert sees ~T*k/N of them, so its weights are reused
+// across many rows and the FFN is a set of small dense GEMMs, one per expert:
+//   H_e = silu(X_e W1_e^T) * (X_e W3_e^T)     X_e: the rows of the tokens routed to e  [n_e, d]
+//   O_e = H_e W2_e^T                                                                    [n_e, d]
+// The (token, rank) pairs are first ordered by expert (permute_pairs_kernel: a stable counting
+// sort, so expert e owns rows [off_e, off_e + n_e) of the sorted order and, inside, its pairs
+// ascend).  The GEMM kernels read the weights through the expert's slot address and gather or
+// scatter rows through the permutation; H is kept in the sorted order (bf16, as in decode) and O
+// lands in the per-(token, rank) rows that the combine reads.
+//
+// Tiles: 64 rows x 64 h-columns for gate/up (the B tile holds the matching 64 rows of W1 and of
+// W3, so SwiGLU is applied in registers), 64 rows x 128 columns for down; K in steps of 32 through
+// double-buffered LDS with padded rows.  Four waves per workgroup, each a 32-row slab of the tile
+// on v_mfma_f32_32x32x16_bf16 (A lane l holds row l%32, k 8*(l/32)..+7; B lane l holds column l%32,
+// same k; D lane l holds column l%32, rows 8*(r/4) + 4*(l/32) + r%4).  Every output element is one
+// fixed-order reduction over K, independent of where its row sits in a tile or which launch holds
+// its expert, so paged and fully resident runs give identical bits.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+
+namespace wisp {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int GM = 64;          // rows (pairs) per tile
+constexpr int GK = 32;          // K per LDS stage
+constexpr int GLD = GK + 8;     // padded LDS row, bf16 elements (80 bytes: conflict-free 16-byte reads)
+constexpr int GN_UP = 64;       // h columns per gate/up tile
+constexpr int GN_DOWN = 128;    // output columns per down tile
+
+__device__ __forceinline__ uint16_t bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// Tile -> (group, row tile, column tile).  Row tiles of a group are contiguous in blockIdx.x /
+// n_ctiles; column tiles of one row tile are adjacent launches (they share the gathered rows).
+__device__ __forceinline__ void tile_of(const GroupedBatch& gb, int n_ctiles, int& g, int& mt, int& ct) {
+  const int mt_all = blockIdx.x / n_ctiles;
+  ct = blockIdx.x - mt_all * n_ctiles;
+  g = 0;
+  while (g + 1 < gb.n_groups && mt_all >= gb.tile_end[g]) ++g;
+  mt = mt_all - (g > 0 ? gb.tile_end[g - 1] : 0);
+}
+
+// Stable counting sort of the pairs p = t*k + j by expert id idx[p] (one workgroup of 16 waves).
+// Wave w owns a contiguous segment of pairs.  Pass 1 counts each expert per wave (lanes with equal
+// ids find each other through eight ballots over the id bits); the counts are scanned over waves
+// and then over experts; pass 2 repeats the walk and writes every pair to
+// off[e] + (earlier pairs of e in earlier waves) + (earlier pairs of e in this wave).
+__global__ void __launch_bounds__(1024) permute_pairs_kernel(const int32_t* __restrict__ idx, int P, int N,
+                                                             int32_t* __restrict__ perm) {
+  __shared__ int32_t cnt[16][256];
+  __shared__ int32_t base[257];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  for (int i = tid; i < 16 * 256; i += 1024) (&cnt[0][0])[i] = 0;
+  __syncthreads();
+  const int seg = (P + 15) / 16;
+  const int p0 = wave * seg, p1 = min(P, p0 + seg);
+  const uint64_t below = (1ull << lane) - 1ull;
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int c0 = p0; c0 < p1; c0 += 64) {
+      const int p = c0 + lane;
+      const bool valid = p < p1;
+      const int e = valid ? idx[p] : 0;
+      uint64_t same = __ballot(valid);
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const bool bit = (e >> b) & 1;
+        const uint64_t m = __ballot(bit);
+        same &= bit ? m : ~m;
+      }
+      if (valid) {
+        const int before = cnt[wave][e];
+        if (pass == 1) perm[base[e] + before + __popcll(same & below)] = p;
+        if ((same & below) == 0) cnt[wave][e] = before + __popcll(same);
+      }
+    }
+    __syncthreads();
+    if (pass == 0) {
+      if (tid < N) {
+        int run = 0;
+        for (int w = 0; w < 16; ++w) {
+          const int c = cnt[w][tid];
+          cnt[w][tid] = run;
+          run += c;
+        }
+        base[tid] = run;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        int run = 0;
+        for (int e = 0; e < N; ++e) {
+          const int c = base[e];
+          base[e] = run;
+          run += c;
+        }
+        base[N] = run;
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// H rows [off_g + m0, +64) x h columns [c0, +64) of one expert: silu(X W1^T) * (X W3^T) -> bf16.
+__global__ void __launch_bounds__(256) grouped_gateup_kernel(GroupedBatch gb, const uint16_t* __restrict__ x,
+                                                             const int32_t* __restrict__ perm, int k, int d, int I,
+                                                             uint16_t* __restrict__ hs) {
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][GM * GLD];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][2 * GN_UP * GLD];
+  int g, mt, ct;
+  tile_of(gb, I / GN_UP, g, mt, ct);
+  const int rows = gb.rows[g], base = gb.row_off[g];
+  const int m0 = mt * GM, c0 = ct * GN_UP;
+  const uint16_t* W1 = reinterpret_cast<const uint16_t*>(gb.w[g]);
+  const uint16_t* W3 = W1 + static_cast<size_t>(I) * d;
+  const int tid = threadIdx.x;
+  const int lr = tid >> 2, lk = (tid & 3) * 8;   // load row (0..63) and k offset of this thread
+  const bool a_ok = m0 + lr < rows;
+  const uint16_t* a_src = x;
+  if (a_ok) a_src = x + static_cast<size_t>(perm[base + m0 + lr] / k) * d + lk;
+  const uint16_t* g_src = W1 + static_cast<size_t>(c0 + lr) * d + lk;
+  const uint16_t* u_src = W3 + static_cast<size_t>(c0 + lr) * d + lk;
+  uint4 ra = make_uint4(0u, 0u, 0u, 0u), rg, ru;
+  const int wave = tid >> 6, lane = tid & 63, wm = wave >> 1, wn = wave & 1;
+  const int fr = lane & 31, fk = (lane >> 5) * 8;
+  f32x16_t accg = {}, accu = {};
+  const int nk = d / GK;
+  if (a_ok) ra = *reinterpret_cast<const uint4*>(a_src);
+  rg = *reinterpret_cast<const uint4*>(g_src);
+  ru = *reinterpret_cast<const uint4*>(u_src);
+  *reinterpret_cast<uint4*>(&As[0][lr * GLD + lk]) = ra;
+  *reinterpret_cast<uint4*>(&Bs[0][lr * GLD + lk]) = rg;
+  *reinterpret_cast<uint4*>(&Bs[0][(GN_UP + lr) * GLD + lk]) = ru;
+  __syncthreads();
+  for (int s = 0; s < nk; ++s) {
+    const int cur = s & 1;
+    const bool more = s + 1 < nk;
+    if (more) {
+      const int kb = (s + 1) * GK;
+      if (a_ok) ra = *reinterpret_cast<const uint4*>(a_src + kb);
+      rg = *reinterpret_cast<const uint4*>(g_src + kb);
+      ru = *reinterpret_cast<const uint4*>(u_src + kb);
+    }
+#pragma unroll
+    for (int kk = 0; kk < GK; kk += 16) {
+      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&As[cur][(wm * 32 + fr) * GLD + kk + fk]);
+      const bf16x8_t bg = *reinterpret_cast<const bf16x8_t*>(&Bs[cur][(wn * 32 + fr) * GLD + kk + fk]);
+      const bf16x8_t bu = *reinterpret_cast<const bf16x8_t*>(&Bs[cur][(GN_UP + wn * 32 + fr) * GLD + kk + fk]);
+      accg = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bg, accg, 0, 0, 0);
+      accu = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bu, accu, 0, 0, 0);
+    }
+    if (more) {
+      *reinterpret_cast<uint4*>(&As[cur ^ 1][lr * GLD + lk]) = ra;
+      *reinterpret_cast<uint4*>(&Bs[cur ^ 1][lr * GLD + lk]) = rg;
+      *reinterpret_cast<uint4*>(&Bs[cur ^ 1][(GN_UP + lr) * GLD + lk]) = ru;
+    }
+    __syncthreads();
+  }
+  const int hc = c0 + wn * 32 + fr;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int i = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+    if (m0 + i < rows) {
+      const float a = accg[r];
+      const float h = a / (1.0f + __expf(-a)) * accu[r];
+      hs[static_cast<size_t>(base + m0 + i) * I + hc] = bf16_rne(h);
+    }
+  }
+}
+
+// O rows of one expert x output columns [c0, +128): H W2^T in fp32, scattered to the rows
+// t*(k+1) + j of the pairs.
+__global__ void __launch_bounds__(256) grouped_down_kernel(GroupedBatch gb, const uint16_t* __restrict__ hs,
+                                                           const int32_t* __restrict__ perm, int k, int d, int I,
+                                                           float* __restrict__ buf) {
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][GM * GLD];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][GN_DOWN * GLD];
+  int g, mt, ct;
+  tile_of(gb, d / GN_DOWN, g, mt, ct);
+  const int rows = gb.rows[g], base = gb.row_off[g];
+  const int m0 = mt * GM, c0 = ct * GN_DOWN;
+  const uint16_t* W2 = reinterpret_cast<const uint16_t*>(gb.w[g]) + 2 * static_cast<size_t>(I) * d;
+  const int tid = threadIdx.x;
+  const int lr = tid >> 2, lk = (tid & 3) * 8;
+  const bool a_ok = m0 + lr < rows;
+  const uint16_t* a_src = hs + static_cast<size_t>(a_ok ? base + m0 + lr : 0) * I + lk;
+  const uint16_t* b0_src = W2 + static_cast<size_t>(c0 + lr) * I + lk;
+  const uint16_t* b1_src = W2 + static_cast<size_t>(c0 + 64 + lr) * I + lk;
+  uint4 ra = make_uint4(0u, 0u, 0u, 0u), rb0, rb1;
+  const int wave = tid >> 6, lane = tid & 63, wm = wave >> 1, wn = wave & 1;
+  const int fr = lane & 31, fk = (lane >> 5) * 8;
+  f32x16_t acc0 = {}, acc1 = {};
+  const int nk = I / GK;
+  if (a_ok) ra = *reinterpret_cast<const uint4*>(a_src);
+  rb0 = *reinterpret_cast<const uint4*>(b0_src);
+  rb1 = *reinterpret_cast<const uint4*>(b1_src);
+  *reinterpret_cast<uint4*>(&As[0][lr * GLD + lk]) = ra;
+  *reinterpret_cast<uint4*>(&Bs[0][lr * GLD + lk]) = rb0;
+  *reinterpret_cast<uint4*>(&Bs[0][(64 + lr) * GLD + lk]) = rb1;
+  __syncthreads();
+  for (int s = 0; s < nk; ++s) {
+    const int cur = s & 1;
+    const bool more = s + 1 < nk;
+    if (more) {
+      const int kb = (s + 1) * GK;
+      if (a_ok) ra = *reinterpret_cast<const uint4*>(a_src + kb);
+      rb0 = *reinterpret_cast<const uint4*>(b0_src + kb);
+      rb1 = *reinterpret_cast<const uint4*>(b1_src + kb);
+    }
+#pragma unroll
+    for (int kk = 0; kk < GK; kk += 16) {
+      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&As[cur][(wm * 32 + fr) * GLD + kk + fk]);
+      const bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(&Bs[cur][(wn * 64 + fr) * GLD + kk + fk]);
+      const bf16x8_t b1 = *reinterpret_cast<const bf16x8_t*>(&Bs[cur][(wn * 64 + 32 + fr) * GLD + kk + fk]);
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b0, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b1, acc1, 0, 0, 0);
+    }
+    if (more) {
+      *reinterpret_cast<uint4*>(&As[cur ^ 1][lr * GLD + lk]) = ra;
+      *reinterpret_cast<uint4*>(&Bs[cur ^ 1][lr * GLD + lk]) = rb0;
+      *reinterpret_cast<uint4*>(&Bs[cur ^ 1][(64 + lr) * GLD + lk]) = rb1;
+    }
+    __syncthreads();
+  }
+  const int oc = c0 + wn * 64 + fr;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int i = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+    if (m0 + i < rows) {
+      const int p = perm[base + m0 + i];
+      const size_t orow = static_cast<size_t>(p / k) * (k + 1) + (p % k);
+      buf[orow * d + oc] = acc0[r];
+      buf[orow * d + oc + 32] = acc1[r];
+    }
+  }
+}
+
+}  // namespace
+
+bool grouped_supported(const FfnShape& s, int has_shared) {
+  return !has_shared && s.blob.w_dtype == DT_BF16 && s.x_dtype == DT_BF16 && s.h_dtype == DT_BF16 &&
+         s.blob.d % GN_DOWN == 0 && s.blob.I % GN_UP == 0 && s.blob.d % GK == 0 && s.blob.I % GK == 0;
+}
+
+int grouped_row_tiles(int rows) { return (rows + GM - 1) / GM; }
+
+hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t* perm, hipStream_t st,
+                                const LaunchTiming& tm) {
+  if (n_pairs <= 0) return hipSuccess;
+  if (N < 1 || N > 256) return hipErrorInvalidValue;
+  hipExtLaunchKernelGGL(permute_pairs_kernel, dim3(1), dim3(1024), 0, st, tm.start, tm.stop, 0, idx, n_pairs, N,
+                        perm);
+  return hipGetLastError();
+}
+
+hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const void* x, const int32_t* perm, int k,
+                                 void* hs, hipStream_t st, const LaunchTiming& tm) {
+  if (b.n_groups <= 0) return hipSuccess;
+  if (b.n_groups > kMaxGroups || !grouped_supported(s, 0)) return hipErrorInvalidValue;
+  const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.I / GN_UP);
+  hipExtLaunchKernelGGL(grouped_gateup_kernel, dim3(tiles), dim3(256), 0, st, tm.start, tm.stop, 0, b,
+                        static_cast<const uint16_t*>(x), perm, k, s.blob.d, s.blob.I, static_cast<uint16_t*>(hs));
+  return hipGetLastError();
+}
+
+hipError_t launch_grouped_down(const GroupedBatch& b, const FfnShape& s, const void* hs, const int32_t* perm, int k,
+                               float* buf, hipStream_t st, const LaunchTiming& tm) {
+  if (b.n_groups <= 0) return hipSuccess;
+  if (b.n_groups > kMaxGroups || !grouped_supported(s, 0)) return hipErrorInvalidValue;
+  const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.d / GN_DOWN);
+  hipExtLaunchKernelGGL(grouped_down_kernel, dim3(tiles), dim3(256), 0, st, tm.start, tm.stop, 0, b,
+                        static_cast<const uint16_t*>(hs), perm, k, s.blob.d, s.blob.I, buf);
+  return hipGetLastError();
+}
+
+}  // namespace wisp

@@ -73,6 +73,30 @@ bool ffn_dev_supported(const FfnShape& s, int T, int k, int has_shared);
 hipError_t launch_combine(int T, int k, int d, int has_shared, const float* w, const float* buf, float* y,
                           hipStream_t st, const LaunchTiming& tm);
 
+// Token batches (prefill): grouped GEMMs on the matrix cores over slot-indirected experts.
+// The (token, rank) pairs p = t*k + j are ordered by expert (stable); expert g of a launch owns
+// rows [row_off, row_off + rows) of that order.  Up to kMaxGroups experts per launch.
+constexpr int kMaxGroups = 32;
+constexpr int kGroupedMinTokens = 16;   // token batches from this size take the grouped GEMMs
+struct GroupedBatch {
+  const uint8_t* w[kMaxGroups];   // the expert's blob in its HBM slot
+  int32_t row_off[kMaxGroups];    // first row of the expert in the expert-sorted pair order
+  int32_t rows[kMaxGroups];       // pairs routed to the expert (>= 1)
+  int32_t tile_end[kMaxGroups];   // cumulative row-tile counts (grouped_row_tiles)
+  int32_t n_groups;
+};
+bool grouped_supported(const FfnShape& s, int has_shared);
+int grouped_row_tiles(int rows);
+// perm[off_e + i] = the i-th pair (ascending) routed to expert e; off_e = pairs of experts < e.
+hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t* perm, hipStream_t st,
+                                const LaunchTiming& tm);
+// hs[row] = bf16(silu(W1 x[t]) * (W3 x[t])) for every row of the batch's experts (row in sorted order).
+hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const void* x, const int32_t* perm, int k,
+                                 void* hs, hipStream_t st, const LaunchTiming& tm);
+// buf[t*(k+1)+j] = W2 hs[row] for the pair p = t*k+j of every row.
+hipError_t launch_grouped_down(const GroupedBatch& b, const FfnShape& s, const void* hs, const int32_t* perm, int k,
+                               float* buf, hipStream_t st, const LaunchTiming& tm);
+
 // Router: logits[t, e] = W_r[e] . x[t] (fp32 accumulate).
 hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int T, int N, int d, float* logits,
                                 hipStream_t st, const LaunchTiming& tm);

@@ -2,7 +2,8 @@
 //
 // router_logits: z[t, e] = W_r[e] . x[t] in fp32.  Decode sizes (T <= 8): one workgroup per
 //   expert row, so the fp32 router matrix is read by N workgroups at once (one HBM round trip);
-//   larger T: one wavefront per (expert row, four tokens).
+//   token batches: a workgroup per 16 tokens with LDS-staged slices of W_r (one wavefront per
+//   (expert row, four tokens) when d is not a multiple of 32).
 // router_select: top-k selection and gates (select.hpp), optionally publishing the ids to the
 //   host pager through host-coherent memory.
 #include <hip/hip_ext.h>
@@ -103,6 +104,59 @@ __global__ void __launch_bounds__(256) router_logits_wide_kernel(const float* __
   }
 }
 
+// Token-batch logits: a workgroup per 16 tokens computes their logits against all N <= 256 router
+// rows, staging 32-column slices of W_r and of the tokens in LDS (fp32; padded rows keep the
+// 16-byte reads conflict-free).  Thread e owns router row e (N <= 128: two half-blocks of 8 tokens
+// each).  Every logit is one fp32 FMA chain in ascending column order.
+template <int XT, int TPT>
+__global__ void __launch_bounds__(256) router_logits_tiled_kernel(const float* __restrict__ wr,
+                                                                  const void* __restrict__ x, int T, int N, int d,
+                                                                  float* __restrict__ logits) {
+  constexpr int TT = 16, KS = 32, LD = KS + 4;
+  __shared__ __attribute__((aligned(16))) float Ws[256 * LD];
+  __shared__ __attribute__((aligned(16))) float Xs[TT * LD];
+  const int tid = threadIdx.x;
+  const int t0 = blockIdx.x * TT;
+  const int e = TPT == 16 ? tid : (tid & 127);
+  const int tb = TPT == 16 ? 0 : (tid >> 7) * 8;
+  float acc[TPT];
+#pragma unroll
+  for (int t = 0; t < TPT; ++t) acc[t] = 0.f;
+  for (int k0 = 0; k0 < d; k0 += KS) {
+    for (int i = tid; i < N * (KS / 4); i += 256) {
+      const int r = i / (KS / 4), c = (i % (KS / 4)) * 4;
+      *reinterpret_cast<float4*>(&Ws[r * LD + c]) =
+          *reinterpret_cast<const float4*>(wr + static_cast<size_t>(r) * d + k0 + c);
+    }
+    if (tid < TT * (KS / 4)) {
+      const int r = tid / (KS / 4), c = (tid % (KS / 4)) * 4;
+      *reinterpret_cast<float4*>(&Xs[r * LD + c]) =
+          t0 + r < T ? load_x4<XT>(x, static_cast<size_t>(t0 + r) * d + k0 + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    __syncthreads();
+    if (e < N) {
+#pragma unroll
+      for (int kk = 0; kk < KS; kk += 4) {
+        const float4 w = *reinterpret_cast<const float4*>(&Ws[e * LD + kk]);
+#pragma unroll
+        for (int t = 0; t < TPT; ++t) {
+          const float4 v = *reinterpret_cast<const float4*>(&Xs[(tb + t) * LD + kk]);
+          acc[t] = fmaf(w.x, v.x, acc[t]);
+          acc[t] = fmaf(w.y, v.y, acc[t]);
+          acc[t] = fmaf(w.z, v.z, acc[t]);
+          acc[t] = fmaf(w.w, v.w, acc[t]);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (e < N) {
+#pragma unroll
+    for (int t = 0; t < TPT; ++t)
+      if (t0 + tb + t < T) logits[static_cast<size_t>(t0 + tb + t) * N + e] = acc[t];
+  }
+}
+
 // Selection (select.hpp) of the workgroup's four tokens; wave w, lane j < k writes rank j of
 // token blockIdx.x * 4 + w.  The indices can also be published to host-coherent memory as 64-bit
 // (seq << 32 | id) words: the host knows an entry is current from its tag alone, so it needs no
@@ -139,6 +193,26 @@ hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int
     else
       hipExtLaunchKernelGGL(router_logits_wide_kernel<DT_BF16>, grid, block, 0, st, tm.start, tm.stop, 0, wr, x, T, N,
                             d, logits);
+    return hipGetLastError();
+  }
+  if (d % 32 == 0 && N <= 256) {
+    dim3 grid((T + 15) / 16), block(256);
+    const bool half = N <= 128;
+    if (x_dtype == DT_F32) {
+      if (half)
+        hipExtLaunchKernelGGL(router_logits_tiled_kernel<DT_F32, 8>, grid, block, 0, st, tm.start, tm.stop, 0, wr, x,
+                              T, N, d, logits);
+      else
+        hipExtLaunchKernelGGL(router_logits_tiled_kernel<DT_F32, 16>, grid, block, 0, st, tm.start, tm.stop, 0, wr,
+                              x, T, N, d, logits);
+    } else {
+      if (half)
+        hipExtLaunchKernelGGL(router_logits_tiled_kernel<DT_BF16, 8>, grid, block, 0, st, tm.start, tm.stop, 0, wr,
+                              x, T, N, d, logits);
+      else
+        hipExtLaunchKernelGGL(router_logits_tiled_kernel<DT_BF16, 16>, grid, block, 0, st, tm.start, tm.stop, 0, wr,
+                              x, T, N, d, logits);
+    }
     return hipGetLastError();
   }
   dim3 grid((N + 3) / 4, (T + 3) / 4), block(256);

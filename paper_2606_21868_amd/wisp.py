@@ -77,7 +77,8 @@ _SIGS = {
     "wisp_expert_in_slot": [_P, _I, _I, ctypes.POINTER(_I)],
     "wisp_read_slot": [_P, _I, _I, _P],
     "wisp_set_profiling": [_P, _I],
-    "wisp_kernel_times": [_P, _I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_U64), ctypes.POINTER(_U64)],
+    "wisp_kernel_times": [_P, _I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_U64), ctypes.POINTER(_U64),
+                          ctypes.POINTER(_U64)],
     "wisp_reset_kernel_times": [_P],
     "wisp_probe_h2d": [_P, _I, _I, ctypes.POINTER(ctypes.c_double)],
     "wisp_hbm_copy": [_P, _P, _U64, _P],
@@ -252,9 +253,10 @@ class Context:
         ms = ctypes.c_double()
         n = _U64()
         b = _U64()
-        check(lib().wisp_kernel_times(self.h, kclass, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(b)),
-              "wisp_kernel_times")
-        return dict(total_ms=ms.value, launches=n.value, bytes=b.value)
+        f = _U64()
+        check(lib().wisp_kernel_times(self.h, kclass, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(b),
+                                      ctypes.byref(f)), "wisp_kernel_times")
+        return dict(total_ms=ms.value, launches=n.value, bytes=b.value, flops=f.value)
 
     def reset_kernel_times(self):
         check(lib().wisp_reset_kernel_times(self.h), "wisp_reset_kernel_times")

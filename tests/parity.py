@@ -105,20 +105,23 @@ def check_pager(wl, cap, gpu_idx, hits, misses, chunks=None):
     return True
 
 
-def check_outputs(run, y_gpu, points, ora_idx=None, threads=None):
-    """Oracle layer output at the given (step, layer) points; returns the worst row-relative error."""
+def check_outputs(run, y_gpu, points, ora_idx=None, threads=None, tokens=None):
+    """Oracle layer output at the given (step, layer) points (all tokens, or the listed ones);
+    returns the worst row-relative error."""
     wl = run.wl
     tol = tolerance(wl)
     worst = 0.0
     worst_el = 0.0
+    tok = np.arange(wl.T) if tokens is None else np.asarray(tokens)
     for (s, l) in points:
         blobs = run.master_ptrs(l)
         shared = run.shared_ptr(l)
-        idx, g, y, _, _ = oracle.moe_layer(wl.route, blobs, run.wr_host[l], run.x_host[l, s], wl.k, wl.I, wl.w_dtype,
+        x = np.ascontiguousarray(run.x_host[l, s][tok])
+        idx, g, y, _, _ = oracle.moe_layer(wl.route, blobs, run.wr_host[l], x, wl.k, wl.I, wl.w_dtype,
                                            shared, wl.n_groups, wl.topk_groups)
         if ora_idx is not None:
-            assert np.array_equal(idx, ora_idx[s, l])
-        yg = y_gpu[s, l].astype(np.float64)
+            assert np.array_equal(idx, ora_idx[s, l][tok])
+        yg = y_gpu[s, l][tok].astype(np.float64)
         scale = np.abs(y).max(axis=-1)
         row_err = np.abs(yg - y).max(axis=-1) / scale
         el = np.abs(yg - y) / np.maximum(np.abs(y), 1e-6 * scale[:, None])
@@ -126,3 +129,85 @@ def check_outputs(run, y_gpu, points, ora_idx=None, threads=None):
         worst_el = max(worst_el, float(el.max()))
         assert row_err.max() <= tol, f"step {s} layer {l}: row-relative error {row_err.max():.3e} > {tol}"
     return worst, worst_el
+
+
+def run_case(wl, cap, steps, sample_points=None, check_all_outputs=False, tokens=None, expect_grouped=None):
+    """Paged run from a cold table, checked against the oracle (routing, pager, outputs at all or the
+    sampled (step, layer) points, optionally on a subset of tokens); the device pager where it
+    applies; then the fully resident run (C = N, preloaded) must give bit-identical outputs."""
+    import pytest
+
+    from paper_2606_21868_amd import wisp
+    log(f"[case] {wl.name} L={wl.L} d={wl.d} I={wl.I} N={wl.N} k={wl.k} T={wl.T} steps={steps} C={cap}")
+    run = wisp.DecodeRun(wl, device=0, steps=steps)
+    try:
+        run.generate()
+        log(f"  generated in {run.gen_seconds:.1f}s; paged decode from cold")
+        assert run.set_cap(cap) == cap
+        if expect_grouped is not None:
+            run.ctx.set_profiling((1 << wisp.K_GROUPED_GATEUP) | (1 << wisp.K_FFN_GATEUP))
+        out = run.decode(record=True)
+        if expect_grouped is not None:
+            run.ctx.set_profiling(0)
+            n_grouped = run.ctx.kernel_times(wisp.K_GROUPED_GATEUP)["launches"]
+            n_items = run.ctx.kernel_times(wisp.K_FFN_GATEUP)["launches"]
+            assert (n_grouped > 0, n_items > 0) == (expect_grouped, not expect_grouped), (n_grouped, n_items)
+            log(f"  expert FFN path: {'grouped MFMA GEMMs' if expect_grouped else 'per-item GEMV'} "
+                f"({n_grouped + n_items} gate/up launches)")
+        log("  oracle routing")
+        ora_idx, ora_g, margin, gmargin, scores = oracle_routing(run, steps)
+        exempt, reordered = check_routing(wl, out["idx"], ora_idx, margin, gmargin, scores)
+        log(f"  routing ok ({len(exempt)} near-tie layer-steps exempt, {len(reordered)} with near-equal ranks "
+            f"swapped); pager vs Algorithm 1 simulator")
+        assert len(exempt) + len(reordered) <= max(2, steps * wl.L * wl.T // 1000)
+        check_pager(wl, cap, out["idx"], out["hits"], out["misses"], out["chunks"])
+        # gates: renormalised, positive, and equal to the oracle's gate of the same expert
+        w = out["w"]
+        assert np.allclose(w.sum(-1), 1.0, atol=1e-5) and (w > 0).all()
+        gate_err = 0.0
+        for s in range(steps):
+            for l in range(wl.L):
+                if (s, l) in exempt:
+                    continue
+                for t in range(wl.T):
+                    og = dict(zip(ora_idx[s, l, t].tolist(), ora_g[s, l, t].tolist()))
+                    for e, g in zip(out["idx"][s, l, t].tolist(), w[s, l, t].tolist()):
+                        gate_err = max(gate_err, abs(g - og[e]))
+        assert gate_err < 1e-5, gate_err
+        if check_all_outputs:
+            points = [(s, l) for s in range(steps) for l in range(wl.L) if (s, l) not in exempt]
+        else:
+            points = [p for p in sample_points if p not in exempt]
+        log(f"  outputs at {len(points)} (step, layer) points")
+        worst, worst_el = check_outputs(run, out["y"], points, ora_idx, tokens=tokens)
+        log(f"  worst row-relative error {worst:.3e} (elementwise {worst_el:.3e}); total misses "
+            f"{int(out['misses'].sum())} of {int(out['hits'].sum() + out['misses'].sum())} references")
+        tables = [[run.ctx.slot_of(l, e) for e in range(wl.N)] for l in range(wl.L)]
+        # the device pager: same trace from cold -> same decisions, same slots, same bits
+        device_ok = cap >= wl.T * wl.k and wl.T <= 4
+        run.ctx.masters_ready()            # drops every resident expert
+        run.ctx.reset_stats()
+        if device_ok:
+            run.ctx.set_pager(wisp.PAGER_DEVICE)
+            dev = run.decode(record=True)
+            assert np.array_equal(dev["idx"], out["idx"])
+            assert np.array_equal(dev["hits"], out["hits"]) and np.array_equal(dev["misses"], out["misses"])
+            assert [[run.ctx.slot_of(l, e) for e in range(wl.N)] for l in range(wl.L)] == tables
+            assert np.array_equal(dev["y"].view(np.uint32), out["y"].view(np.uint32)), "device pager changed bits"
+            log("  device pager: same routing, faults, slot tables and output bits as the host pager")
+        else:
+            with pytest.raises(wisp.WispError) as ei:
+                run.ctx.set_pager(wisp.PAGER_DEVICE)
+            assert ei.value.status == wisp.E_INVAL
+        # fully resident: C = N, preloaded, same kernels -> bit-identical, no faults
+        assert run.set_cap(wl.N) == wl.N
+        run.ctx.preload()
+        run.ctx.reset_stats()
+        res = run.decode(record=True)
+        assert int(res["misses"].sum()) == 0
+        assert np.array_equal(res["idx"], out["idx"])
+        assert np.array_equal(res["y"].view(np.uint32), out["y"].view(np.uint32)), "paged != resident bits"
+        log(f"  paged output bit-identical to the fully resident run ({'device' if device_ok else 'host'} pager)")
+        return out
+    finally:
+        run.close()

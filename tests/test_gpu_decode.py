@@ -9,80 +9,12 @@ import numpy as np
 import pytest
 
 import oracle
-from parity import check_outputs, check_pager, check_routing, log, oracle_routing
+from parity import run_case as _run_case
 from paper_2606_21868_amd.workloads import WORKLOADS
 
 torch = pytest.importorskip("torch")
 
 pytestmark = pytest.mark.gpu
-
-
-def _run_case(wl, cap, steps, sample_points=None, check_all_outputs=False):
-    from paper_2606_21868_amd import wisp
-    log(f"[case] {wl.name} L={wl.L} d={wl.d} I={wl.I} N={wl.N} k={wl.k} T={wl.T} steps={steps} C={cap}")
-    run = wisp.DecodeRun(wl, device=0, steps=steps)
-    try:
-        run.generate()
-        log(f"  generated in {run.gen_seconds:.1f}s; paged decode from cold")
-        assert run.set_cap(cap) == cap
-        out = run.decode(record=True)
-        log("  oracle routing")
-        ora_idx, ora_g, margin, gmargin, scores = oracle_routing(run, steps)
-        exempt, reordered = check_routing(wl, out["idx"], ora_idx, margin, gmargin, scores)
-        log(f"  routing ok ({len(exempt)} near-tie layer-steps exempt, {len(reordered)} with near-equal ranks "
-            f"swapped); pager vs Algorithm 1 simulator")
-        assert len(exempt) + len(reordered) <= max(2, steps * wl.L // 1000)
-        check_pager(wl, cap, out["idx"], out["hits"], out["misses"], out["chunks"])
-        # gates: renormalised, positive, and equal to the oracle's gate of the same expert
-        w = out["w"]
-        assert np.allclose(w.sum(-1), 1.0, atol=1e-5) and (w > 0).all()
-        gate_err = 0.0
-        for s in range(steps):
-            for l in range(wl.L):
-                if (s, l) in exempt:
-                    continue
-                for t in range(wl.T):
-                    og = dict(zip(ora_idx[s, l, t].tolist(), ora_g[s, l, t].tolist()))
-                    for e, g in zip(out["idx"][s, l, t].tolist(), w[s, l, t].tolist()):
-                        gate_err = max(gate_err, abs(g - og[e]))
-        assert gate_err < 1e-5, gate_err
-        if check_all_outputs:
-            points = [(s, l) for s in range(steps) for l in range(wl.L) if (s, l) not in exempt]
-        else:
-            points = [p for p in sample_points if p not in exempt]
-        log(f"  outputs at {len(points)} (step, layer) points")
-        worst, worst_el = check_outputs(run, out["y"], points, ora_idx)
-        log(f"  worst row-relative error {worst:.3e} (elementwise {worst_el:.3e}); total misses "
-            f"{int(out['misses'].sum())} of {int(out['hits'].sum() + out['misses'].sum())} references")
-        tables = [[run.ctx.slot_of(l, e) for e in range(wl.N)] for l in range(wl.L)]
-        # the device pager: same trace from cold -> same decisions, same slots, same bits
-        device_ok = cap >= wl.T * wl.k and wl.T <= 4
-        run.ctx.masters_ready()            # drops every resident expert
-        run.ctx.reset_stats()
-        if device_ok:
-            run.ctx.set_pager(wisp.PAGER_DEVICE)
-            dev = run.decode(record=True)
-            assert np.array_equal(dev["idx"], out["idx"])
-            assert np.array_equal(dev["hits"], out["hits"]) and np.array_equal(dev["misses"], out["misses"])
-            assert [[run.ctx.slot_of(l, e) for e in range(wl.N)] for l in range(wl.L)] == tables
-            assert np.array_equal(dev["y"].view(np.uint32), out["y"].view(np.uint32)), "device pager changed bits"
-            log("  device pager: same routing, faults, slot tables and output bits as the host pager")
-        else:
-            with pytest.raises(wisp.WispError) as ei:
-                run.ctx.set_pager(wisp.PAGER_DEVICE)
-            assert ei.value.status == wisp.E_INVAL
-        # fully resident: C = N, preloaded, same kernels -> bit-identical, no faults
-        assert run.set_cap(wl.N) == wl.N
-        run.ctx.preload()
-        run.ctx.reset_stats()
-        res = run.decode(record=True)
-        assert int(res["misses"].sum()) == 0
-        assert np.array_equal(res["idx"], out["idx"])
-        assert np.array_equal(res["y"].view(np.uint32), out["y"].view(np.uint32)), "paged != resident bits"
-        log(f"  paged output bit-identical to the fully resident run ({'device' if device_ok else 'host'} pager)")
-        return out
-    finally:
-        run.close()
 
 
 def test_tiny_fp32_full():

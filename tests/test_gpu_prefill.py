@@ -1,0 +1,51 @@
+"""GPU parity of the token-batch (prefill) path through the C ABI, against the oracle.
+
+A prefill step routes a batch of prompt tokens per layer; the union of their experts exceeds the
+cap, so each layer-step is several chunked Algorithm 1 steps, and the expert FFN runs as grouped
+GEMMs on the matrix cores (the pairs ordered by expert on the device).  Checked as in decode:
+routing and per-expert gates, hit/miss/chunk counts against the oracle's simulator, outputs within
+the bf16 tolerance, and bit-identity with the fully resident run (C = N).
+"""
+import numpy as np
+import pytest
+
+from parity import run_case
+from paper_2606_21868_amd.workloads import WORKLOADS
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+
+def test_prefill_qwen3_shape_reduced():
+    # the prefill layer shape (d=2048, I=768, 128 experts top-8, C=32) at 2 layers x 128 tokens:
+    # ~8 rows per expert, four chunks per layer-step
+    wl = WORKLOADS["qwen3-30b-a3b-prefill"].with_(L=2, T=128)
+    out = run_case(wl, 32, 1, check_all_outputs=True, expect_grouped=True)
+    assert out["chunks"].min() >= 4
+
+
+def test_prefill_multi_tile_ragged():
+    # several 64-row tiles per expert with ragged last tiles, a ragged 16-token router tile
+    # (520 = 32 * 16 + 8), and small caps (16 experts, C = 5 -> four chunks)
+    wl = WORKLOADS["qwen3-30b-a3b-prefill"].with_(L=2, T=520, d=256, I=128, N=16, k=4)
+    out = run_case(wl, 5, 1, check_all_outputs=True, expect_grouped=True)
+    assert out["chunks"].min() >= 4
+
+
+def test_prefill_below_grouped_threshold():
+    # a 12-token batch stays on the per-item GEMV path (one partial tile of the token-batch router)
+    wl = WORKLOADS["qwen3-30b-a3b-prefill"].with_(L=2, T=12, d=256, I=128, N=16, k=4)
+    run_case(wl, 5, 1, check_all_outputs=True, expect_grouped=False)
+
+
+def test_prefill_full_size_sampled():
+    """The prefill workload at full size (48 layers x 2048 tokens, 57.98 GB of masters, C = 32):
+    every routing decision and paging count against the oracle; outputs of 24 sampled tokens at
+    four layers; bit-identity with the fully resident run."""
+    wl = WORKLOADS["qwen3-30b-a3b-prefill"]
+    rng = np.random.default_rng(1)
+    tokens = np.sort(np.concatenate([[0, wl.T - 1], rng.choice(np.arange(1, wl.T - 1), 22, replace=False)]))
+    points = [(0, 0), (0, 17), (0, 30), (0, wl.L - 1)]
+    out = run_case(wl, wl.cap, 1, sample_points=points, tokens=tokens, expect_grouped=True)
+    assert int(out["misses"].sum()) == int((out["hits"] + out["misses"]).sum())   # a cold pass: all compulsory
