@@ -16,7 +16,11 @@ Reported beside the throughput:
   path_roofline  the whole path against T_roof = sum over layer-steps of HBM bytes / 8 TB/s +
                  fault bytes / measured host-link bandwidth (exact fault counts of the run);
   cpu_baseline   the fp64 CPU oracle (fully resident layer) on a bounded sample of the same
-                 workload, on this host's cores.
+                 workload, on this host's cores;
+  prefill        the Qwen3-30B-A3B-shaped prefill chunk (2048 tokens per layer, same weights and
+                 cap): tokens/s of a cold pass against T_roof = fault bytes / link + max(HBM bytes /
+                 8 TB/s, FLOPs / 2.5 PFLOP/s), and the matrix-core rate of the grouped GEMMs in a
+                 fully resident pass.
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
 from __future__ import annotations
@@ -33,6 +37,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0      # dense bf16 matrix-core peak of the MI355X
+PREFILL_WORKLOAD = "qwen3-30b-a3b-prefill"
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "ffn_gateup_qwen3-30b-a3b-decode_hbm_traffic.txt")
 FFN_SOURCE = os.path.join(ROOT, "paper_2606_21868_amd", "csrc", "expert_ffn.hip")
 
@@ -105,6 +111,88 @@ def cpu_baseline(run, wl, start_step, max_tokens=24, budget_s=15.0):
                        f"(fully resident fp64 layer, weights read from the same pinned host masters), {dt:.1f} s")
 
 
+def prefill_leg(wisp, torch, link, passes=3):
+    """Prefill tokens/s of the token-batch path (2048 tokens per layer, union 128 > C = 32, so four
+    chunked Algorithm 1 steps per layer, grouped MFMA GEMMs), from cold slot tables each pass as the
+    workload prescribes; then a fully resident pass (C = N, preloaded) for the matrix-core rate of
+    the grouped GEMMs alone."""
+    from paper_2606_21868_amd.workloads import WORKLOADS
+    wl = WORKLOADS[PREFILL_WORKLOAD]
+    run = wisp.DecodeRun(wl, device=0, steps=1)
+    try:
+        t0 = time.time()
+        run.generate()
+        log(f"prefill: generated {wl.L * wl.N} expert blobs and {wl.T} x {wl.L} token rows in {time.time() - t0:.1f} s")
+        assert run.set_cap(wl.cap) == wl.cap
+        times = []
+        out = None
+        for i in range(passes + 1):                    # the first pass is a warmup
+            run.ctx.masters_ready()                    # cold: every slot empty
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            out = run.decode(record=False, steps=1)
+            torch.cuda.synchronize()
+            if i > 0:
+                times.append(time.perf_counter() - t1)
+        times.sort()
+        el = times[len(times) // 2]
+        misses = int(out["misses"].sum())
+        distinct = int((out["hits"] + out["misses"]).sum())
+        pairs = wl.T * wl.k
+        flops = 6.0 * wl.d * wl.I * pairs * wl.L
+        t_link = misses * wl.blob / (link * 1e9)
+        t_hbm = distinct * wl.blob / (HBM_PEAK_GBPS * 1e9)
+        t_mfma = flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+        t_roof = t_link + max(t_hbm, t_mfma)
+        log(f"prefill: cold pass {el * 1e3:.1f} ms -> {wl.T / el:.0f} tokens/s, {t_roof / el:.3f} of the roofline")
+        # fully resident: the same kernels with no faults; grouped GEMMs timed by HIP events
+        assert run.set_cap(wl.N) == wl.N
+        run.ctx.preload()
+        run.decode(record=False, steps=1)
+        mask = (1 << wisp.K_GROUPED_GATEUP) | (1 << wisp.K_GROUPED_DOWN) | (1 << wisp.K_PERMUTE) | \
+               (1 << wisp.K_ROUTER_LOGITS) | (1 << wisp.K_ROUTER_SELECT) | (1 << wisp.K_COMBINE)
+        rtimes = []
+        for i in range(passes):
+            if i == passes - 1:
+                run.ctx.reset_kernel_times()
+                run.ctx.set_profiling(mask)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            run.decode(record=False, steps=1)
+            torch.cuda.synchronize()
+            rtimes.append(time.perf_counter() - t1)
+        run.ctx.set_profiling(0)
+        kern = {}
+        gflops, gms = 0, 0.0
+        for kc in (wisp.K_GROUPED_GATEUP, wisp.K_GROUPED_DOWN, wisp.K_PERMUTE, wisp.K_ROUTER_LOGITS,
+                   wisp.K_ROUTER_SELECT, wisp.K_COMBINE):
+            t = run.ctx.kernel_times(kc)
+            if not t["launches"]:
+                continue
+            e = dict(launches=t["launches"], avg_us=t["total_ms"] * 1e3 / t["launches"], total_ms=t["total_ms"])
+            if t["flops"]:
+                e["TFLOPs"] = t["flops"] / (t["total_ms"] * 1e-3) / 1e12
+                gflops += t["flops"]
+                gms += t["total_ms"]
+            kern[wisp.KERNEL_CLASS_NAMES[kc]] = e
+        achieved = gflops / (gms * 1e-3) / 1e12 if gms > 0 else None
+        rtimes.sort()
+        rel = rtimes[len(rtimes) // 2]
+        log(f"prefill: resident pass {rel * 1e3:.2f} ms -> {wl.T / rel:.0f} tokens/s; grouped GEMMs "
+            f"{achieved:.0f} TFLOP/s ({achieved / MFMA_BF16_PEAK_TFLOPS:.3f} of the bf16 peak)")
+        return dict(
+            workload=wl.description, tokens_per_s=wl.T / el, pass_ms=el * 1e3, passes=len(times),
+            pass_ms_all=[t * 1e3 for t in times], cap_per_layer=wl.cap, faults=misses, distinct_experts=distinct,
+            roofline=dict(t_roof_s=t_roof, t_link_s=t_link, t_hbm_s=t_hbm, t_mfma_s=t_mfma, frac=t_roof / el,
+                          roofline_tokens_per_s=wl.T / t_roof, link_GBps_measured=link, flops=flops),
+            resident=dict(tokens_per_s=wl.T / rel, pass_ms=rel * 1e3, kernels=kern),
+            mfma=dict(bound="mfma", achieved=achieved, peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
+                      frac=achieved / MFMA_BF16_PEAK_TFLOPS if achieved else None,
+                      kernels="grouped gate/up + down (bf16 v_mfma_f32_32x32x16), resident pass"))
+    finally:
+        run.close()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -117,6 +205,7 @@ def main():
                          "gate/up GEMV, on which the roofline is reported)")
     ap.add_argument("--pager", choices=["both", "device", "host"], default="both",
                     help="which pager(s) to time; value is the device pager's when it runs")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the prefill leg")
     ap.add_argument("--census-steps", type=int, default=24,
                     help="extra decode steps after the timed region with every kernel class timed (0 = skip)")
     args = ap.parse_args()
@@ -242,6 +331,10 @@ def main():
         log("cpu baseline (oracle)")
         cpu = cpu_baseline(run, wl, warmup)
         log(f"cpu oracle {cpu['value']:.3f} tokens/s on {cpu['cores']} threads")
+    run.close()
+    prefill = None
+    if not args.no_prefill:
+        prefill = prefill_leg(wisp, torch, link)
 
     result = {
         "metric": "paged MoE decode tokens/s at fixed VRAM expert budget",
@@ -265,8 +358,8 @@ def main():
         "pager": main_pass,
         "passes": passes,
         "kernel_timing": args.kernel_timing,
+        "prefill": prefill,
     }
-    run.close()
     print(json.dumps(result), flush=True)
 
 
