@@ -69,6 +69,11 @@ typedef struct {
   int32_t w_dtype;     /* wisp_dtype of expert weights */
   int32_t x_dtype;     /* WISP_F32 or WISP_BF16 hidden states */
   int32_t max_tokens;  /* largest T passed to route / forward */
+  int32_t pageable_masters; /* 0: masters in pinned host memory (one DMA copy per fault).  1: masters
+                             * in ordinary pageable memory, for master sets larger than the pinned
+                             * memory a process may hold: faults are copied piece by piece through a
+                             * small pinned bounce ring by host threads (wisp_page_in then blocks
+                             * while it stages), and the device pager is not available. */
 } wisp_model_desc;
 
 typedef struct {

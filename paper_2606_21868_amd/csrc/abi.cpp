@@ -9,6 +9,7 @@
 // overlaps the fills.  When the union of a layer-step exceeds C, chunk i+1's fills wait for
 // chunk i's FFN.
 #include <hip/hip_runtime.h>
+#include <sys/mman.h>
 
 #include <algorithm>
 #include <cstring>
@@ -18,7 +19,10 @@
 
 #include "kernels.hpp"
 #include "slot_table.hpp"
+#include "staging.hpp"
 #include "wisp.h"
+
+#include <thread>
 
 using namespace wisp;
 
@@ -75,6 +79,9 @@ struct wisp_ctx {
   size_t master_stride = 0;
   std::vector<uint8_t*> masters;
   std::vector<uint8_t*> shared_master;
+  bool pageable = false;             // masters in pageable memory (mapped, not pinned)
+  size_t master_map_bytes = 0;       // bytes of one layer's mapping (pageable masters)
+  std::unique_ptr<BounceRing> bounce;
   int32_t cap = 0;
   std::vector<LayerState> layers;
   hipStream_t side = nullptr;
@@ -203,6 +210,7 @@ wisp_status check_desc(const wisp_model_desc* d) {
   if ((d->d_model / epl) % 8 || (d->d_ff / epl) % 8)
     return fail(WISP_E_INVAL, "d_model and d_ff must be multiples of 8 x 16-byte chunks");
   if (d->has_shared != 0 && d->has_shared != 1) return fail(WISP_E_INVAL, "has_shared must be 0 or 1");
+  if (d->pageable_masters != 0 && d->pageable_masters != 1) return fail(WISP_E_INVAL, "pageable_masters must be 0 or 1");
   return WISP_OK;
 }
 
@@ -232,8 +240,11 @@ void free_ctx(wisp_ctx* c) {
     for (auto e : L.fill_ev) hipEventDestroy(e);
     for (auto e : L.chunk_ev) hipEventDestroy(e);
   }
-  for (auto* p : c->masters) if (p) hipHostFree(p);
-  for (auto* p : c->shared_master) if (p) hipHostFree(p);
+  c->bounce.reset();
+  for (auto* p : c->masters)
+    if (p) c->pageable ? (void)munmap(p, c->master_map_bytes) : (void)hipHostFree(p);
+  for (auto* p : c->shared_master)
+    if (p) c->pageable ? (void)munmap(p, c->master_stride) : (void)hipHostFree(p);
   for (auto& t : c->timed) { hipEventDestroy(t.a); hipEventDestroy(t.b); }
   for (auto e : c->ev_pool) hipEventDestroy(e);
   if (c->route_ev) hipEventDestroy(c->route_ev);
@@ -343,6 +354,17 @@ wisp_status with_host_tables(wisp_ctx* c, F body) {
 }
 
 // Enqueue the fills of chunk ci of `layer`'s pending plan on the side stream.
+// host master -> device copy on `st`: one DMA copy from pinned masters, or staged through the
+// pinned bounce ring from pageable ones.
+wisp_status master_h2d(wisp_ctx* c, void* dst, const uint8_t* src, size_t bytes, hipStream_t st) {
+  if (!c->pageable) {
+    WISP_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, st), "hipMemcpyAsync(master)");
+  } else {
+    WISP_HIP(c->bounce->copy_to_device(dst, src, bytes, st), "staged copy(master)");
+  }
+  return WISP_OK;
+}
+
 wisp_status issue_fills(wisp_ctx* c, int32_t layer, size_t ci) {
   LayerState& L = c->layers[layer];
   const ChunkPlan& cp = L.plan.chunks[ci];
@@ -356,9 +378,8 @@ wisp_status issue_fills(wisp_ctx* c, int32_t layer, size_t ci) {
   if (tm.start) WISP_HIP(hipEventRecord(tm.start, c->side), "hipEventRecord");
   for (size_t i = 0; i < cp.experts.size(); ++i) {
     if (!cp.fault[i]) continue;
-    WISP_HIP(hipMemcpyAsync(L.slot_mem[cp.slots[i]], c->master(layer, cp.experts[i]), c->blob.bytes,
-                            hipMemcpyHostToDevice, c->side),
-             "hipMemcpyAsync(fill)");
+    wisp_status s = master_h2d(c, L.slot_mem[cp.slots[i]], c->master(layer, cp.experts[i]), c->blob.bytes, c->side);
+    if (s != WISP_OK) return s;
   }
   if (tm.stop) WISP_HIP(hipEventRecord(tm.stop, c->side), "hipEventRecord");
   timing_end(c, tm, WISP_K_H2D_FILL, static_cast<uint64_t>(cp.n_faults) * c->blob.bytes);
@@ -464,15 +485,36 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
     free_ctx(c);
     return fail(st, m);
   };
+  c->pageable = desc->pageable_masters != 0;
+  c->master_map_bytes = static_cast<size_t>(N) * c->master_stride;
+  auto host_alloc = [&](size_t bytes) -> uint8_t* {
+    if (c->pageable) {
+      void* m = mmap(nullptr, bytes, PROT_READ | PROT_WRITE, MAP_PRIVATE | MAP_ANONYMOUS | MAP_NORESERVE, -1, 0);
+      return m == MAP_FAILED ? nullptr : static_cast<uint8_t*>(m);
+    }
+    void* m = nullptr;
+    if (hipHostMalloc(&m, bytes, hipHostMallocDefault) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    return static_cast<uint8_t*>(m);
+  };
+  if (c->pageable) {
+    c->bounce.reset(new (std::nothrow) BounceRing());
+    const int hw = static_cast<int>(std::thread::hardware_concurrency());
+    if (!c->bounce || c->bounce->init(std::max(1, std::min(8, hw))) != hipSuccess)
+      return bail(WISP_E_NOMEM, "pinned bounce buffers for the pageable masters");
+  }
   for (int l = 0; l < L; ++l) {
     void* p = nullptr;
-    if (hipHostMalloc(&p, static_cast<size_t>(N) * c->master_stride, hipHostMallocDefault) != hipSuccess)
-      return bail(WISP_E_NOMEM, "hipHostMalloc of the expert masters failed");
-    c->masters[l] = static_cast<uint8_t*>(p);
+    c->masters[l] = host_alloc(c->master_map_bytes);
+    if (!c->masters[l])
+      return bail(WISP_E_NOMEM, c->pageable ? "mapping the pageable expert masters failed"
+                                            : "hipHostMalloc of the expert masters failed (pinned memory limit? "
+                                              "set pageable_masters)");
     if (desc->has_shared) {
-      if (hipHostMalloc(&p, c->master_stride, hipHostMallocDefault) != hipSuccess)
-        return bail(WISP_E_NOMEM, "hipHostMalloc of the shared-expert master failed");
-      c->shared_master[l] = static_cast<uint8_t*>(p);
+      c->shared_master[l] = host_alloc(c->master_stride);
+      if (!c->shared_master[l]) return bail(WISP_E_NOMEM, "allocating the shared-expert master failed");
       if (hipMalloc(&p, c->blob.bytes) != hipSuccess) return bail(WISP_E_NOMEM, "hipMalloc of a shared expert failed");
       c->layers[l].shared_dev = static_cast<uint8_t*>(p);
     }
@@ -545,11 +587,12 @@ static wisp_status masters_ready_host(wisp_ctx* ctx) {
     if (L.pending) return fail(WISP_E_STATE, "a page-in is pending");
   for (int l = 0; l < ctx->desc.n_layers; ++l) {
     LayerState& L = ctx->layers[l];
-    if (ctx->desc.has_shared)
-      WISP_HIP(hipMemcpy(L.shared_dev, ctx->shared_master[l], ctx->blob.bytes, hipMemcpyHostToDevice),
-               "hipMemcpy(shared expert)");
+    if (ctx->desc.has_shared &&
+        (s = master_h2d(ctx, L.shared_dev, ctx->shared_master[l], ctx->blob.bytes, ctx->side)) != WISP_OK)
+      return s;
     if (L.table) L.table->clear();
   }
+  WISP_HIP(hipStreamSynchronize(ctx->side), "hipStreamSynchronize(side)");
   return WISP_OK;
 }
 
@@ -658,9 +701,9 @@ static wisp_status preload_host(wisp_ctx* ctx) {
     for (const ChunkPlan& cp : plan.chunks)
       for (size_t i = 0; i < cp.experts.size(); ++i)
         if (cp.fault[i])
-          WISP_HIP(hipMemcpyAsync(L.slot_mem[cp.slots[i]], ctx->master(l, cp.experts[i]), ctx->blob.bytes,
-                                  hipMemcpyHostToDevice, ctx->side),
-                   "hipMemcpyAsync(preload)");
+          if ((s = master_h2d(ctx, L.slot_mem[cp.slots[i]], ctx->master(l, cp.experts[i]), ctx->blob.bytes,
+                              ctx->side)) != WISP_OK)
+            return s;
   }
   WISP_HIP(hipStreamSynchronize(ctx->side), "hipStreamSynchronize(side)");
   return WISP_OK;
@@ -704,6 +747,7 @@ wisp_status wisp_set_pager(wisp_ctx* ctx, int32_t pager) {
     const auto& d = ctx->desc;
     if (ctx->cap < 1) return fail(WISP_E_STATE, "no expert budget set");
     if (d.max_tokens > 4) return fail(WISP_E_INVAL, "the device pager handles max_tokens <= 4");
+    if (ctx->pageable) return fail(WISP_E_INVAL, "the device pager reads pinned masters; these are pageable");
     if (ctx->cap < d.max_tokens * d.top_k)
       return fail(WISP_E_INVAL, "the device pager needs C >= max_tokens * k (one Algorithm 1 step per layer-step)");
     if (!ffn_dev_supported(ctx->shape, d.max_tokens, d.top_k, d.has_shared))
@@ -1142,8 +1186,12 @@ wisp_status wisp_probe_h2d(wisp_ctx* ctx, int32_t count, int32_t reps, double* g
     e = hipEventRecord(a, ctx->side);
     for (int i = 0; i < count && e == hipSuccess; ++i, ++src) {
       const int l = (src / ne) % nl, x = src % ne;
-      e = hipMemcpyAsync(static_cast<uint8_t*>(scratch) + static_cast<size_t>(i) * B, ctx->master(l, x), B,
-                         hipMemcpyHostToDevice, ctx->side);
+      if (!ctx->pageable)
+        e = hipMemcpyAsync(static_cast<uint8_t*>(scratch) + static_cast<size_t>(i) * B, ctx->master(l, x), B,
+                           hipMemcpyHostToDevice, ctx->side);
+      else
+        e = ctx->bounce->copy_to_device(static_cast<uint8_t*>(scratch) + static_cast<size_t>(i) * B,
+                                        ctx->master(l, x), B, ctx->side);
     }
     if (e == hipSuccess) e = hipEventRecord(b, ctx->side);
     if (e == hipSuccess) e = hipEventSynchronize(b);

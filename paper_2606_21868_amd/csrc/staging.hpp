@@ -1,0 +1,65 @@
+// Host->device copies out of pageable host memory, staged through a small pinned bounce ring.
+//
+// Expert masters normally live in pinned host memory and a fault is one DMA copy.  A machine may
+// cap the pinned memory of a process below the size of the master set; the masters then live in
+// ordinary pageable memory, and each copy goes piece by piece through pinned bounce buffers:
+// host threads copy a piece into a free buffer, a DMA copy on the stream moves it to the device,
+// and an event recorded after it frees the buffer again.  The host copy of the next piece overlaps
+// the DMA of the previous ones.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <condition_variable>
+#include <cstddef>
+#include <cstdint>
+#include <mutex>
+#include <thread>
+#include <vector>
+
+namespace wisp {
+
+// A fixed set of worker threads that split one memcpy between them.
+class CopyPool {
+ public:
+  explicit CopyPool(int threads);
+  ~CopyPool();
+  CopyPool(const CopyPool&) = delete;
+  CopyPool& operator=(const CopyPool&) = delete;
+  void copy(void* dst, const void* src, size_t bytes);   // returns when the copy is complete
+
+ private:
+  void worker(int id);
+  std::vector<std::thread> threads_;
+  std::mutex mu_;
+  std::condition_variable cv_, done_cv_;
+  uint8_t* dst_ = nullptr;
+  const uint8_t* src_ = nullptr;
+  size_t bytes_ = 0;
+  uint64_t generation_ = 0;
+  int pending_ = 0;
+  bool stop_ = false;
+};
+
+class BounceRing {
+ public:
+  static constexpr size_t kPieceBytes = 32ull << 20;
+  static constexpr int kBuffers = 4;
+  BounceRing() = default;
+  ~BounceRing();
+  BounceRing(const BounceRing&) = delete;
+  BounceRing& operator=(const BounceRing&) = delete;
+  hipError_t init(int threads);   // pinned buffers, events and the copy threads
+  // Enqueue dst[0, bytes) <- src[0, bytes) on `st`.  Blocks while every buffer still feeds a DMA
+  // copy that has not run; all work those copies wait for must already be enqueued.
+  hipError_t copy_to_device(void* dst, const uint8_t* src, size_t bytes, hipStream_t st);
+
+ private:
+  uint8_t* buf_[kBuffers] = {};
+  hipEvent_t ev_[kBuffers] = {};
+  bool used_[kBuffers] = {};
+  int next_ = 0;
+  CopyPool* pool_ = nullptr;
+};
+
+}  // namespace wisp

@@ -38,7 +38,7 @@ class WispError(RuntimeError):
 class ModelDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_layers", "d_model", "d_ff", "n_experts", "top_k", "n_groups", "topk_groups", "has_shared", "route",
-        "w_dtype", "x_dtype", "max_tokens")]
+        "w_dtype", "x_dtype", "max_tokens", "pageable_masters")]
 
 
 class PageStats(ctypes.Structure):
@@ -140,9 +140,9 @@ def _stream(s):
     return s.cuda_stream if hasattr(s, "cuda_stream") else int(s)
 
 
-def desc_of(wl, max_tokens=None):
+def desc_of(wl, max_tokens=None, pageable=False):
     return ModelDesc(wl.L, wl.d, wl.I, wl.N, wl.k, wl.n_groups, wl.topk_groups, int(wl.has_shared), wl.route,
-                     wl.w_dtype, wl.x_dtype, max_tokens or wl.T)
+                     wl.w_dtype, wl.x_dtype, max_tokens or wl.T, int(bool(pageable)))
 
 
 def expert_bytes(desc):
@@ -336,7 +336,7 @@ class DecodeRun:
     ([steps, L, T, d] on the device), and declares the masters ready.
     """
 
-    def __init__(self, wl, device=0, max_tokens=None, steps=None):
+    def __init__(self, wl, device=0, max_tokens=None, steps=None, pageable=False):
         import torch
         self.torch = torch
         self.wl = wl
@@ -345,7 +345,8 @@ class DecodeRun:
         self.dev = torch.device("cuda", device)
         self.stream = torch.cuda.Stream(device=self.dev)
         self.steps = steps or wl.steps
-        self.ctx = Context(desc_of(wl, max_tokens))
+        self.pageable = bool(pageable)
+        self.ctx = Context(desc_of(wl, max_tokens, pageable))
         self.blob_bytes = expert_bytes(self.ctx.desc)
         self.gen_seconds = None
 

@@ -131,15 +131,17 @@ def check_outputs(run, y_gpu, points, ora_idx=None, threads=None, tokens=None):
     return worst, worst_el
 
 
-def run_case(wl, cap, steps, sample_points=None, check_all_outputs=False, tokens=None, expect_grouped=None):
+def run_case(wl, cap, steps, sample_points=None, check_all_outputs=False, tokens=None, expect_grouped=None,
+             pageable=False):
     """Paged run from a cold table, checked against the oracle (routing, pager, outputs at all or the
     sampled (step, layer) points, optionally on a subset of tokens); the device pager where it
     applies; then the fully resident run (C = N, preloaded) must give bit-identical outputs."""
     import pytest
 
     from paper_2606_21868_amd import wisp
-    log(f"[case] {wl.name} L={wl.L} d={wl.d} I={wl.I} N={wl.N} k={wl.k} T={wl.T} steps={steps} C={cap}")
-    run = wisp.DecodeRun(wl, device=0, steps=steps)
+    log(f"[case] {wl.name} L={wl.L} d={wl.d} I={wl.I} N={wl.N} k={wl.k} T={wl.T} steps={steps} C={cap}"
+        f"{' (pageable masters)' if pageable else ''}")
+    run = wisp.DecodeRun(wl, device=0, steps=steps, pageable=pageable)
     try:
         run.generate()
         log(f"  generated in {run.gen_seconds:.1f}s; paged decode from cold")
@@ -184,7 +186,7 @@ def run_case(wl, cap, steps, sample_points=None, check_all_outputs=False, tokens
             f"{int(out['misses'].sum())} of {int(out['hits'].sum() + out['misses'].sum())} references")
         tables = [[run.ctx.slot_of(l, e) for e in range(wl.N)] for l in range(wl.L)]
         # the device pager: same trace from cold -> same decisions, same slots, same bits
-        device_ok = cap >= wl.T * wl.k and wl.T <= 4
+        device_ok = cap >= wl.T * wl.k and wl.T <= 4 and not pageable
         run.ctx.masters_ready()            # drops every resident expert
         run.ctx.reset_stats()
         if device_ok:
