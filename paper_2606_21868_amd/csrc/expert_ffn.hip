@@ -122,6 +122,13 @@ __device__ __forceinline__ void reg_chunk(const uint4* q, float* o) {
   }
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// acc + w.lo * x.lo + w.hi * x.hi on two packed bf16 pairs (one v_dot2c_f32_bf16).
+__device__ __forceinline__ float dot2_bf16(uint32_t w, uint32_t x, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), __builtin_bit_cast(bf16x2_t, x), acc, false);
+}
+
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
   u += 0x7FFFu + ((u >> 16) & 1u);
@@ -165,14 +172,8 @@ __device__ __forceinline__ void rows_body(const FfnItem& it, const uint8_t* rd, 
   const bool xreg = NLT > 0 && ntok == 1;
   uint4 xr[NLT > 0 ? NLT * XQ : 1];
   const int rbase0 = r_begin + wave * RPW;
-  if (xreg) {
-    const uint8_t* xrow = vin + static_cast<size_t>(MODE == MODE_GATEUP ? it.tok[0] : it.out[0]) * vin_stride * IS;
-#pragma unroll
-    for (int m = 0; m < (NLT > 0 ? NLT : 1); ++m)
-#pragma unroll
-      for (int q = 0; q < XQ; ++q)
-        xr[m * XQ + q] = reinterpret_cast<const uint4*>(xrow + static_cast<size_t>((m * LPR + sl) * EPL) * IS)[q];
-  } else {
+  const uint8_t* xrow = vin + static_cast<size_t>(MODE == MODE_GATEUP ? it.tok[0] : it.out[0]) * vin_stride * IS;
+  if (!xreg) {
     // stage the item's input rows (x for gate/up, h for down) in LDS
     for (int t = 0; t < ntok; ++t) {
       const int src_row = MODE == MODE_GATEUP ? it.tok[t] : it.out[t];
@@ -203,6 +204,19 @@ __device__ __forceinline__ void rows_body(const FfnItem& it, const uint8_t* rd, 
           if constexpr (MODE == MODE_GATEUP) b[u] = row1[m * LPR + sl];
         }
       }
+      if (xreg && m0 == 0) {
+        // the input slice is read after the weight loads are issued, through an address the
+        // compiler cannot see as loop-invariant, so neither the load nor its conversion is hoisted
+        // ahead of the weight loads (which would put two memory round trips in a row)
+        uint32_t opaque = 0;
+        asm volatile("" : "+s"(opaque));
+        const uint8_t* xp = xrow + opaque;
+#pragma unroll
+        for (int m = 0; m < (NLT > 0 ? NLT : 1); ++m)
+#pragma unroll
+          for (int q = 0; q < XQ; ++q)
+            xr[m * XQ + q] = reinterpret_cast<const uint4*>(xp + static_cast<size_t>((m * LPR + sl) * EPL) * IS)[q];
+      }
       if (wr && valid) {
         uint4* w0 = reinterpret_cast<uint4*>(wr + off0 + rr * row_stride_b);
         uint4* w1 = reinterpret_cast<uint4*>(wr + off1 + rr * row_stride_b);
@@ -220,6 +234,27 @@ __device__ __forceinline__ void rows_body(const FfnItem& it, const uint8_t* rd, 
         const int m = m0 + u;
         if (!(NLT > 0 || m < NL)) continue;
         const int col = (m * LPR + sl) * EPL;
+        if constexpr (WT == DT_BF16 && IT == DT_BF16) {
+          // packed bf16 pairs straight into v_dot2c_f32_bf16: a*b products of bf16 values are exact in
+          // fp32, so only the sums round; no unpacking of weights or inputs
+#pragma unroll
+          for (int t = 0; t < kMaxTokPerItem; ++t) {
+            if (t >= ntok) break;
+            const uint4 xq = xreg ? xr[(NLT > 0 ? m : 0) * XQ]
+                                  : *reinterpret_cast<const uint4*>(lds + t * row_bytes + col * 2);
+            acc0[t] = dot2_bf16(a[u].x, xq.x, acc0[t]);
+            acc0[t] = dot2_bf16(a[u].y, xq.y, acc0[t]);
+            acc0[t] = dot2_bf16(a[u].z, xq.z, acc0[t]);
+            acc0[t] = dot2_bf16(a[u].w, xq.w, acc0[t]);
+            if constexpr (MODE == MODE_GATEUP) {
+              acc1[t] = dot2_bf16(b[u].x, xq.x, acc1[t]);
+              acc1[t] = dot2_bf16(b[u].y, xq.y, acc1[t]);
+              acc1[t] = dot2_bf16(b[u].z, xq.z, acc1[t]);
+              acc1[t] = dot2_bf16(b[u].w, xq.w, acc1[t]);
+            }
+          }
+          continue;
+        }
         float wa[EPL], wb[EPL];
         decode_chunk<WT>(a[u], wa);
         if constexpr (MODE == MODE_GATEUP) decode_chunk<WT>(b[u], wb);
