@@ -41,11 +41,19 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
   return static_cast<uint16_t>(u >> 16);
 }
 
-// Tile -> (group, row tile, column tile).  Row tiles of a group are contiguous in blockIdx.x /
-// n_ctiles; column tiles of one row tile are adjacent launches (they share the gathered rows).
+// Tile -> (group, row tile, column tile).  Workgroups are dealt to the 8 XCDs round-robin by
+// blockIdx.x, and each XCD has its own L2; the logical tile order is remapped so that every XCD gets
+// one contiguous run of logical tiles.  In that order the column tiles of a row tile are adjacent
+// (they share the gathered rows) and so are the row tiles of an expert (they share its weights),
+// so those re-reads stay within one XCD's L2.
+constexpr int kXcds = 8;
 __device__ __forceinline__ void tile_of(const GroupedBatch& gb, int n_ctiles, int& g, int& mt, int& ct) {
-  const int mt_all = blockIdx.x / n_ctiles;
-  ct = blockIdx.x - mt_all * n_ctiles;
+  const int n = static_cast<int>(gridDim.x);
+  const int xcd = static_cast<int>(blockIdx.x) % kXcds, j = static_cast<int>(blockIdx.x) / kXcds;
+  const int q = n / kXcds, r = n % kXcds;
+  const int logical = xcd * q + min(xcd, r) + j;   // a bijection of [0, n)
+  const int mt_all = logical / n_ctiles;
+  ct = logical - mt_all * n_ctiles;
   g = 0;
   while (g + 1 < gb.n_groups && mt_all >= gb.tile_end[g]) ++g;
   mt = mt_all - (g > 0 ? gb.tile_end[g - 1] : 0);
