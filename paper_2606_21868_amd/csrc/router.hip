@@ -2,8 +2,8 @@
 //
 // router_logits: z[t, e] = W_r[e] . x[t] in fp32.  Decode sizes (T <= 8): one workgroup per
 //   expert row, so the fp32 router matrix is read by N workgroups at once (one HBM round trip);
-//   token batches: a workgroup per 16 tokens with LDS-staged slices of W_r (one wavefront per
-//   (expert row, four tokens) when d is not a multiple of 32).
+//   token batches: fp32 matrix cores (a 16-token x 16-row block per workgroup) when N is a
+//   multiple of 16 and d of 64, else a workgroup per 16 tokens with LDS-staged slices of W_r.
 // router_select: top-k selection and gates (select.hpp), optionally publishing the ids to the
 //   host pager through host-coherent memory.
 #include <hip/hip_ext.h>
@@ -26,40 +26,6 @@ __device__ __forceinline__ float4 load_x4(const void* x, size_t idx) {
     return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u),
                        __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xFFFF0000u));
   }
-}
-
-template <int XT>
-__global__ void __launch_bounds__(256) router_logits_kernel(const float* __restrict__ wr, const void* __restrict__ x,
-                                                            int T, int N, int d, float* __restrict__ logits) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int e = blockIdx.x * 4 + wave;
-  const int t0 = blockIdx.y * 4;
-  if (e >= N) return;
-  const int ntok = min(4, T - t0);
-  const float4* row = reinterpret_cast<const float4*>(wr + static_cast<size_t>(e) * d);
-  const int chunks = d / 4;
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int c = lane; c < chunks; c += 64) {
-    const float4 w = row[c];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      if (t >= ntok) break;
-      const float4 v = load_x4<XT>(x, static_cast<size_t>(t0 + t) * d + static_cast<size_t>(c) * 4);
-      acc[t] = fmaf(w.x, v.x, acc[t]);
-      acc[t] = fmaf(w.y, v.y, acc[t]);
-      acc[t] = fmaf(w.z, v.z, acc[t]);
-      acc[t] = fmaf(w.w, v.w, acc[t]);
-    }
-  }
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    if (t >= ntok) break;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) acc[t] += __shfl_xor(acc[t], off, 64);
-  }
-  if (lane == 0)
-    for (int t = 0; t < ntok; ++t) logits[static_cast<size_t>(t0 + t) * N + e] = acc[t];
 }
 
 // Decode-sized logits: one workgroup per expert row; 256 threads split the row (16-byte loads),
@@ -157,6 +123,62 @@ __global__ void __launch_bounds__(256) router_logits_tiled_kernel(const float* _
   }
 }
 
+// Token-batch logits on the fp32 matrix cores (v_mfma_f32_16x16x4_f32).  A workgroup computes a
+// 16-token x 16-row block; its four waves take one quarter of the columns each and their partial
+// sums are added in wave order through LDS.  W_r stays fp32 and x is widened exactly, so the
+// products are those of the FMA kernels and only the summation order differs.  Lane l owns token
+// l%16 and router row l%16; for each 16-column step it reads columns 4(l/16) .. +3 of both (one 8-
+// or 16-byte load each, issued a step ahead) for four MFMA steps, which keeps the column index of a
+// lane's A and B operands equal, as the product requires.  Output lane l: tokens 4(l/16) .. +3, row l%16.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+template <int XT>
+__global__ void __launch_bounds__(256) router_logits_mfma_kernel(const float* __restrict__ wr,
+                                                                 const void* __restrict__ x, int T, int N, int d,
+                                                                 float* __restrict__ logits) {
+  __shared__ f32x4_t part[3][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int t0 = blockIdx.x * 16, e0 = blockIdx.y * 16;
+  const int r = lane & 15, g = lane >> 4;
+  const bool tok_ok = t0 + r < T;
+  const int kq = d / 4;                         // columns per wave (d % 64 == 0)
+  const int kbeg = wave * kq;
+  const float* wrow = wr + static_cast<size_t>(e0 + r) * d + kbeg + 4 * g;
+  const size_t xoff = static_cast<size_t>(tok_ok ? t0 + r : 0) * d + kbeg + 4 * g;
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  float4 w = *reinterpret_cast<const float4*>(wrow);
+  float4 v = tok_ok ? load_x4<XT>(x, xoff) : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int k0 = 0; k0 < kq; k0 += 16) {
+    float4 wn = w, vn = v;
+    if (k0 + 16 < kq) {
+      wn = *reinterpret_cast<const float4*>(wrow + k0 + 16);
+      if (tok_ok) vn = load_x4<XT>(x, xoff + k0 + 16);
+    }
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(v.x, w.x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(v.y, w.y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(v.z, w.z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(v.w, w.w, acc, 0, 0, 0);
+    w = wn;
+    v = vn;
+  }
+  if (wave > 0) part[wave - 1][lane] = acc;
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      const f32x4_t p = part[q][lane];
+      acc[0] += p[0];
+      acc[1] += p[1];
+      acc[2] += p[2];
+      acc[3] += p[3];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int t = t0 + 4 * g + q;
+      if (t < T) logits[static_cast<size_t>(t) * N + e0 + r] = acc[q];
+    }
+  }
+}
+
 // Selection (select.hpp) of the workgroup's four tokens; wave w, lane j < k writes rank j of
 // token blockIdx.x * 4 + w.  The indices can also be published to host-coherent memory as 64-bit
 // (seq << 32 | id) words: the host knows an entry is current from its tag alone, so it needs no
@@ -195,6 +217,16 @@ hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int
                             d, logits);
     return hipGetLastError();
   }
+  if (N % 16 == 0 && d % 64 == 0) {
+    dim3 grid((T + 15) / 16, N / 16), block(256);
+    if (x_dtype == DT_F32)
+      hipExtLaunchKernelGGL(router_logits_mfma_kernel<DT_F32>, grid, block, 0, st, tm.start, tm.stop, 0, wr, x, T, N,
+                            d, logits);
+    else
+      hipExtLaunchKernelGGL(router_logits_mfma_kernel<DT_BF16>, grid, block, 0, st, tm.start, tm.stop, 0, wr, x, T,
+                            N, d, logits);
+    return hipGetLastError();
+  }
   if (d % 32 == 0 && N <= 256) {
     dim3 grid((T + 15) / 16), block(256);
     const bool half = N <= 128;
@@ -215,14 +247,7 @@ hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int
     }
     return hipGetLastError();
   }
-  dim3 grid((N + 3) / 4, (T + 3) / 4), block(256);
-  if (x_dtype == DT_F32)
-    hipExtLaunchKernelGGL(router_logits_kernel<DT_F32>, grid, block, 0, st, tm.start, tm.stop, 0, wr, x, T, N, d,
-                          logits);
-  else
-    hipExtLaunchKernelGGL(router_logits_kernel<DT_BF16>, grid, block, 0, st, tm.start, tm.stop, 0, wr, x, T, N, d,
-                          logits);
-  return hipGetLastError();
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_router_select(const float* logits, int T, int N, int k, int route, int n_groups, int topk_groups,

@@ -39,6 +39,12 @@ def test_prefill_below_grouped_threshold():
     run_case(wl, 5, 1, check_all_outputs=True, expect_grouped=False)
 
 
+def test_prefill_router_rows_not_multiple_of_16():
+    # 24 experts: the token-batch router takes its LDS-tiled FMA kernel instead of the matrix cores
+    wl = WORKLOADS["qwen3-30b-a3b-prefill"].with_(L=2, T=40, d=256, I=128, N=24, k=4)
+    run_case(wl, 7, 1, check_all_outputs=True, expect_grouped=True)
+
+
 def test_prefill_full_size_sampled():
     """The prefill workload at full size (48 layers x 2048 tokens, 57.98 GB of masters, C = 32):
     every routing decision and paging count against the oracle; outputs of 24 sampled tokens at
