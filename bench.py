@@ -163,23 +163,27 @@ def prefill_leg(wisp, torch, link, passes=3):
             rtimes.append(time.perf_counter() - t1)
         run.ctx.set_profiling(0)
         kern = {}
-        gflops, gms = 0, 0.0
+        gflops, gbytes, gms = 0, 0, 0.0
         for kc in (wisp.K_GROUPED_GATEUP, wisp.K_GROUPED_DOWN, wisp.K_PERMUTE, wisp.K_ROUTER_LOGITS,
                    wisp.K_ROUTER_SELECT, wisp.K_COMBINE):
             t = run.ctx.kernel_times(kc)
             if not t["launches"]:
                 continue
             e = dict(launches=t["launches"], avg_us=t["total_ms"] * 1e3 / t["launches"], total_ms=t["total_ms"])
+            if t["bytes"]:
+                e["GBps"] = t["bytes"] / (t["total_ms"] * 1e-3) / 1e9
             if t["flops"]:
                 e["TFLOPs"] = t["flops"] / (t["total_ms"] * 1e-3) / 1e12
                 gflops += t["flops"]
+                gbytes += t["bytes"]
                 gms += t["total_ms"]
             kern[wisp.KERNEL_CLASS_NAMES[kc]] = e
         achieved = gflops / (gms * 1e-3) / 1e12 if gms > 0 else None
         rtimes.sort()
         rel = rtimes[len(rtimes) // 2]
         log(f"prefill: resident pass {rel * 1e3:.2f} ms -> {wl.T / rel:.0f} tokens/s; grouped GEMMs "
-            f"{achieved:.0f} TFLOP/s ({achieved / MFMA_BF16_PEAK_TFLOPS:.3f} of the bf16 peak)")
+            f"{achieved:.0f} TFLOP/s ({achieved / MFMA_BF16_PEAK_TFLOPS:.3f} of the bf16 peak), "
+            f"{gbytes / (gms * 1e-3) / 1e9:.0f} GB/s ({gbytes / (gms * 1e-3) / 1e9 / HBM_PEAK_GBPS:.3f} of HBM)")
         return dict(
             workload=wl.description, tokens_per_s=wl.T / el, pass_ms=el * 1e3, passes=len(times),
             pass_ms_all=[t * 1e3 for t in times], cap_per_layer=wl.cap, faults=misses, distinct_experts=distinct,
@@ -188,7 +192,12 @@ def prefill_leg(wisp, torch, link, passes=3):
             resident=dict(tokens_per_s=wl.T / rel, pass_ms=rel * 1e3, kernels=kern),
             mfma=dict(bound="mfma", achieved=achieved, peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
                       frac=achieved / MFMA_BF16_PEAK_TFLOPS if achieved else None,
-                      kernels="grouped gate/up + down (bf16 v_mfma_f32_32x32x16), resident pass"))
+                      kernels="grouped gate/up + down (bf16 v_mfma_f32_32x32x16), resident pass"),
+            # at ~4096 rows per 32-expert launch the grouped GEMMs do ~100 FLOP per weight byte, below
+            # the bf16 ridge (2.5 PFLOP/s / 8 TB/s = 312): HBM is their bound
+            hbm=dict(bound="hbm", achieved=gbytes / (gms * 1e-3) / 1e9 if gms > 0 else None, peak=HBM_PEAK_GBPS,
+                     unit="GB/s", frac=gbytes / (gms * 1e-3) / 1e9 / HBM_PEAK_GBPS if gms > 0 else None,
+                     kernels="grouped gate/up + down, algorithmic bytes (weights once, rows in and out)"))
     finally:
         run.close()
 
