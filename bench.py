@@ -17,6 +17,9 @@ Reported beside the throughput:
                  fault bytes / measured host-link bandwidth (exact fault counts of the run);
   cpu_baseline   the fp64 CPU oracle (fully resident layer) on a bounded sample of the same
                  workload, on this host's cores;
+  sweep          at per-layer caps 8..128, the pager against static layer-level offload (whole layers
+                 resident, the rest copied in bulk each step) and zero-copy offload (the routed experts
+                 of non-resident layers read over the link each step) at the same VRAM expert budget;
   prefill        the Qwen3-30B-A3B-shaped prefill chunk (2048 tokens per layer, same weights and
                  cap): tokens/s of a cold pass against T_roof = fault bytes / link + max(HBM bytes /
                  8 TB/s, FLOPs / 2.5 PFLOP/s), and the matrix-core rate of the grouped GEMMs in a
@@ -109,6 +112,56 @@ def cpu_baseline(run, wl, start_step, max_tokens=24, budget_s=15.0):
     return dict(value=tokens / dt, unit="tokens/s", cores=threads, kind="oracle",
                 sample=f"{tokens // wl.T} decode step(s) x {wl.L} layers x batch {wl.T} "
                        f"(fully resident fp64 layer, weights read from the same pinned host masters), {dt:.1f} s")
+
+
+SWEEP_CAPS = (8, 16, 32, 64, 128)
+
+
+def sweep_leg(run, wl, wisp, torch, warmup=16, steps=96, offload_steps=3):
+    """Iso-VRAM sweep over the expert budget (the analogue of the paper's Fig. 3 and Table 1): at each
+    per-layer cap C the budget is C * L * M_e bytes, spent three ways on the same steps and kernels:
+    the pager (device pager, cold start; preloaded when C = N, where every expert fits), static
+    layer-level offload (whole layers resident, every other layer copied in bulk each step, as the
+    paper describes the baseline), and zero-copy offload (whole layers resident, the routed experts of
+    the other layers read over the host link each step, nothing cached)."""
+    out = []
+
+    def timed(fn, n):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        fn(n)
+        torch.cuda.synchronize()
+        return wl.T * n / (time.perf_counter() - t0)
+
+    for cap in SWEEP_CAPS:
+        if cap > wl.N:
+            continue
+        budget = cap * wl.L * wl.blob
+        run.ctx.set_pager(wisp.PAGER_HOST)
+        run.ctx.masters_ready()
+        assert run.set_cap(cap) == cap
+        if cap == wl.N:
+            run.ctx.preload()
+        run.ctx.set_pager(wisp.PAGER_DEVICE)
+        run.decode(record=False, steps=warmup, start=0, stats=False)
+        paged = timed(lambda n: run.decode(record=False, steps=n, start=warmup, stats=False), steps)
+        run.ctx.set_pager(wisp.PAGER_HOST)
+        arms = {}
+        for mode, name in ((wisp.OFFLOAD_BULK, "static_offload"), (wisp.OFFLOAD_ZERO_COPY, "zero_copy_offload")):
+            r = run.ctx.offload_begin(budget, mode)
+            run.offload(record=False, steps=1, start=0)
+            n = offload_steps if (mode == wisp.OFFLOAD_BULK and r < wl.L) else 4 * offload_steps
+            arms[name] = (timed(lambda n: run.offload(record=False, steps=n, start=1), n), r)
+            run.ctx.offload_end()
+        st, zc = arms["static_offload"], arms["zero_copy_offload"]
+        out.append(dict(cap=cap, budget_GB=budget / 1e9, paged_tokens_per_s=paged, paged_preloaded=cap == wl.N,
+                        static_offload_tokens_per_s=st[0], static_resident_layers=st[1],
+                        zero_copy_offload_tokens_per_s=zc[0], zero_copy_resident_layers=zc[1],
+                        speedup_vs_static=paged / st[0], speedup_vs_zero_copy=paged / zc[0]))
+        log(f"sweep C={cap:3d} ({budget / 1e9:5.1f} GB): paged {paged:7.2f} tokens/s; static offload {st[0]:7.2f} "
+            f"({st[1]} resident layers) -> {paged / st[0]:5.1f}x; zero-copy offload {zc[0]:7.2f} ({zc[1]}) -> "
+            f"{paged / zc[0]:4.1f}x")
+    return out
 
 
 def prefill_leg(wisp, torch, link, passes=3):
@@ -215,6 +268,7 @@ def main():
     ap.add_argument("--pager", choices=["both", "device", "host"], default="both",
                     help="which pager(s) to time; value is the device pager's when it runs")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill leg")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the iso-VRAM budget sweep against static offload")
     ap.add_argument("--census-steps", type=int, default=24,
                     help="extra decode steps after the timed region with every kernel class timed (0 = skip)")
     args = ap.parse_args()
@@ -335,6 +389,9 @@ def main():
     elapsed = steps / tok_s * wl.T
     path = passes[main_pass]["path_roofline"]
 
+    sweep = None
+    if not args.no_sweep and wl.name == BENCH_WORKLOAD:
+        sweep = sweep_leg(run, wl, wisp, torch)
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
@@ -368,6 +425,7 @@ def main():
         "passes": passes,
         "kernel_timing": args.kernel_timing,
         "prefill": prefill,
+        "sweep": sweep,
     }
     print(json.dumps(result), flush=True)
 

@@ -170,6 +170,26 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
 wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_t* idx_dev, float* w_dev,
                              float* y_dev, void* stream, wisp_page_stats* st);
 
+/* Static offload at a VRAM expert budget: the comparison arm of the paper's iso-VRAM evaluation
+ * (Sec. 1 and Sec. 5.2: static layer-level offload keeps most weights on the host and moves them over
+ * the link when the layer runs, routing-blind).  Layers 0 .. R-1 keep all N experts resident; the
+ * others are served from the masters every step, by mode:
+ *  WISP_OFFLOAD_BULK: the N experts of each other layer are copied in one bulk copy into one of two
+ *    layer-sized staging buffers on the side stream, the next layer's copy overlapping the current
+ *    layer's compute; R = floor((expert_bytes - 2 N M_e) / (N M_e)); needs two layers' worth of bytes.
+ *  WISP_OFFLOAD_ZERO_COPY: no staging; the expert kernels read the routed experts of the other
+ *    layers straight from the pinned masters (zero-copy over the host link, nothing cached);
+ *    R = floor(expert_bytes / (N M_e)); needs pinned masters.
+ * R = L when every layer fits.  wisp_offload_step takes the arguments of wisp_decode_step and runs the
+ * same router, expert and combine kernels as the pager, so outputs equal those of the paged and fully
+ * resident runs bit for bit.  wisp_offload_end waits for outstanding copies and frees the buffers.
+ * The pager's own slots are left as they are (unused meanwhile).  Host pager only. */
+typedef enum { WISP_OFFLOAD_BULK = 0, WISP_OFFLOAD_ZERO_COPY = 1 } wisp_offload_mode;
+wisp_status wisp_offload_begin(wisp_ctx* ctx, uint64_t expert_bytes, int32_t mode, int32_t* resident_layers_out);
+wisp_status wisp_offload_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_t* idx_dev, float* w_dev,
+                              float* y_dev, void* stream);
+wisp_status wisp_offload_end(wisp_ctx* ctx);
+
 /* Cumulative counts of `layer` since creation or the last wisp_reset_stats. */
 wisp_status wisp_get_stats(wisp_ctx* ctx, int32_t layer, wisp_page_stats* cumulative);
 wisp_status wisp_reset_stats(wisp_ctx* ctx);

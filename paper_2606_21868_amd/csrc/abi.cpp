@@ -109,6 +109,19 @@ struct wisp_ctx {
   bool ids_ev_recorded = false;
   std::vector<int32_t> e_cnt, e_off; // pairs per expert and their first sorted row
   std::vector<int32_t> pair_order;   // pairs sorted by expert (host copy, for the per-item path)
+  // routing-blind static offload (comparison arm)
+  struct Offload {
+    bool on = false;
+    int32_t mode = 0;                  // wisp_offload_mode
+    int32_t resident_layers = 0;       // layers 0 .. R-1 hold all N experts in HBM
+    uint8_t* resident = nullptr;       // [R][N] blobs at master_stride
+    uint8_t* staging[2] = {nullptr, nullptr};
+    hipEvent_t filled[2] = {nullptr, nullptr};
+    hipEvent_t used[2] = {nullptr, nullptr};
+    bool used_rec[2] = {false, false};
+    int32_t next_copy = 0;             // streamed-layer sequence number of the next copy to issue
+    int32_t next_use = 0;              // sequence number of the next streamed layer to compute
+  } off;
   int32_t fail_alloc_at = 0;
   int32_t alloc_counter = 0;
   // device pager (WISP_PAGER_DEVICE): the slot tables in HBM are authoritative while it is on
@@ -226,8 +239,22 @@ wisp_status check_layer(wisp_ctx* c, int32_t l) {
   return WISP_OK;
 }
 
+void free_offload(wisp_ctx* c) {
+  auto& o = c->off;
+  if (c->side) hipStreamSynchronize(c->side);
+  for (int b = 0; b < 2; ++b) {
+    if (o.used_rec[b]) hipEventSynchronize(o.used[b]);
+    if (o.staging[b]) hipFree(o.staging[b]);
+    if (o.filled[b]) hipEventDestroy(o.filled[b]);
+    if (o.used[b]) hipEventDestroy(o.used[b]);
+  }
+  if (o.resident) hipFree(o.resident);
+  o = wisp_ctx::Offload{};
+}
+
 void free_ctx(wisp_ctx* c) {
   if (!c) return;
+  free_offload(c);
   if (c->side) hipStreamSynchronize(c->side);
   for (auto& L : c->layers) {
     if (L.use_ev_recorded) hipEventSynchronize(L.use_ev);
@@ -1077,6 +1104,159 @@ wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_
     if ((s = wisp_page_in(ctx, l, ctx->ids_scratch.data(), T, st ? st + l : nullptr)) != WISP_OK) return s;
     if ((s = wisp_moe_forward(ctx, l, xl, T, wl, yl, stream, nullptr)) != WISP_OK) return s;
   }
+  return WISP_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// Routing-blind static offload at a VRAM expert budget (the comparison arm of Sec. 5.2)
+// ------------------------------------------------------------------------------------------
+namespace {
+
+// Streamed layers are R .. L-1, visited in order every step; sequence number q (counting across
+// steps) is layer R + q % S and uses staging buffer q % 2.
+wisp_status offload_issue_copy(wisp_ctx* c) {
+  auto& o = c->off;
+  const int32_t L = c->desc.n_layers, S = L - o.resident_layers;
+  const int32_t q = o.next_copy++;
+  const int b = q & 1;
+  const int32_t layer = o.resident_layers + q % S;
+  if (o.used_rec[b]) WISP_HIP(hipStreamWaitEvent(c->side, o.used[b], 0), "hipStreamWaitEvent(staging use)");
+  wisp_status s = master_h2d(c, o.staging[b], c->masters[layer], c->master_map_bytes, c->side);
+  if (s != WISP_OK) return s;
+  WISP_HIP(hipEventRecord(o.filled[b], c->side), "hipEventRecord(staging fill)");
+  return WISP_OK;
+}
+
+}  // namespace
+
+wisp_status wisp_offload_begin(wisp_ctx* ctx, uint64_t expert_bytes, int32_t mode, int32_t* resident_layers_out) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (ctx->off.on) return fail(WISP_E_STATE, "static offload already active");
+  if (mode != WISP_OFFLOAD_BULK && mode != WISP_OFFLOAD_ZERO_COPY) return fail(WISP_E_INVAL, "unknown offload mode");
+  if (mode == WISP_OFFLOAD_ZERO_COPY && ctx->pageable)
+    return fail(WISP_E_INVAL, "zero-copy offload reads pinned masters; these are pageable");
+  if (ctx->pager == WISP_PAGER_DEVICE) return fail(WISP_E_STATE, "switch to the host pager first");
+  for (auto& L : ctx->layers) {
+    if (L.pending) return fail(WISP_E_STATE, "a page-in is pending");
+    if (!L.wr) return fail(WISP_E_STATE, "router weights not set for every layer");
+  }
+  const uint64_t layer_bytes = static_cast<uint64_t>(ctx->master_map_bytes);
+  const int32_t L = ctx->desc.n_layers;
+  int32_t R = 0, staging = 0;
+  if (expert_bytes >= layer_bytes * static_cast<uint64_t>(L)) {
+    R = L;                                              // everything fits: no streaming
+  } else if (mode == WISP_OFFLOAD_ZERO_COPY) {
+    R = static_cast<int32_t>(expert_bytes / layer_bytes);   // no staging: the kernels read host memory
+  } else if (expert_bytes >= 2 * layer_bytes) {
+    R = static_cast<int32_t>((expert_bytes - 2 * layer_bytes) / layer_bytes);
+    staging = 2;
+  } else {
+    return fail(WISP_E_INVAL, "static offload needs a budget of at least two layers of experts");
+  }
+  if ((s = drain(ctx)) != WISP_OK) return s;
+  auto& o = ctx->off;
+  auto bail = [&](wisp_status st, const char* m) {
+    free_offload(ctx);
+    return fail(st, m);
+  };
+  if (R > 0 && hipMalloc(&o.resident, layer_bytes * R) != hipSuccess) {
+    (void)hipGetLastError();
+    return bail(WISP_E_NOMEM, "hipMalloc of the resident layers failed");
+  }
+  for (int b = 0; b < staging; ++b) {
+    void* p = nullptr;
+    if (hipMalloc(&p, layer_bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      return bail(WISP_E_NOMEM, "hipMalloc of a staging buffer failed");
+    }
+    o.staging[b] = static_cast<uint8_t*>(p);
+    if (hipEventCreateWithFlags(&o.filled[b], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&o.used[b], hipEventDisableTiming) != hipSuccess)
+      return bail(WISP_E_HIP, "hipEventCreate failed");
+  }
+  o.resident_layers = R;
+  o.mode = mode;
+  for (int32_t l = 0; l < R; ++l)
+    if ((s = master_h2d(ctx, o.resident + layer_bytes * l, ctx->masters[l], layer_bytes, ctx->side)) != WISP_OK)
+      return bail(s, "copying a resident layer failed");
+  o.on = true;
+  // two copies in flight from the start (with one streamed layer both are that layer)
+  for (int i = 0; i < 2 && R < L && mode == WISP_OFFLOAD_BULK; ++i)
+    if ((s = offload_issue_copy(ctx)) != WISP_OK) return s;
+  WISP_HIP(hipStreamSynchronize(ctx->side), "hipStreamSynchronize(side)");
+  if (resident_layers_out) *resident_layers_out = R;
+  return WISP_OK;
+}
+
+wisp_status wisp_offload_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_t* idx_dev, float* w_dev,
+                              float* y_dev, void* stream) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  auto& o = ctx->off;
+  if (!o.on) return fail(WISP_E_STATE, "static offload not active");
+  if (!x_dev || !idx_dev || !w_dev || !y_dev) return fail(WISP_E_INVAL, "NULL device pointer");
+  if (T < 1 || T > ctx->desc.max_tokens) return fail(WISP_E_INVAL, "T out of [1, max_tokens]");
+  const auto& d = ctx->desc;
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  const size_t xs = static_cast<size_t>(T) * d.d_model * ctx->x_elem();
+  const int k = d.top_k, rows = k + 1;
+  const int32_t S = d.n_layers - o.resident_layers;
+  for (int32_t l = 0; l < d.n_layers; ++l) {
+    const void* xl = static_cast<const uint8_t*>(x_dev) + l * xs;
+    int32_t* il = idx_dev + static_cast<size_t>(l) * T * k;
+    float* wl = w_dev + static_cast<size_t>(l) * T * k;
+    float* yl = y_dev + static_cast<size_t>(l) * T * d.d_model;
+    int32_t* ids = ctx->ids_scratch.data();
+    if ((s = wisp_route_topk(ctx, l, xl, T, il, wl, ids, stream)) != WISP_OK) return s;
+    const uint8_t* base;
+    int b = -1;
+    if (l < o.resident_layers) {
+      base = o.resident + ctx->master_map_bytes * static_cast<size_t>(l);
+    } else if (o.mode == WISP_OFFLOAD_ZERO_COPY) {
+      base = ctx->masters[l];          // the expert kernels read the routed experts over the host link
+    } else {
+      const int32_t q = o.next_use++;
+      b = q & 1;
+      if (o.resident_layers + q % S != l) return fail(WISP_E_STATE, "static offload out of step");
+      base = o.staging[b];
+      WISP_HIP(hipStreamWaitEvent(sm, o.filled[b], 0), "hipStreamWaitEvent(staging fill)");
+    }
+    // the routed experts of the layer, ascending, each with its (token, rank) pairs
+    std::vector<Work> work;
+    for (int e = 0; e < d.n_experts; ++e) {
+      Work wk;
+      for (int32_t t = 0; t < T; ++t)
+        for (int j = 0; j < k; ++j)
+          if (ids[t * k + j] == e) wk.pairs.push_back({t, t * rows + j});
+      if (wk.pairs.empty()) continue;
+      wk.w = base + static_cast<size_t>(e) * ctx->master_stride;
+      work.push_back(std::move(wk));
+    }
+    if (d.has_shared) {
+      Work wk;
+      wk.w = ctx->layers[l].shared_dev;
+      for (int32_t t = 0; t < T; ++t) wk.pairs.push_back({t, t * rows + k});
+      work.push_back(std::move(wk));
+    }
+    if ((s = run_ffn(ctx, work, xl, sm)) != WISP_OK) return s;
+    LaunchTiming tc = timing_begin(ctx, WISP_K_COMBINE);
+    WISP_HIP(launch_combine(T, k, d.d_model, d.has_shared, wl, ctx->buf, yl, sm, tc), "combine launch");
+    timing_end(ctx, tc, WISP_K_COMBINE, 0);
+    if (b >= 0) {
+      WISP_HIP(hipEventRecord(o.used[b], sm), "hipEventRecord(staging use)");
+      o.used_rec[b] = true;
+      if ((s = offload_issue_copy(ctx)) != WISP_OK) return s;   // two streamed layers ahead, same buffer
+    }
+  }
+  return WISP_OK;
+}
+
+wisp_status wisp_offload_end(wisp_ctx* ctx) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (!ctx->off.on) return fail(WISP_E_STATE, "static offload not active");
+  free_offload(ctx);
   return WISP_OK;
 }
 

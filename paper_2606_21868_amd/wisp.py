@@ -23,6 +23,7 @@ OK, E_INVAL, E_NOMEM, E_HIP, E_NOT_RESIDENT, E_STATE = 0, -1, -2, -3, -4, -5
 STATUS_NAMES = {0: "OK", -1: "E_INVAL", -2: "E_NOMEM", -3: "E_HIP", -4: "E_NOT_RESIDENT", -5: "E_STATE"}
 F32, BF16, FP8 = 0, 1, 2
 PAGER_HOST, PAGER_DEVICE = 0, 1
+OFFLOAD_BULK, OFFLOAD_ZERO_COPY = 0, 1
 (K_ROUTER_LOGITS, K_ROUTER_SELECT, K_FFN_GATEUP, K_FFN_DOWN, K_COMBINE, K_H2D_FILL, K_GROUPED_GATEUP,
  K_GROUPED_DOWN, K_PERMUTE) = range(9)
 KERNEL_CLASS_NAMES = ["router_logits", "router_select", "ffn_gateup", "ffn_down", "combine", "h2d_fill",
@@ -70,6 +71,9 @@ _SIGS = {
     "wisp_page_in": [_P, _I, _P, _I, ctypes.POINTER(PageStats)],
     "wisp_moe_forward": [_P, _I, _P, _I, _P, _P, _P, ctypes.POINTER(PageStats)],
     "wisp_decode_step": [_P, _P, _I, _P, _P, _P, _P, _P],
+    "wisp_offload_begin": [_P, _U64, _I, ctypes.POINTER(_I)],
+    "wisp_offload_step": [_P, _P, _I, _P, _P, _P, _P],
+    "wisp_offload_end": [_P],
     "wisp_get_stats": [_P, _I, ctypes.POINTER(PageStats)],
     "wisp_reset_stats": [_P],
     "wisp_get_cap": [_P, ctypes.POINTER(_I)],
@@ -215,6 +219,20 @@ class Context:
     def decode_step(self, x, T, idx, w, y, stream=None, stats=None):
         check(lib().wisp_decode_step(self.h, _ptr(x), T, _ptr(idx), _ptr(w), _ptr(y), _stream(stream), _ptr(stats)),
               "wisp_decode_step")
+
+    def offload_begin(self, expert_bytes, mode=0):
+        """Static offload at this VRAM expert budget (mode OFFLOAD_BULK or OFFLOAD_ZERO_COPY); returns
+        the number of resident layers."""
+        r = _I()
+        check(lib().wisp_offload_begin(self.h, int(expert_bytes), int(mode), ctypes.byref(r)), "wisp_offload_begin")
+        return r.value
+
+    def offload_step(self, x, T, idx, w, y, stream=None):
+        check(lib().wisp_offload_step(self.h, _ptr(x), T, _ptr(idx), _ptr(w), _ptr(y), _stream(stream)),
+              "wisp_offload_step")
+
+    def offload_end(self):
+        check(lib().wisp_offload_end(self.h), "wisp_offload_end")
 
     def stats(self, layer):
         st = PageStats()
@@ -432,6 +450,28 @@ class DecodeRun:
                         chunks[s, l] = st[l].chunks
         self.stream.synchronize()
         out = dict(hits=hits, misses=misses, chunks=chunks)
+        if record:
+            out.update(idx=idx.cpu().numpy(), w=w.cpu().numpy(), y=y.cpu().numpy())
+        return out
+
+    def offload(self, record=True, steps=None, start=0):
+        """Run decode steps [start, start + steps) through the static-offload arm (wisp_offload_begin
+        must have been called).  Returns idx, w, y as decode() does (if record)."""
+        torch = self.torch
+        wl = self.wl
+        S = steps if steps is not None else self.steps - start
+        T, L, k, d = wl.T, wl.L, wl.k, wl.d
+        nrec = S if record else 1
+        idx = torch.zeros((nrec, L, T, k), dtype=torch.int32, device=self.dev)
+        w = torch.zeros((nrec, L, T, k), dtype=torch.float32, device=self.dev)
+        y = torch.zeros((nrec, L, T, d), dtype=torch.float32, device=self.dev)
+        torch.cuda.synchronize(self.dev)
+        with torch.cuda.stream(self.stream):
+            for s in range(S):
+                r = s if record else 0
+                self.ctx.offload_step(self.x_dev[start + s], T, idx[r], w[r], y[r], self.stream)
+        self.stream.synchronize()
+        out = {}
         if record:
             out.update(idx=idx.cpu().numpy(), w=w.cpu().numpy(), y=y.cpu().numpy())
         return out
