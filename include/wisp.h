@@ -190,6 +190,9 @@ wisp_status wisp_offload_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32
                               float* y_dev, void* stream);
 wisp_status wisp_offload_end(wisp_ctx* ctx);
 
+/* The description the context was created with. */
+wisp_status wisp_get_desc(wisp_ctx* ctx, wisp_model_desc* desc);
+
 /* Cumulative counts of `layer` since creation or the last wisp_reset_stats. */
 wisp_status wisp_get_stats(wisp_ctx* ctx, int32_t layer, wisp_page_stats* cumulative);
 wisp_status wisp_reset_stats(wisp_ctx* ctx);

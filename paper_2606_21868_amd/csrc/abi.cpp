@@ -19,6 +19,7 @@
 
 #include "kernels.hpp"
 #include "slot_table.hpp"
+#include "errors.hpp"
 #include "staging.hpp"
 #include "wisp.h"
 
@@ -34,6 +35,12 @@ wisp_status fail(wisp_status s, const std::string& msg) {
   g_err = msg;
   return s;
 }
+
+}  // namespace
+
+wisp_status wisp::set_error(wisp_status s, const std::string& msg) { return fail(s, msg); }
+
+namespace {
 
 #define WISP_HIP(expr, what)                                                               \
   do {                                                                                     \
@@ -1257,6 +1264,12 @@ wisp_status wisp_offload_end(wisp_ctx* ctx) {
   if (s != WISP_OK) return s;
   if (!ctx->off.on) return fail(WISP_E_STATE, "static offload not active");
   free_offload(ctx);
+  return WISP_OK;
+}
+
+wisp_status wisp_get_desc(wisp_ctx* ctx, wisp_model_desc* desc) {
+  if (!ctx || !desc) return fail(WISP_E_INVAL, "NULL argument");
+  *desc = ctx->desc;
   return WISP_OK;
 }
 

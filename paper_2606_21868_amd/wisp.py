@@ -51,6 +51,23 @@ class PageStats(ctypes.Structure):
                     h2d_bytes=self.h2d_bytes)
 
 
+class MvwsaProblem(ctypes.Structure):
+    _fields_ = [("budget_bytes", ctypes.c_uint64), ("expert_set_bytes", ctypes.c_uint64),
+                ("kv_block_bytes", ctypes.c_uint64), ("kv_min_blocks", ctypes.c_int64), ("c_exp", ctypes.c_double),
+                ("c_kv", ctypes.c_double), ("n_experts", ctypes.c_int32), ("kv_curve_len", ctypes.c_int64)]
+
+
+class MvwsaSplit(ctypes.Structure):
+    _fields_ = [("cap", ctypes.c_int32), ("kv_blocks", ctypes.c_int64), ("kv_bytes", ctypes.c_uint64),
+                ("f", ctypes.c_double), ("latency", ctypes.c_double), ("floor_binding", ctypes.c_int32)]
+
+
+class ResizeLaw(ctypes.Structure):
+    _fields_ = [("budget_bytes", ctypes.c_uint64), ("expert_set_bytes", ctypes.c_uint64),
+                ("kv_block_bytes", ctypes.c_uint64), ("kv_min_blocks", ctypes.c_int64), ("headroom", ctypes.c_double),
+                ("cap_min", ctypes.c_int32), ("cap_max", ctypes.c_int32), ("dead_zone", ctypes.c_int32)]
+
+
 _lib = None
 _P = ctypes.c_void_p
 _I = ctypes.c_int32
@@ -74,6 +91,16 @@ _SIGS = {
     "wisp_offload_begin": [_P, _U64, _I, ctypes.POINTER(_I)],
     "wisp_offload_step": [_P, _P, _I, _P, _P, _P, _P],
     "wisp_offload_end": [_P],
+    "wisp_get_desc": [_P, ctypes.POINTER(ModelDesc)],
+    "wisp_miss_curve": [_P, _I, _I, _I, _P],
+    "wisp_mvwsa_configure": [ctypes.POINTER(MvwsaProblem), _P, _P, ctypes.POINTER(MvwsaSplit)],
+    "wisp_resize_target": [ctypes.POINTER(ResizeLaw), ctypes.c_int64, _I, ctypes.POINTER(_I),
+                           ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(_I)],
+    "wisp_kv_pool_create": [ctypes.c_uint64, ctypes.c_int64, ctypes.POINTER(_P)],
+    "wisp_kv_pool_blocks": [_P, ctypes.POINTER(ctypes.c_int64)],
+    "wisp_kv_pool_resize": [_P, ctypes.c_int64],
+    "wisp_kv_pool_destroy": [_P],
+    "wisp_dual_resize": [_P, _P, _I, ctypes.c_int64],
     "wisp_get_stats": [_P, _I, ctypes.POINTER(PageStats)],
     "wisp_reset_stats": [_P],
     "wisp_get_cap": [_P, ctypes.POINTER(_I)],
@@ -341,6 +368,69 @@ class SlotTable:
     @property
     def cap(self):
         return lib().wisp_slot_table_cap(self.h)
+
+
+# ------------------------------------------------------------------------------------------------
+# Expert <-> KV allocator (wisp_mvwsa.h)
+# ------------------------------------------------------------------------------------------------
+def miss_curve(ids, n_experts):
+    """Expert miss curve m(C), C = 0..n_experts, of one layer's routing trace ids [steps, refs]."""
+    ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int32))
+    if ids.ndim == 1:
+        ids = ids[:, None]
+    out = np.zeros(n_experts + 1, np.uint64)
+    check(lib().wisp_miss_curve(ids.ctypes.data, ids.shape[0], ids.shape[1], n_experts, out.ctypes.data),
+          "wisp_miss_curve")
+    return out
+
+
+def mvwsa_configure(B, a, b, kv_min, c_exp, c_kv, m_exp, m_kv):
+    """MV-WSA startup configurator (Eqs. 3-5); returns dict(cap, kv_blocks, kv_bytes, f, latency, floor_binding)."""
+    m_exp = np.ascontiguousarray(np.asarray(m_exp, dtype=np.uint64))
+    m_kv = np.ascontiguousarray(np.asarray(m_kv, dtype=np.float64))
+    pr = MvwsaProblem(int(B), int(a), int(b), int(kv_min), float(c_exp), float(c_kv), m_exp.size - 1, m_kv.size)
+    out = MvwsaSplit()
+    check(lib().wisp_mvwsa_configure(ctypes.byref(pr), m_exp.ctypes.data, m_kv.ctypes.data, ctypes.byref(out)),
+          "wisp_mvwsa_configure")
+    return dict(cap=out.cap, kv_blocks=out.kv_blocks, kv_bytes=out.kv_bytes, f=out.f, latency=out.latency,
+                floor_binding=bool(out.floor_binding))
+
+
+def resize_target(B, a, b, kv_min, headroom, cap_min, cap_max, dead_zone, peak_blocks, cap_now):
+    """Dual-resize control law (App. B, Eqs. 6-8); returns (cap, kv_blocks, move)."""
+    law = ResizeLaw(int(B), int(a), int(b), int(kv_min), float(headroom), int(cap_min), int(cap_max), int(dead_zone))
+    c, k, m = _I(), ctypes.c_int64(), _I()
+    check(lib().wisp_resize_target(ctypes.byref(law), int(peak_blocks), int(cap_now), ctypes.byref(c), ctypes.byref(k),
+                                   ctypes.byref(m)), "wisp_resize_target")
+    return c.value, k.value, bool(m.value)
+
+
+class KvPool:
+    """A KV block pool in device memory (wisp_kv_pool_*); the KV side of the budget."""
+
+    def __init__(self, block_bytes, blocks):
+        self.h = _P()
+        check(lib().wisp_kv_pool_create(int(block_bytes), int(blocks), ctypes.byref(self.h)), "wisp_kv_pool_create")
+        self.block_bytes = int(block_bytes)
+
+    @property
+    def blocks(self):
+        n = ctypes.c_int64()
+        check(lib().wisp_kv_pool_blocks(self.h, ctypes.byref(n)), "wisp_kv_pool_blocks")
+        return n.value
+
+    def resize(self, blocks):
+        check(lib().wisp_kv_pool_resize(self.h, int(blocks)), "wisp_kv_pool_resize")
+
+    def close(self):
+        if self.h:
+            check(lib().wisp_kv_pool_destroy(self.h), "wisp_kv_pool_destroy")
+            self.h = _P()
+
+
+def dual_resize(ctx, pool, cap_new, kv_blocks_new):
+    """The drained-barrier move of App. B between the expert scratch of ctx and the KV pool."""
+    check(lib().wisp_dual_resize(ctx.h, pool.h, int(cap_new), int(kv_blocks_new)), "wisp_dual_resize")
 
 
 # ------------------------------------------------------------------------------------------------
