@@ -20,6 +20,8 @@ Reported beside the throughput:
   sweep          at per-layer caps 8..128, the pager against static layer-level offload (whole layers
                  resident, the rest copied in bulk each step) and zero-copy offload (the routed experts
                  of non-resident layers read over the link each step) at the same VRAM expert budget;
+  controller     the live dual-resize (App. B): a fixed split's idle KV moved to expert slots by the
+                 control law, decode tokens/s before and after;
   prefill        the Qwen3-30B-A3B-shaped prefill chunk (2048 tokens per layer, same weights and
                  cap): tokens/s of a cold pass against T_roof = fault bytes / link + max(HBM bytes /
                  8 TB/s, FLOPs / 2.5 PFLOP/s), and the matrix-core rate of the grouped GEMMs in a
@@ -162,6 +164,59 @@ def sweep_leg(run, wl, wisp, torch, warmup=16, steps=96, offload_steps=3):
             f"({st[1]} resident layers) -> {paged / st[0]:5.1f}x; zero-copy offload {zc[0]:7.2f} ({zc[1]}) -> "
             f"{paged / zc[0]:4.1f}x")
     return out
+
+
+# Qwen3-30B-A3B KV cache: 48 layers x (K, V) x 4 KV heads x 128 x bf16 per token, 16-token blocks
+KV_BLOCK_BYTES = 16 * 48 * 2 * 4 * 128 * 2
+KV_POOL_GIB = 2.79          # the fixed split's KV pool in the paper's live run
+KV_PEAK_FRACTION = 0.44     # its observed peak occupancy
+KV_HEADROOM = 0.2
+
+
+def controller_leg(run, wl, wisp, torch, warmup=16, steps=96):
+    """The live dual-resize of Sec. 3.5 / App. B on the decode workload: a fixed split (cap 32 and a
+    2.79 GiB KV pool of real device memory) serves a burst whose KV peaks at 44 % of the pool; at the
+    drained barrier the control law (Eqs. 6-8) moves the idle KV to expert slots and the move is
+    applied (KV shrunk first, then the scratch grown).  Decode tokens/s are timed before and after on
+    the same steps (the KV cache itself is simulated: its bytes are held, not read)."""
+    a = wl.L * wl.blob
+    b = KV_BLOCK_BYTES
+    kv0 = int(KV_POOL_GIB * (1 << 30)) // b
+    B = wl.cap * a + kv0 * b
+
+    def measure():
+        run.ctx.set_pager(wisp.PAGER_HOST)
+        run.ctx.masters_ready()
+        run.ctx.set_pager(wisp.PAGER_DEVICE)
+        run.decode(record=False, steps=warmup, start=0, stats=False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run.decode(record=False, steps=steps, start=warmup, stats=False)
+        torch.cuda.synchronize()
+        return wl.T * steps / (time.perf_counter() - t0)
+
+    run.ctx.set_pager(wisp.PAGER_HOST)
+    assert run.set_cap(wl.cap) == wl.cap
+    pool = wisp.KvPool(b, kv0)
+    try:
+        fixed = measure()
+        run.ctx.set_pager(wisp.PAGER_HOST)
+        cap, kv, move = wisp.resize_target(B, a, b, 0, KV_HEADROOM, 1, wl.N, 1, int(KV_PEAK_FRACTION * kv0), wl.cap)
+        t0 = time.perf_counter()
+        if move:
+            wisp.dual_resize(run.ctx, pool, cap, kv)
+        move_s = time.perf_counter() - t0
+        dyn = measure()
+        res = dict(budget_GiB=B / (1 << 30), kv_block_bytes=b,
+                   fixed=dict(cap=wl.cap, kv_GiB=kv0 * b / (1 << 30), tokens_per_s=fixed),
+                   dynamic=dict(cap=run.ctx.cap(), kv_GiB=pool.blocks * b / (1 << 30), tokens_per_s=dyn),
+                   move_seconds=move_s, decode_speedup=dyn / fixed)
+        log(f"controller: cap {wl.cap} / KV {kv0 * b / (1 << 30):.2f} GiB -> cap {run.ctx.cap()} / KV "
+            f"{pool.blocks * b / (1 << 30):.2f} GiB (move {move_s * 1e3:.0f} ms); decode {fixed:.2f} -> {dyn:.2f} "
+            f"tokens/s ({dyn / fixed:.3f}x)")
+        return res
+    finally:
+        pool.close()
 
 
 def prefill_leg(wisp, torch, link, passes=3):
@@ -390,8 +445,10 @@ def main():
     path = passes[main_pass]["path_roofline"]
 
     sweep = None
+    controller = None
     if not args.no_sweep and wl.name == BENCH_WORKLOAD:
         sweep = sweep_leg(run, wl, wisp, torch)
+        controller = controller_leg(run, wl, wisp, torch)
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
@@ -426,6 +483,7 @@ def main():
         "kernel_timing": args.kernel_timing,
         "prefill": prefill,
         "sweep": sweep,
+        "controller": controller,
     }
     print(json.dumps(result), flush=True)
 
