@@ -399,6 +399,86 @@ __global__ void __launch_bounds__(256) ffn_down_dev(const FfnBatch* __restrict__
                                          off2, soff2, soff2, reinterpret_cast<uint8_t*>(buf), d, lds);
 }
 
+// Single-token launches with bf16 weights and inputs (every decode launch at batch 1): a lean copy
+// of rows_body for this case.  All weight loads of a row group are issued first and the input slice
+// after them, and each row is the same chain of v_dot2c_f32_bf16
+// over the lane's chunks followed by the same shuffle reduction as rows_body, so a row's result has
+// the same bits whichever of the two kernels computes it.
+struct FfnT1Batch {
+  const uint8_t* w[kMaxItems];
+  int32_t row[kMaxItems];    // input row: the token (gate/up) or the h row (down)
+  int32_t out[kMaxItems];    // output row
+  int32_t n_items;
+};
+
+template <int MODE, int LPR, int NL>
+__global__ void __launch_bounds__(256) ffn_rows_t1(const FfnT1Batch B, const uint8_t* __restrict__ vin, int vin_stride,
+                                                   int K, int R, int rows_per_wg, int blocks_per_item, uint32_t off0,
+                                                   uint32_t off1, uint8_t* __restrict__ out, int out_stride) {
+  constexpr int RPW = 64 / LPR;
+  const int item = blockIdx.x / blocks_per_item;
+  const int rb = blockIdx.x - item * blocks_per_item;
+  const int r_begin = rb * rows_per_wg, r_end = min(R, r_begin + rows_per_wg);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int sub = lane / LPR, sl = lane - sub * LPR;
+  const uint8_t* w = B.w[item];
+  const size_t row_b = static_cast<size_t>(K) * 2;
+  const uint4* xrow = reinterpret_cast<const uint4*>(vin + static_cast<size_t>(B.row[item]) * vin_stride * 2);
+  for (int rbase = r_begin + wave * RPW; rbase < r_end; rbase += 4 * RPW) {
+    const int r = rbase + sub;
+    const bool valid = r < r_end;
+    const int rr = valid ? r : r_begin;
+    const uint4* row0 = reinterpret_cast<const uint4*>(w + off0 + rr * row_b);
+    const uint4* row1 = reinterpret_cast<const uint4*>(w + off1 + rr * row_b);
+    uint4 a[NL], b[NL], xr[NL];
+#pragma unroll
+    for (int m = 0; m < NL; ++m) {
+      a[m] = row0[m * LPR + sl];
+      if constexpr (MODE == MODE_GATEUP) b[m] = row1[m * LPR + sl];
+    }
+#pragma unroll
+    for (int m = 0; m < NL; ++m) xr[m] = xrow[m * LPR + sl];
+    float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll
+    for (int m = 0; m < NL; ++m) {
+      acc0 = dot2_bf16(a[m].x, xr[m].x, acc0);
+      acc0 = dot2_bf16(a[m].y, xr[m].y, acc0);
+      acc0 = dot2_bf16(a[m].z, xr[m].z, acc0);
+      acc0 = dot2_bf16(a[m].w, xr[m].w, acc0);
+      if constexpr (MODE == MODE_GATEUP) {
+        acc1 = dot2_bf16(b[m].x, xr[m].x, acc1);
+        acc1 = dot2_bf16(b[m].y, xr[m].y, acc1);
+        acc1 = dot2_bf16(b[m].z, xr[m].z, acc1);
+        acc1 = dot2_bf16(b[m].w, xr[m].w, acc1);
+      }
+    }
+#pragma unroll
+    for (int off = LPR / 2; off > 0; off >>= 1) {
+      acc0 += __shfl_xor(acc0, off, 64);
+      if constexpr (MODE == MODE_GATEUP) acc1 += __shfl_xor(acc1, off, 64);
+    }
+    if (valid && sl == 0) {
+      const size_t o = static_cast<size_t>(B.out[item]) * out_stride + r;
+      if constexpr (MODE == MODE_GATEUP)
+        reinterpret_cast<uint16_t*>(out)[o] = f32_to_bf16_rne(acc0 / (1.0f + __expf(-acc0)) * acc1);
+      else
+        reinterpret_cast<float*>(out)[o] = acc0;
+    }
+  }
+}
+
+using T1Kernel = void (*)(const FfnT1Batch, const uint8_t*, int, int, int, int, int, uint32_t, uint32_t, uint8_t*, int);
+
+T1Kernel pick_t1(int mode, int lpr, int nl) {
+#define WISP_T1(M, L, N) \
+  if (mode == M && lpr == L && nl == N) return &ffn_rows_t1<M, L, N>;
+  WISP_T1(MODE_GATEUP, 64, 4) WISP_T1(MODE_GATEUP, 64, 8) WISP_T1(MODE_DOWN, 32, 3) WISP_T1(MODE_DOWN, 64, 28)
+  WISP_T1(MODE_DOWN, 32, 1) WISP_T1(MODE_DOWN, 16, 1) WISP_T1(MODE_DOWN, 16, 3) WISP_T1(MODE_GATEUP, 32, 1)
+  WISP_T1(MODE_GATEUP, 16, 3)
+#undef WISP_T1
+  return nullptr;
+}
+
 using RowsKernel = void (*)(const FfnBatch, const uint8_t*, int, int, int, int, int, uint32_t, uint32_t, uint32_t,
                             uint32_t, uint8_t*, int);
 
@@ -480,6 +560,21 @@ hipError_t launch_rows(int mode, const FfnBatch& b, const FfnShape& s, const voi
   }
   const uint32_t off0 = static_cast<uint32_t>(mode == MODE_GATEUP ? L.off_w1 : L.off_w2);
   const uint32_t off1 = static_cast<uint32_t>(mode == MODE_GATEUP ? L.off_w3 : L.off_w2);
+  if (b.max_ntok == 1 && WT == DT_BF16 && IT == DT_BF16) {
+    if (T1Kernel k1 = pick_t1(mode, lpr, nl)) {
+      FfnT1Batch t1;
+      t1.n_items = b.n_items;
+      for (int i = 0; i < b.n_items; ++i) {
+        t1.w[i] = b.items[i].w;
+        t1.row[i] = mode == MODE_GATEUP ? b.items[i].tok[0] : b.items[i].out[0];
+        t1.out[i] = b.items[i].out[0];
+      }
+      dim3 grid(static_cast<unsigned>(b.n_items * bpi)), block(256);
+      hipExtLaunchKernelGGL(k1, grid, block, 0, st, tm.start, tm.stop, 0, t1, static_cast<const uint8_t*>(vin),
+                            vin_stride, K, R, rows_per_wg, bpi, off0, off1, static_cast<uint8_t*>(out), out_stride);
+      return hipGetLastError();
+    }
+  }
   const uint32_t soff0 = static_cast<uint32_t>(mode == MODE_GATEUP ? L.off_s1 : L.off_s2);
   const uint32_t soff1 = static_cast<uint32_t>(mode == MODE_GATEUP ? L.off_s3 : L.off_s2);
   dim3 grid(static_cast<unsigned>(b.n_items * bpi)), block(256);
