@@ -22,6 +22,8 @@ Reported beside the throughput:
                  of non-resident layers read over the link each step) at the same VRAM expert budget;
   controller     the live dual-resize (App. B): a fixed split's idle KV moved to expert slots by the
                  control law, decode tokens/s before and after;
+  prefetch       speculative prefetch (Sec. 4) at caps 8/16/32: off, the online co-activation predictor
+                 (App. E), and perfect hints (each step's true routing), on the host pager;
   prefill        the Qwen3-30B-A3B-shaped prefill chunk (2048 tokens per layer, same weights and
                  cap): tokens/s of a cold pass against T_roof = fault bytes / link + max(HBM bytes /
                  8 TB/s, FLOPs / 2.5 PFLOP/s), and the matrix-core rate of the grouped GEMMs in a
@@ -126,6 +128,7 @@ def sweep_leg(run, wl, wisp, torch, warmup=16, steps=96, offload_steps=3):
     layer-level offload (whole layers resident, every other layer copied in bulk each step, as the
     paper describes the baseline), and zero-copy offload (whole layers resident, the routed experts of
     the other layers read over the host link each step, nothing cached)."""
+    steps = min(steps, run.steps - warmup)
     out = []
 
     def timed(fn, n):
@@ -179,6 +182,7 @@ def controller_leg(run, wl, wisp, torch, warmup=16, steps=96):
     drained barrier the control law (Eqs. 6-8) moves the idle KV to expert slots and the move is
     applied (KV shrunk first, then the scratch grown).  Decode tokens/s are timed before and after on
     the same steps (the KV cache itself is simulated: its bytes are held, not read)."""
+    steps = min(steps, run.steps - warmup)
     a = wl.L * wl.blob
     b = KV_BLOCK_BYTES
     kv0 = int(KV_POOL_GIB * (1 << 30)) // b
@@ -217,6 +221,69 @@ def controller_leg(run, wl, wisp, torch, warmup=16, steps=96):
         return res
     finally:
         pool.close()
+
+
+PREFETCH_CAPS = (8, 16, 32)
+PREFETCH_HORIZON = 4
+PREFETCH_GAMMA = 0.5
+
+
+def prefetch_leg(run, wl, wisp, torch, warmup=16, steps=96):
+    """Speculative prefetch (Sec. 4) on the decode workload, host pager, per-layer caps 8/16/32: no
+    prefetch; the online co-activation predictor of App. E (fresh each arm, top-k of each layer
+    prefetched before it is routed, source layers within PREFETCH_HORIZON, decay PREFETCH_GAMMA); and
+    perfect hints (each step's true routing).  Tokens/s, demand faults and prefetch copies per
+    token, and the predictor's precision (prefetched experts the next step used / copies)."""
+    import numpy as np
+    steps = min(steps, run.steps - warmup)
+    out = []
+    run.ctx.set_pager(wisp.PAGER_HOST)
+    for cap in PREFETCH_CAPS:
+        if cap > wl.N:
+            continue
+        assert run.set_cap(cap) == cap
+        arms = {}
+        trace = None
+        for arm in ("off", "predictor", "perfect"):
+            run.ctx.masters_ready()
+            pred = None
+            if arm == "predictor":
+                pred = wisp.Predictor(wl.L, wl.N, PREFETCH_HORIZON, PREFETCH_GAMMA)
+                run.ctx.set_prefetch(wisp.PREFETCH_PREDICTOR, pred, wl.k)
+            elif arm == "perfect":
+                run.ctx.set_prefetch(wisp.PREFETCH_HINTS)
+            hints = trace.reshape(trace.shape[0], wl.L, -1) if arm == "perfect" else None
+            run.decode(record=False, steps=warmup, start=0, hints=hints[:warmup] if hints is not None else None)
+            run.ctx.reset_stats()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            o = run.decode(record=arm == "off", steps=steps, start=warmup,
+                           hints=hints[warmup:] if hints is not None else None)
+            torch.cuda.synchronize()
+            el = time.perf_counter() - t0
+            st = run.ctx.prefetch_stats()
+            run.ctx.set_prefetch(wisp.PREFETCH_OFF)
+            if pred is not None:
+                pred.close()
+            if arm == "off":
+                full = run.decode(record=True, steps=warmup, start=0)   # the warmup steps' routing
+                trace = np.concatenate([full["idx"], o["idx"]])
+            n_tok = wl.T * steps
+            arms[arm] = dict(tokens_per_s=n_tok / el, demand_faults_per_token=float(o["misses"].sum()) / n_tok,
+                             prefetch_copies_per_token=st["issued"] / n_tok,
+                             precision=st["useful"] / st["issued"] if st["issued"] else None,
+                             link_GB_per_token=(float(o["misses"].sum()) + st["issued"]) * wl.blob / n_tok / 1e9)
+        row = dict(cap=cap, **{a: v for a, v in arms.items()},
+                   predictor_speedup=arms["predictor"]["tokens_per_s"] / arms["off"]["tokens_per_s"],
+                   perfect_speedup=arms["perfect"]["tokens_per_s"] / arms["off"]["tokens_per_s"])
+        out.append(row)
+        pr = arms["predictor"]
+        log(f"prefetch C={cap:3d}: off {arms['off']['tokens_per_s']:6.2f} tokens/s; predictor {pr['tokens_per_s']:6.2f} "
+            f"({row['predictor_speedup']:.2f}x, precision {pr['precision'] or 0:.2f}, "
+            f"{pr['prefetch_copies_per_token']:.1f} copies + {pr['demand_faults_per_token']:.1f} faults per token); "
+            f"perfect hints {arms['perfect']['tokens_per_s']:6.2f} ({row['perfect_speedup']:.2f}x)")
+    assert run.set_cap(wl.cap) == wl.cap
+    return out
 
 
 def prefill_leg(wisp, torch, link, passes=3):
@@ -324,6 +391,7 @@ def main():
                     help="which pager(s) to time; value is the device pager's when it runs")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill leg")
     ap.add_argument("--no-sweep", action="store_true", help="skip the iso-VRAM budget sweep against static offload")
+    ap.add_argument("--no-prefetch", action="store_true", help="skip the speculative-prefetch leg")
     ap.add_argument("--census-steps", type=int, default=24,
                     help="extra decode steps after the timed region with every kernel class timed (0 = skip)")
     args = ap.parse_args()
@@ -449,6 +517,9 @@ def main():
     if not args.no_sweep and wl.name == BENCH_WORKLOAD:
         sweep = sweep_leg(run, wl, wisp, torch)
         controller = controller_leg(run, wl, wisp, torch)
+    prefetch = None
+    if not args.no_prefetch and wl.name == BENCH_WORKLOAD:
+        prefetch = prefetch_leg(run, wl, wisp, torch)
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
@@ -484,6 +555,7 @@ def main():
         "prefill": prefill,
         "sweep": sweep,
         "controller": controller,
+        "prefetch": prefetch,
     }
     print(json.dumps(result), flush=True)
 

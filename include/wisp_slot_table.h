@@ -33,6 +33,14 @@ void wisp_slot_table_destroy(wisp_slot_table* t);
 int32_t wisp_slot_table_step(wisp_slot_table* t, const int32_t* ids, int32_t n, int32_t* hits, int32_t* misses,
                              int32_t* chunks, int32_t* miss_ids, int32_t* miss_slots, int32_t* miss_chunk);
 
+/* Speculative page-in (no step is counted): the distinct ids of ids[0..n), in order and at most C of
+ * them, are made resident.  Each absent one takes a victim among the slots whose occupant is not one
+ * of those ids, ordered (tau asc, slot asc), and gets tau = c (the current clock).  fill_ids /
+ * fill_slots (capacity min(n, C), may be NULL) receive the copies to issue in order.  Returns their
+ * count, or -1 on a bad id (table unchanged). */
+int32_t wisp_slot_table_prefetch(wisp_slot_table* t, const int32_t* ids, int32_t n, int32_t* fill_ids,
+                                 int32_t* fill_slots);
+
 /* Change the cap (1 <= cap <= N); returns 0 or -1 (table unchanged). */
 int32_t wisp_slot_table_resize(wisp_slot_table* t, int32_t cap);
 

@@ -50,6 +50,7 @@ def lib():
         L.oracle_lru_cap.argtypes = [_p]
         L.oracle_lru_step.argtypes = [_p, _p, _i, _p, _p, _p, _p, _p]
         L.oracle_lru_resize.argtypes = [_p, _i]
+        L.oracle_lru_prefetch.argtypes = [_p, _p, _i, _p, _p]
         L.oracle_num_threads.argtypes = []
         _lib = L
     return _lib
@@ -149,6 +150,16 @@ class LRU:
         nm = int(m[0])
         return dict(hits=int(h[0]), misses=nm, chunks=int(c[0]), miss_ids=mi[:nm].copy(),
                     miss_slots=ms[:nm].copy())
+
+    def prefetch(self, ids):
+        """Speculative prefetch; returns (fill_ids, fill_slots) in copy order."""
+        ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int32).ravel())
+        fi = np.zeros(max(ids.size, 1), np.int32)
+        fs = np.zeros(max(ids.size, 1), np.int32)
+        m = lib().oracle_lru_prefetch(self._h, ids.ctypes.data, ids.size, fi.ctypes.data, fs.ctypes.data)
+        if m < 0:
+            raise ValueError("expert id out of range")
+        return fi[:m].copy(), fs[:m].copy()
 
     def slot(self, e):
         return lib().oracle_lru_slot(self._h, e)

@@ -393,6 +393,51 @@ int oracle_lru_step(oracle_lru* s, const int32_t* ids, int n, int32_t* hits, int
 }
 
 /*
+ * Speculative prefetch (Sec. 4; the victim rule is this layer's Algorithm 1 rule, a reading: the
+ * paper states only that speculative copies take slots and may evict experts still needed).
+ * P = the distinct ids of ids[0..n) in the order given, keeping the first C.  Every id of P that is
+ * not resident takes, in P's order, the not-yet-taken slot of smallest (tau, slot) among the slots
+ * whose occupant is not in P (empty slots have tau = 0), evicting that occupant; its tick becomes
+ * the current clock c.  No step is counted and c does not move.  fill_ids / fill_slots get the
+ * copies in order.  Returns their count, or -1 on an id out of range (nothing changed).
+ */
+int oracle_lru_prefetch(oracle_lru* s, const int32_t* ids, int n, int32_t* fill_ids, int32_t* fill_slots) {
+  if (n < 0) return -1;
+  for (int i = 0; i < n; ++i)
+    if (ids[i] < 0 || ids[i] >= s->N) return -1;
+  int* inP = (int*)calloc((size_t)s->N, sizeof(int));
+  int* P = (int*)malloc(sizeof(int) * (size_t)(n ? n : 1));
+  int np_ = 0;
+  for (int i = 0; i < n && np_ < s->C; ++i)
+    if (!inP[ids[i]]) { inP[ids[i]] = 1; P[np_++] = ids[i]; }
+  int* taken = (int*)calloc((size_t)s->C, sizeof(int));
+  int nf = 0;
+  for (int i = 0; i < np_; ++i) {
+    int e = P[i];
+    if (s->pi[e] >= 0) continue;
+    int best = -1;
+    for (int sl = 0; sl < s->C; ++sl) {
+      if (taken[sl]) continue;
+      if (s->pinv[sl] >= 0 && inP[s->pinv[sl]]) continue;
+      if (best < 0 || s->tau[sl] < s->tau[best]) best = sl;
+    }
+    /* |P| <= C: at least as many such slots as absent members of P */
+    taken[best] = 1;
+    if (s->pinv[best] >= 0) s->pi[s->pinv[best]] = -1;
+    s->pi[e] = best;
+    s->pinv[best] = e;
+    s->tau[best] = s->c;
+    if (fill_ids) fill_ids[nf] = e;
+    if (fill_slots) fill_slots[nf] = best;
+    nf++;
+  }
+  free(taken);
+  free(P);
+  free(inP);
+  return nf;
+}
+
+/*
  * Change the cap to newC (1 <= newC <= N).  Shrink: keep the newC resident experts with the
  * largest tau (ties: lower slot first), renumber them 0.. in their old slot order, drop the rest.
  * Grow: keep every slot and append empty ones.  Ticks and the clock are kept.

@@ -22,6 +22,7 @@
 #include "errors.hpp"
 #include "staging.hpp"
 #include "wisp.h"
+#include "wisp_predictor.h"
 
 #include <thread>
 
@@ -72,6 +73,12 @@ struct LayerState {
   StepPlan plan;
   std::vector<std::vector<const uint8_t*>> chunk_ptrs;
   wisp_page_stats cum{};
+  // speculative prefetch (host pager): copies issued since the last forward that waited for them
+  hipEvent_t pf_ev = nullptr;        // the layer's last prefetch copy has landed
+  bool pf_pending = false;
+  std::vector<int32_t> pf_inflight;  // experts whose prefetch copy is ordered before pf_ev
+  std::vector<int32_t> pf_unused;    // prefetched since the last page-in, not yet routed to
+  std::vector<int32_t> pf_req;       // ids requested for this layer by the last decode step
 };
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -142,6 +149,14 @@ struct wisp_ctx {
   FfnBatch* d_plan = nullptr;        // launch plan written by the device pager
   uint32_t* d_stats = nullptr;       // [L][2] hits, misses of the current step
   uint32_t* h_stats = nullptr;       // pinned copy
+  // speculative prefetch inside wisp_decode_step (host pager)
+  int32_t pf_mode = WISP_PREFETCH_OFF;
+  wisp_predictor* pf_pred = nullptr;
+  int32_t pf_depth = 0;
+  std::vector<int32_t> pf_hints;     // [L][pf_hint_n] for the next decode step, -1 = none
+  int32_t pf_hint_n = 0;
+  uint64_t pf_issued = 0, pf_useful = 0;
+  std::vector<uint8_t> pf_mark;      // [N] scratch
 
   uint8_t* master(int l, int e) const { return masters[l] + static_cast<size_t>(e) * master_stride; }
   int k() const { return desc.top_k; }
@@ -271,6 +286,7 @@ void free_ctx(wisp_ctx* c) {
     for (auto* p : L.slot_mem) if (p) hipFree(p);
     if (L.shared_dev) hipFree(L.shared_dev);
     if (L.use_ev) hipEventDestroy(L.use_ev);
+    if (L.pf_ev) hipEventDestroy(L.pf_ev);
     for (auto e : L.fill_ev) hipEventDestroy(e);
     for (auto e : L.chunk_ev) hipEventDestroy(e);
   }
@@ -312,8 +328,11 @@ wisp_status ensure_events(std::vector<hipEvent_t>& v, size_t n) {
 wisp_status drain(wisp_ctx* c) {
   if (c->pager == WISP_PAGER_DEVICE) WISP_HIP(hipDeviceSynchronize(), "hipDeviceSynchronize");
   WISP_HIP(hipStreamSynchronize(c->side), "hipStreamSynchronize(side)");
-  for (auto& L : c->layers)
+  for (auto& L : c->layers) {
     if (L.use_ev_recorded) WISP_HIP(hipEventSynchronize(L.use_ev), "hipEventSynchronize(layer)");
+    L.pf_pending = false;
+    L.pf_inflight.clear();
+  }
   return WISP_OK;
 }
 
@@ -477,6 +496,52 @@ wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, h
   return flush();
 }
 
+// Speculative prefetch of ids[0..n) into `layer`'s slots (host pager).  Validated by the caller.
+wisp_status prefetch_layer(wisp_ctx* c, int32_t layer, const int32_t* ids, int32_t n) {
+  LayerState& L = c->layers[layer];
+  std::vector<std::pair<int32_t, int32_t>> fills;
+  if (!L.table->prefetch(ids, n, &fills)) return fail(WISP_E_INVAL, "expert id out of range");
+  if (fills.empty()) return WISP_OK;
+  if (L.use_ev_recorded) WISP_HIP(hipStreamWaitEvent(c->side, L.use_ev, 0), "hipStreamWaitEvent(use)");
+  LaunchTiming tm = timing_begin(c, WISP_K_H2D_FILL);
+  if (tm.start) WISP_HIP(hipEventRecord(tm.start, c->side), "hipEventRecord");
+  for (const auto& f : fills) {
+    wisp_status s = master_h2d(c, L.slot_mem[f.second], c->master(layer, f.first), c->blob.bytes, c->side);
+    if (s != WISP_OK) return s;
+    L.pf_inflight.push_back(f.first);
+    L.pf_unused.push_back(f.first);
+  }
+  if (tm.stop) WISP_HIP(hipEventRecord(tm.stop, c->side), "hipEventRecord");
+  timing_end(c, tm, WISP_K_H2D_FILL, static_cast<uint64_t>(fills.size()) * c->blob.bytes);
+  WISP_HIP(hipEventRecord(L.pf_ev, c->side), "hipEventRecord(prefetch)");
+  L.pf_pending = true;
+  c->pf_issued += fills.size();
+  return WISP_OK;
+}
+
+// The prefetch wisp_decode_step issues for `layer` before routing it: the predictor's top `depth`
+// from the layers already routed in this pass, or the hints given for this step.
+wisp_status prefetch_before_route(wisp_ctx* c, int32_t layer) {
+  std::vector<int32_t>& ids = c->layers[layer].pf_req;
+  ids.clear();
+  if (c->pf_mode == WISP_PREFETCH_OFF) return WISP_OK;
+  if (c->pf_mode == WISP_PREFETCH_PREDICTOR) {
+    if (layer == 0 || c->pf_depth < 1) return WISP_OK;
+    ids.resize(c->pf_depth);
+    int32_t n = 0;
+    wisp_status s = wisp_predictor_predict(c->pf_pred, layer, c->pf_depth, ids.data(), &n, nullptr);
+    if (s != WISP_OK) return s;
+    ids.resize(n);
+  } else {
+    if (c->pf_hint_n < 1) return WISP_OK;
+    const int32_t* h = &c->pf_hints[static_cast<size_t>(layer) * c->pf_hint_n];
+    for (int32_t i = 0; i < c->pf_hint_n; ++i)
+      if (h[i] >= 0) ids.push_back(h[i]);
+  }
+  if (ids.empty()) return WISP_OK;
+  return prefetch_layer(c, layer, ids.data(), static_cast<int32_t>(ids.size()));
+}
+
 }  // namespace
 
 // ==========================================================================================
@@ -552,7 +617,8 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
       if (hipMalloc(&p, c->blob.bytes) != hipSuccess) return bail(WISP_E_NOMEM, "hipMalloc of a shared expert failed");
       c->layers[l].shared_dev = static_cast<uint8_t*>(p);
     }
-    if (hipEventCreateWithFlags(&c->layers[l].use_ev, hipEventDisableTiming) != hipSuccess)
+    if (hipEventCreateWithFlags(&c->layers[l].use_ev, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&c->layers[l].pf_ev, hipEventDisableTiming) != hipSuccess)
       return bail(WISP_E_HIP, "hipEventCreate failed");
   }
   if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess)
@@ -584,6 +650,7 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
     return bail(WISP_E_HIP, "hipEventCreate failed");
   c->e_cnt.assign(N, 0);
   c->e_off.assign(N + 1, 0);
+  c->pf_mark.assign(N, 0);
   c->pair_order.resize(static_cast<size_t>(T) * k);
   *out = c;
   g_err.clear();
@@ -780,6 +847,7 @@ wisp_status wisp_set_pager(wisp_ctx* ctx, int32_t pager) {
   if (pager == WISP_PAGER_DEVICE) {
     const auto& d = ctx->desc;
     if (ctx->cap < 1) return fail(WISP_E_STATE, "no expert budget set");
+    if (ctx->pf_mode != WISP_PREFETCH_OFF) return fail(WISP_E_STATE, "prefetch runs with the host pager; turn it off");
     if (d.max_tokens > 4) return fail(WISP_E_INVAL, "the device pager handles max_tokens <= 4");
     if (ctx->pageable) return fail(WISP_E_INVAL, "the device pager reads pinned masters; these are pageable");
     if (ctx->cap < d.max_tokens * d.top_k)
@@ -870,6 +938,17 @@ wisp_status wisp_page_in(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, 
   const int32_t n = T * ctx->desc.top_k;
   for (int32_t i = 0; i < n; ++i)
     if (ids_host[i] < 0 || ids_host[i] >= ctx->desc.n_experts) return fail(WISP_E_INVAL, "expert id out of range");
+  if (!L.pf_unused.empty()) {
+    // prefetched experts this page-in routes to while they are still resident
+    std::vector<uint8_t>& mk = ctx->pf_mark;
+    for (int32_t e : L.pf_unused) mk[e] = 1;
+    for (int32_t i = 0; i < n; ++i) {
+      const int32_t e = ids_host[i];
+      if (mk[e] == 1 && L.table->slot_of(e) >= 0) { ++ctx->pf_useful; mk[e] = 2; }
+    }
+    for (int32_t e : L.pf_unused) mk[e] = 0;
+    L.pf_unused.clear();
+  }
   if (!L.table->step(ids_host, n, &L.plan)) return fail(WISP_E_INVAL, "expert id out of range");
   L.ids.assign(ids_host, ids_host + n);
   L.T = T;
@@ -933,6 +1012,16 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
       for (int32_t e : L.plan.chunks[ci].experts) planned[e] = 1;
     for (int e = 0; e < N; ++e)
       if (cnt[e] > 0 && !planned[e]) return fail(WISP_E_NOT_RESIDENT, "routed expert missing from the page-in plan");
+  }
+  if (L.pf_pending) {
+    // a routed expert whose prefetch copy may still be in flight: the FFN waits for the copies
+    bool need = false;
+    for (int32_t e : L.pf_inflight) need = need || cnt[e] > 0;
+    if (need) {
+      WISP_HIP(hipStreamWaitEvent(sm, L.pf_ev, 0), "hipStreamWaitEvent(prefetch)");
+      L.pf_pending = false;
+      L.pf_inflight.clear();
+    }
   }
   const bool grouped = T >= kGroupedMinTokens && grouped_supported(ctx->shape, ctx->desc.has_shared);
   if (grouped) {
@@ -1107,10 +1196,87 @@ wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_
     int32_t* il = idx_dev + static_cast<size_t>(l) * T * d.top_k;
     float* wl = w_dev + static_cast<size_t>(l) * T * d.top_k;
     float* yl = y_dev + static_cast<size_t>(l) * T * d.d_model;
+    if ((s = prefetch_before_route(ctx, l)) != WISP_OK) return s;
     if ((s = wisp_route_topk(ctx, l, xl, T, il, wl, ctx->ids_scratch.data(), stream)) != WISP_OK) return s;
+    if (ctx->pf_mode == WISP_PREFETCH_PREDICTOR &&
+        (s = wisp_predictor_observe(ctx->pf_pred, l, ctx->ids_scratch.data(), T * d.top_k)) != WISP_OK)
+      return s;
     if ((s = wisp_page_in(ctx, l, ctx->ids_scratch.data(), T, st ? st + l : nullptr)) != WISP_OK) return s;
     if ((s = wisp_moe_forward(ctx, l, xl, T, wl, yl, stream, nullptr)) != WISP_OK) return s;
   }
+  if (ctx->pf_mode == WISP_PREFETCH_PREDICTOR && (s = wisp_predictor_end_pass(ctx->pf_pred)) != WISP_OK) return s;
+  if (ctx->pf_mode == WISP_PREFETCH_HINTS) ctx->pf_hint_n = 0;
+  return WISP_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// Speculative prefetch (the experiment of Sec. 4 with the predictor of App. E)
+// ------------------------------------------------------------------------------------------
+wisp_status wisp_prefetch(wisp_ctx* ctx, int32_t layer, const int32_t* ids, int32_t n) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if ((s = check_layer(ctx, layer)) != WISP_OK) return s;
+  if (n < 0 || (n > 0 && !ids)) return fail(WISP_E_INVAL, "bad id list");
+  if (ctx->cap < 1) return fail(WISP_E_STATE, "no expert budget set");
+  if (ctx->pager != WISP_PAGER_HOST) return fail(WISP_E_STATE, "prefetch runs with the host pager");
+  if (ctx->off.on) return fail(WISP_E_STATE, "static offload is active");
+  if (ctx->layers[layer].pending) return fail(WISP_E_STATE, "a page-in of this layer is pending");
+  for (int32_t i = 0; i < n; ++i)
+    if (ids[i] < 0 || ids[i] >= ctx->desc.n_experts) return fail(WISP_E_INVAL, "expert id out of range");
+  return prefetch_layer(ctx, layer, ids, n);
+}
+
+wisp_status wisp_set_prefetch(wisp_ctx* ctx, int32_t mode, wisp_predictor* predictor, int32_t depth) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (mode != WISP_PREFETCH_OFF && mode != WISP_PREFETCH_PREDICTOR && mode != WISP_PREFETCH_HINTS)
+    return fail(WISP_E_INVAL, "unknown prefetch mode");
+  if (mode != WISP_PREFETCH_OFF && ctx->pager != WISP_PAGER_HOST)
+    return fail(WISP_E_STATE, "prefetch runs with the host pager");
+  if (mode == WISP_PREFETCH_PREDICTOR) {
+    if (!predictor) return fail(WISP_E_INVAL, "predictor is NULL");
+    int32_t L = 0, N = 0;
+    if ((s = wisp_predictor_shape(predictor, &L, &N)) != WISP_OK) return s;
+    if (L != ctx->desc.n_layers || N != ctx->desc.n_experts)
+      return fail(WISP_E_INVAL, "predictor shape differs from the model");
+    if (depth < 1 || depth > ctx->desc.n_experts) return fail(WISP_E_INVAL, "depth out of [1, N]");
+  }
+  ctx->pf_mode = mode;
+  ctx->pf_pred = mode == WISP_PREFETCH_PREDICTOR ? predictor : nullptr;
+  ctx->pf_depth = mode == WISP_PREFETCH_PREDICTOR ? depth : 0;
+  ctx->pf_hint_n = 0;
+  return WISP_OK;
+}
+
+wisp_status wisp_set_prefetch_hints(wisp_ctx* ctx, const int32_t* ids, int32_t n) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if (ctx->pf_mode != WISP_PREFETCH_HINTS) return fail(WISP_E_STATE, "prefetch mode is not HINTS");
+  if (n < 0 || n > ctx->desc.n_experts || (n > 0 && !ids)) return fail(WISP_E_INVAL, "bad hint list");
+  const size_t tot = static_cast<size_t>(ctx->desc.n_layers) * n;
+  for (size_t i = 0; i < tot; ++i)
+    if (ids[i] < -1 || ids[i] >= ctx->desc.n_experts) return fail(WISP_E_INVAL, "hint id out of range");
+  ctx->pf_hints.assign(ids, ids + tot);
+  ctx->pf_hint_n = n;
+  return WISP_OK;
+}
+
+wisp_status wisp_prefetch_requests(wisp_ctx* ctx, int32_t layer, int32_t* ids_out, int32_t cap, int32_t* n_out) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if ((s = check_layer(ctx, layer)) != WISP_OK) return s;
+  if (!n_out || cap < 0 || (cap > 0 && !ids_out)) return fail(WISP_E_INVAL, "bad output buffer");
+  const std::vector<int32_t>& r = ctx->layers[layer].pf_req;
+  if (static_cast<size_t>(cap) < r.size()) return fail(WISP_E_INVAL, "output buffer too small");
+  std::copy(r.begin(), r.end(), ids_out);
+  *n_out = static_cast<int32_t>(r.size());
+  return WISP_OK;
+}
+
+wisp_status wisp_prefetch_stats(wisp_ctx* ctx, uint64_t* issued, uint64_t* useful) {
+  if (!ctx || !issued || !useful) return fail(WISP_E_INVAL, "NULL argument");
+  *issued = ctx->pf_issued;
+  *useful = ctx->pf_useful;
   return WISP_OK;
 }
 
@@ -1284,6 +1450,7 @@ wisp_status wisp_get_stats(wisp_ctx* ctx, int32_t layer, wisp_page_stats* cumula
 wisp_status wisp_reset_stats(wisp_ctx* ctx) {
   if (!ctx) return fail(WISP_E_INVAL, "ctx is NULL");
   for (auto& L : ctx->layers) L.cum = wisp_page_stats{};
+  ctx->pf_issued = ctx->pf_useful = 0;
   return WISP_OK;
 }
 

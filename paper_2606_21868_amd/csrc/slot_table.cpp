@@ -105,6 +105,32 @@ bool SlotTable::step(const int32_t* ids, int32_t n, StepPlan* plan) {
   return true;
 }
 
+bool SlotTable::prefetch(const int32_t* ids, int32_t n, std::vector<std::pair<int32_t, int32_t>>* fills) {
+  fills->clear();
+  for (int32_t i = 0; i < n; ++i)
+    if (ids[i] < 0 || ids[i] >= N_) return false;
+  std::vector<int32_t> P;
+  for (int32_t i = 0; i < n && static_cast<int32_t>(P.size()) < C_; ++i)
+    if (!mark_[ids[i]]) { mark_[ids[i]] = 1; P.push_back(ids[i]); }
+  std::vector<int32_t> victims;
+  for (int32_t s = 0; s < C_; ++s)
+    if (pinv_[s] < 0 || !mark_[pinv_[s]]) victims.push_back(s);
+  std::sort(victims.begin(), victims.end(),
+            [&](int32_t a, int32_t b) { return tau_[a] < tau_[b] || (tau_[a] == tau_[b] && a < b); });
+  size_t v = 0;
+  for (int32_t e : P) {
+    mark_[e] = 0;
+    if (pi_[e] >= 0 || v >= victims.size()) continue;
+    const int32_t s = victims[v++];
+    if (pinv_[s] >= 0) pi_[pinv_[s]] = -1;
+    pi_[e] = s;
+    pinv_[s] = e;
+    tau_[s] = clock_;
+    fills->push_back({e, s});
+  }
+  return true;
+}
+
 bool SlotTable::resize(int32_t new_cap, std::vector<int32_t>* old_slot_of_new) {
   if (new_cap < 1 || new_cap > N_) return false;
   std::vector<int32_t> map(new_cap, -1);
@@ -175,6 +201,18 @@ int32_t wisp_slot_table_step(wisp_slot_table* t, const int32_t* ids, int32_t n, 
   if (misses) *misses = t->plan.misses;
   if (chunks) *chunks = static_cast<int32_t>(t->plan.chunks.size());
   return 0;
+}
+
+int32_t wisp_slot_table_prefetch(wisp_slot_table* t, const int32_t* ids, int32_t n, int32_t* fill_ids,
+                                 int32_t* fill_slots) {
+  if (!t || (n > 0 && !ids) || n < 0) return -1;
+  std::vector<std::pair<int32_t, int32_t>> fills;
+  if (!t->t.prefetch(ids, n, &fills)) return -1;
+  for (size_t i = 0; i < fills.size(); ++i) {
+    if (fill_ids) fill_ids[i] = fills[i].first;
+    if (fill_slots) fill_slots[i] = fills[i].second;
+  }
+  return static_cast<int32_t>(fills.size());
 }
 
 int32_t wisp_slot_table_resize(wisp_slot_table* t, int32_t cap) {

@@ -3,6 +3,7 @@
 #pragma once
 
 #include <cstdint>
+#include <utility>
 #include <vector>
 
 namespace wisp {
@@ -38,6 +39,12 @@ class SlotTable {
   // Resize to new_cap.  old_slot_of_new[i] = the old slot whose contents become slot i, or -1 for
   // a new empty slot.  Returns false (table unchanged) on a bad cap.
   bool resize(int32_t new_cap, std::vector<int32_t>* old_slot_of_new);
+
+  // Speculative page-in of ids[0..n) (distinct ids taken in order, at most C): each absent one takes
+  // a victim, the slots whose occupant is not among the ids ordered (tick asc, slot asc), and gets
+  // the current clock as its tick (recent, but no step is counted).  fills receives (expert, slot)
+  // per copy to issue.  Returns false (table unchanged) if an id is out of range.
+  bool prefetch(const int32_t* ids, int32_t n, std::vector<std::pair<int32_t, int32_t>>* fills);
 
   // Drop every resident expert (all slots empty, ticks 0); the clock keeps counting.
   void clear();

@@ -24,6 +24,7 @@ STATUS_NAMES = {0: "OK", -1: "E_INVAL", -2: "E_NOMEM", -3: "E_HIP", -4: "E_NOT_R
 F32, BF16, FP8 = 0, 1, 2
 PAGER_HOST, PAGER_DEVICE = 0, 1
 OFFLOAD_BULK, OFFLOAD_ZERO_COPY = 0, 1
+PREFETCH_OFF, PREFETCH_PREDICTOR, PREFETCH_HINTS = 0, 1, 2
 (K_ROUTER_LOGITS, K_ROUTER_SELECT, K_FFN_GATEUP, K_FFN_DOWN, K_COMBINE, K_H2D_FILL, K_GROUPED_GATEUP,
  K_GROUPED_DOWN, K_PERMUTE) = range(9)
 KERNEL_CLASS_NAMES = ["router_logits", "router_select", "ffn_gateup", "ffn_down", "combine", "h2d_fill",
@@ -73,7 +74,7 @@ _P = ctypes.c_void_p
 _I = ctypes.c_int32
 _U64 = ctypes.c_uint64
 
-# (name, argtypes) for every function of include/wisp.h and include/wisp_slot_table.h
+# (name, argtypes) for every function of include/*.h
 _SIGS = {
     "wisp_expert_bytes": [ctypes.POINTER(ModelDesc), ctypes.POINTER(_U64)],
     "wisp_create": [ctypes.POINTER(ModelDesc), ctypes.POINTER(_P)],
@@ -115,11 +116,23 @@ _SIGS = {
     "wisp_hbm_copy": [_P, _P, _U64, _P],
     "wisp_decode_fp8": [_P, _P, _I, _P],
     "wisp_debug_fail_slot_alloc": [_P, _I],
+    "wisp_predictor_create": [_I, _I, _I, ctypes.c_double, ctypes.POINTER(_P)],
+    "wisp_predictor_destroy": [_P],
+    "wisp_predictor_shape": [_P, ctypes.POINTER(_I), ctypes.POINTER(_I)],
+    "wisp_predictor_observe": [_P, _I, _P, _I],
+    "wisp_predictor_end_pass": [_P],
+    "wisp_predictor_predict": [_P, _I, _I, _P, ctypes.POINTER(_I), _P],
+    "wisp_prefetch": [_P, _I, _P, _I],
+    "wisp_set_prefetch": [_P, _I, _P, _I],
+    "wisp_set_prefetch_hints": [_P, _P, _I],
+    "wisp_prefetch_requests": [_P, _I, _P, _I, ctypes.POINTER(_I)],
+    "wisp_prefetch_stats": [_P, ctypes.POINTER(_U64), ctypes.POINTER(_U64)],
     "wisp_last_error": [],
     "wisp_slot_table_create": [_I, _I],
     "wisp_slot_table_destroy": [_P],
     "wisp_slot_table_step": [_P, _P, _I, _P, _P, _P, _P, _P, _P],
     "wisp_slot_table_resize": [_P, _I],
+    "wisp_slot_table_prefetch": [_P, _P, _I, _P, _P],
     "wisp_slot_table_slot_of": [_P, _I],
     "wisp_slot_table_expert_in": [_P, _I],
     "wisp_slot_table_tick": [_P, _I],
@@ -314,6 +327,72 @@ class Context:
     def debug_fail_slot_alloc(self, n):
         check(lib().wisp_debug_fail_slot_alloc(self.h, n), "wisp_debug_fail_slot_alloc")
 
+    def prefetch(self, layer, ids):
+        ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int32).ravel())
+        check(lib().wisp_prefetch(self.h, layer, ids.ctypes.data if ids.size else None, ids.size), "wisp_prefetch")
+
+    def set_prefetch(self, mode, predictor=None, depth=0):
+        """PREFETCH_OFF, PREFETCH_PREDICTOR (with a Predictor and a depth) or PREFETCH_HINTS."""
+        check(lib().wisp_set_prefetch(self.h, int(mode), predictor.h if predictor is not None else None, int(depth)),
+              "wisp_set_prefetch")
+
+    def set_prefetch_hints(self, ids):
+        """ids [L, n] (-1 = none): the experts prefetched per layer during the next decode step."""
+        ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int32))
+        n = ids.shape[1] if ids.ndim == 2 else 0
+        check(lib().wisp_set_prefetch_hints(self.h, ids.ctypes.data if ids.size else None, n),
+              "wisp_set_prefetch_hints")
+
+    def prefetch_requests(self, layer):
+        """The ids the last decode step asked to prefetch for `layer`."""
+        out = np.zeros(max(self.desc.n_experts, 1), np.int32)
+        n = _I()
+        check(lib().wisp_prefetch_requests(self.h, int(layer), out.ctypes.data, out.size, ctypes.byref(n)),
+              "wisp_prefetch_requests")
+        return out[:n.value].copy()
+
+    def prefetch_stats(self):
+        a, b = _U64(), _U64()
+        check(lib().wisp_prefetch_stats(self.h, ctypes.byref(a), ctypes.byref(b)), "wisp_prefetch_stats")
+        return dict(issued=a.value, useful=b.value)
+
+
+class Predictor:
+    """The co-activation predictor (wisp_predictor_*): host code, no GPU."""
+
+    def __init__(self, n_layers, n_experts, horizon, gamma):
+        self.h = _P()
+        check(lib().wisp_predictor_create(int(n_layers), int(n_experts), int(horizon), float(gamma),
+                                          ctypes.byref(self.h)), "wisp_predictor_create")
+
+    def close(self):
+        if self.h:
+            check(lib().wisp_predictor_destroy(self.h), "wisp_predictor_destroy")
+            self.h = _P()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def observe(self, layer, ids):
+        ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int32).ravel())
+        check(lib().wisp_predictor_observe(self.h, int(layer), ids.ctypes.data if ids.size else None, ids.size),
+              "wisp_predictor_observe")
+
+    def end_pass(self):
+        check(lib().wisp_predictor_end_pass(self.h), "wisp_predictor_end_pass")
+
+    def predict(self, layer, depth):
+        """(ids, scores) of the `depth` best-scoring experts of `layer` (score desc, id asc; positive only)."""
+        ids = np.zeros(max(depth, 1), np.int32)
+        sc = np.zeros(max(depth, 1), np.float64)
+        n = _I()
+        check(lib().wisp_predictor_predict(self.h, int(layer), int(depth), ids.ctypes.data, ctypes.byref(n),
+                                           sc.ctypes.data), "wisp_predictor_predict")
+        return ids[:n.value].copy(), sc[:n.value].copy()
+
 
 def hbm_copy(src, dst, nbytes, stream=None):
     check(lib().wisp_hbm_copy(_ptr(src), _ptr(dst), int(nbytes), _stream(stream)), "wisp_hbm_copy")
@@ -351,6 +430,17 @@ class SlotTable:
         k = m.value
         return dict(hits=h.value, misses=k, chunks=c.value, miss_ids=mi[:k].copy(), miss_slots=ms[:k].copy(),
                     miss_chunk=mc[:k].copy())
+
+    def prefetch(self, ids):
+        """Speculative page-in; returns (fill_ids, fill_slots) in copy order."""
+        ids = np.ascontiguousarray(np.asarray(ids, np.int32).ravel())
+        fi = np.zeros(max(ids.size, 1), np.int32)
+        fs = np.zeros(max(ids.size, 1), np.int32)
+        m = lib().wisp_slot_table_prefetch(self.h, ids.ctypes.data if ids.size else None, ids.size, fi.ctypes.data,
+                                           fs.ctypes.data)
+        if m < 0:
+            raise ValueError("bad expert id")
+        return fi[:m].copy(), fs[:m].copy()
 
     def resize(self, C):
         if lib().wisp_slot_table_resize(self.h, C) != 0:
@@ -510,11 +600,13 @@ class DecodeRun:
     def set_cap(self, cap):
         return self.ctx.set_budget(cap * self.wl.L * self.blob_bytes)
 
-    def decode(self, record=True, steps=None, start=0, stats=True):
+    def decode(self, record=True, steps=None, start=0, stats=True, hints=None, prefetch_log=False):
         """Run decode steps [start, start + steps) through wisp_decode_step.
 
         Returns numpy arrays idx [S, L, T, k], w [S, L, T, k], y [S, L, T, d] (if record), and per
-        (step, layer) hits/misses."""
+        (step, layer) hits/misses.  hints [S, L, n]: prefetch hints set before each step (prefetch
+        mode PREFETCH_HINTS); prefetch_log: also return the ids each step asked to prefetch per layer
+        (``requests[s][l]``)."""
         torch = self.torch
         wl = self.wl
         S = steps if steps is not None else self.steps - start
@@ -527,10 +619,13 @@ class DecodeRun:
         hits = np.zeros((S, L), np.int64)
         misses = np.zeros((S, L), np.int64)
         chunks = np.zeros((S, L), np.int64)
+        requests = []
         torch.cuda.synchronize(self.dev)
         with torch.cuda.stream(self.stream):
             for s in range(S):
                 r = s if record else 0
+                if hints is not None:
+                    self.ctx.set_prefetch_hints(hints[s])
                 self.ctx.decode_step(self.x_dev[start + s], T, idx[r], w[r], y[r], self.stream,
                                      ctypes.addressof(st) if stats else None)
                 if stats:
@@ -538,8 +633,12 @@ class DecodeRun:
                         hits[s, l] = st[l].hits
                         misses[s, l] = st[l].misses
                         chunks[s, l] = st[l].chunks
+                if prefetch_log:
+                    requests.append([self.ctx.prefetch_requests(l) for l in range(L)])
         self.stream.synchronize()
         out = dict(hits=hits, misses=misses, chunks=chunks)
+        if prefetch_log:
+            out["requests"] = requests
         if record:
             out.update(idx=idx.cpu().numpy(), w=w.cpu().numpy(), y=y.cpu().numpy())
         return out

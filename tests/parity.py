@@ -213,3 +213,20 @@ def run_case(wl, cap, steps, sample_points=None, check_all_outputs=False, tokens
         return out
     finally:
         run.close()
+
+
+def check_prediction(ids, scores, exact, depth):
+    """ids/scores from the library against the oracle's exact scores: every score within 1e-12
+    (relative), the order non-increasing with ties in id order, and the set equal to the oracle's
+    top `depth` up to candidates tied with the last kept score."""
+    assert len(ids) == len(scores)
+    for e, s in zip(ids, scores):
+        assert abs(s - float(exact[e])) <= 1e-12 * max(1.0, float(exact[e])), (e, s, exact[e])
+    for a, b in zip(ids[:-1], ids[1:]):
+        assert exact[a] > exact[b] or (exact[a] == exact[b] and a < b) or abs(float(exact[a] - exact[b])) < 1e-12
+    positive = sorted((e for e in range(len(exact)) if exact[e] > 0), key=lambda e: (-exact[e], e))
+    assert len(ids) == min(depth, len(positive))
+    if ids:
+        cut = exact[ids[-1]]
+        above = {e for e in positive if exact[e] > cut and float(exact[e] - cut) >= 1e-12}
+        assert above <= set(ids)
