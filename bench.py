@@ -46,7 +46,8 @@ if ROOT not in sys.path:
 HBM_PEAK_GBPS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0      # dense bf16 matrix-core peak of the MI355X
 PREFILL_WORKLOAD = "qwen3-30b-a3b-prefill"
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "ffn_gateup_qwen3-30b-a3b-decode_hbm_traffic.txt")
+TRAFFIC_SUMMARIES = {k: os.path.join(ROOT, "profiles", f"{k}_qwen3-30b-a3b-decode_hbm_traffic.txt")
+                     for k in ("ffn_gateup",)}
 FFN_SOURCE = os.path.join(ROOT, "paper_2606_21868_amd", "csrc", "expert_ffn.hip")
 
 
@@ -73,15 +74,16 @@ def measure_hbm_copy(torch, wisp, nbytes=1 << 30, reps=5):
     return rates[len(rates) // 2]
 
 
-def measured_traffic(workload):
-    """HBM bytes per gate/up launch from the committed FETCH_SIZE/WRITE_SIZE counter summary (scaled by
-    the copy-kernel calibration it records), or None when there is none for this workload or the kernel
-    source has changed since the counters were taken."""
+def measured_traffic(workload, kname):
+    """HBM bytes per launch of kernel class kname from its committed FETCH_SIZE/WRITE_SIZE counter summary
+    (scaled by the copy-kernel calibration it records), or None when there is none for this workload and
+    kernel or the kernel source has changed since the counters were taken."""
     import hashlib
-    if workload != "qwen3-30b-a3b-decode" or not os.path.exists(TRAFFIC_SUMMARY):
+    summary = TRAFFIC_SUMMARIES.get(kname)
+    if workload != "qwen3-30b-a3b-decode" or summary is None or not os.path.exists(summary):
         return None
     fields = {}
-    for line in open(TRAFFIC_SUMMARY):
+    for line in open(summary):
         parts = line.split()
         if len(parts) >= 2 and parts[0].startswith("traffic_"):
             fields[parts[0]] = float(parts[1])
@@ -94,7 +96,7 @@ def measured_traffic(workload):
         return None
     return dict(bytes_per_launch=fields["traffic_bytes_per_launch"],
                 algorithmic_bytes_per_launch=fields.get("traffic_algorithmic_bytes_per_launch"),
-                source=os.path.relpath(TRAFFIC_SUMMARY, ROOT))
+                source=os.path.relpath(summary, ROOT))
 
 
 def cpu_baseline(run, wl, start_step, max_tokens=24, budget_s=15.0):
@@ -392,6 +394,8 @@ def main():
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill leg")
     ap.add_argument("--no-sweep", action="store_true", help="skip the iso-VRAM budget sweep against static offload")
     ap.add_argument("--no-prefetch", action="store_true", help="skip the speculative-prefetch leg")
+    ap.add_argument("--no-fusion", action="store_true",
+                    help="separate down and combine kernels instead of the fused down+combine (single-token steps)")
     ap.add_argument("--census-steps", type=int, default=24,
                     help="extra decode steps after the timed region with every kernel class timed (0 = skip)")
     args = ap.parse_args()
@@ -428,6 +432,7 @@ def main():
     hbm_copy = measure_hbm_copy(torch, wisp)
     log(f"host->device {link:.1f} GB/s (median of 5 x {n_probe} blobs); device copy {hbm_copy:.0f} GB/s")
     assert run.set_cap(wl.cap) == wl.cap
+    run.ctx.set_fusion(not args.no_fusion)
 
     def timed_pass(pager, mask):
         """Cold slot tables, `warmup` untimed steps, then the timed steps; returns (elapsed, stats)."""
@@ -496,7 +501,7 @@ def main():
             f"{passes['host']['path_roofline']['frac']:.3f} of the path roofline")
         if "ffn_gateup" in tk:
             g = tk["ffn_gateup"]
-            tr = measured_traffic(wl.name)
+            tr = measured_traffic(wl.name, "ffn_gateup")
             roof = dict(bound="hbm", achieved=g["GBps"], peak=HBM_PEAK_GBPS, unit="GB/s", frac=g["GBps"] / HBM_PEAK_GBPS,
                         traffic=tr["bytes_per_launch"] if tr else None,
                         traffic_detail=tr, kernel="ffn_rows<bf16,bf16,gate/up> expert GEMV (W1+W3 rows), host-pager pass",

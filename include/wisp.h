@@ -207,6 +207,14 @@ wisp_status wisp_expert_in_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, int3
 /* Copy the device bytes of `slot` of `layer` to host memory dst (M_e bytes); synchronous. */
 wisp_status wisp_read_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, void* dst);
 
+/* Down projection fused with the combine (on by default).  A layer-step of one token with bf16
+ * weights whose union fits the cap runs the down projection of all its experts and the
+ * gate-weighted combine in one launch (the per-expert outputs stay on chip) instead of a down launch
+ * per expert group and a combine launch; the arithmetic of every row and of the combine is the
+ * same, so the outputs are bit-identical either way.  on = 0 selects the separate kernels (for
+ * comparison).  Applies to both pagers.  WISP_E_STATE while a page-in is pending. */
+wisp_status wisp_set_fusion(wisp_ctx* ctx, int32_t on);
+
 /* Kernel timing.  Launches of the classes whose bit is set in class_mask (1 << wisp_kernel_class;
  * 0 = off) are bracketed by HIP events on their own stream (kernels through the launch's own
  * start/stop events, fill batches by events on the side stream); durations accumulate per class.
@@ -214,7 +222,7 @@ wisp_status wisp_read_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, void* dst
 typedef enum {
   WISP_K_ROUTER_LOGITS = 0, WISP_K_ROUTER_SELECT = 1, WISP_K_FFN_GATEUP = 2, WISP_K_FFN_DOWN = 3,
   WISP_K_COMBINE = 4, WISP_K_H2D_FILL = 5, WISP_K_GROUPED_GATEUP = 6, WISP_K_GROUPED_DOWN = 7,
-  WISP_K_PERMUTE = 8, WISP_K_NUM = 9
+  WISP_K_PERMUTE = 8, WISP_K_DOWN_COMBINE = 9, WISP_K_NUM = 10
 } wisp_kernel_class;
 wisp_status wisp_set_profiling(wisp_ctx* ctx, int32_t class_mask);
 /* Waits for outstanding timed work, then returns the accumulated total milliseconds, number of

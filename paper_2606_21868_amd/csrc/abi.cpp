@@ -149,6 +149,7 @@ struct wisp_ctx {
   FfnBatch* d_plan = nullptr;        // launch plan written by the device pager
   uint32_t* d_stats = nullptr;       // [L][2] hits, misses of the current step
   uint32_t* h_stats = nullptr;       // pinned copy
+  bool fusion = true;                // single-token steps: down projection fused with the combine
   // speculative prefetch inside wisp_decode_step (host pager)
   int32_t pf_mode = WISP_PREFETCH_OFF;
   wisp_predictor* pf_pred = nullptr;
@@ -210,6 +211,8 @@ void harvest(wisp_ctx* c, bool wait) {
       c->k_n[p.kclass] += 1;
       c->k_bytes[p.kclass] += p.bytes;
       c->k_flops[p.kclass] += p.flops;
+    } else {
+      (void)hipGetLastError();   // a pair that could not be timed must not leave an error for the next launch check
     }
     c->ev_pool.push_back(p.a);
     c->ev_pool.push_back(p.b);
@@ -458,7 +461,7 @@ uint64_t ffn_bytes(const wisp_ctx* c, const FfnBatch& b, bool gateup) {
 struct Pair { int32_t t, out; };
 struct Work { const uint8_t* w; std::vector<Pair> pairs; };
 
-wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, hipStream_t st) {
+wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, hipStream_t st, bool down = true) {
   FfnBatch b;
   b.n_items = 0;
   b.max_ntok = 0;
@@ -467,9 +470,11 @@ wisp_status run_ffn(wisp_ctx* c, const std::vector<Work>& work, const void* x, h
     LaunchTiming t1 = timing_begin(c, WISP_K_FFN_GATEUP);
     WISP_HIP(launch_ffn_gateup(b, c->shape, x, c->h, st, t1), "ffn gate/up launch");
     timing_end(c, t1, WISP_K_FFN_GATEUP, ffn_bytes(c, b, true));
-    LaunchTiming t2 = timing_begin(c, WISP_K_FFN_DOWN);
-    WISP_HIP(launch_ffn_down(b, c->shape, c->h, c->buf, st, t2), "ffn down launch");
-    timing_end(c, t2, WISP_K_FFN_DOWN, ffn_bytes(c, b, false));
+    if (down) {
+      LaunchTiming t2 = timing_begin(c, WISP_K_FFN_DOWN);
+      WISP_HIP(launch_ffn_down(b, c->shape, c->h, c->buf, st, t2), "ffn down launch");
+      timing_end(c, t2, WISP_K_FFN_DOWN, ffn_bytes(c, b, false));
+    }
     b.n_items = 0;
     b.max_ntok = 0;
     return WISP_OK;
@@ -651,6 +656,7 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   c->e_cnt.assign(N, 0);
   c->e_off.assign(N + 1, 0);
   c->pf_mark.assign(N, 0);
+
   c->pair_order.resize(static_cast<size_t>(T) * k);
   *out = c;
   g_err.clear();
@@ -835,6 +841,15 @@ wisp_status wisp_preload(wisp_ctx* ctx) {
   if (s != WISP_OK) return s;
   if (ctx->pager == WISP_PAGER_DEVICE) return with_host_tables(ctx, [&] { return preload_host(ctx); });
   return preload_host(ctx);
+}
+
+wisp_status wisp_set_fusion(wisp_ctx* ctx, int32_t on) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  for (auto& L : ctx->layers)
+    if (L.pending) return fail(WISP_E_STATE, "a page-in is pending");
+  ctx->fusion = on != 0;
+  return WISP_OK;
 }
 
 wisp_status wisp_set_pager(wisp_ctx* ctx, int32_t pager) {
@@ -1079,7 +1094,43 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
     }
     return wk;
   };
-  for (size_t ci = 0; ci < nch; ++ci) {
+  // one token, one chunk: gate/up of the resident experts (and the shared one), then of the faulted
+  // ones after their fills, then one down + combine launch over all of them
+  const bool fused = !grouped && ctx->fusion && nch == 1 && T == 1 && down_combine_supported(ctx->shape);
+  if (fused) {
+    const ChunkPlan& cp = L.plan.chunks[0];
+    std::vector<Work> hits, faults;
+    FusedT1Items all{};
+    for (size_t i = 0; i < cp.experts.size(); ++i) {
+      (cp.fault[i] ? faults : hits).push_back(work_of(cp.experts[i], L.chunk_ptrs[0][i]));
+      all.w[all.n_items] = L.chunk_ptrs[0][i];
+      all.rank[all.n_items] = ctx->pair_order[off[cp.experts[i]]];   // T = 1: the pair index is the rank
+      ++all.n_items;
+    }
+    if (ctx->desc.has_shared) {
+      Work wk;
+      wk.w = L.shared_dev;
+      wk.pairs.push_back({0, k});
+      hits.push_back(std::move(wk));
+      all.w[all.n_items] = L.shared_dev;
+      all.rank[all.n_items] = k;
+      ++all.n_items;
+    }
+    if (!hits.empty() && (s = run_ffn(ctx, hits, x_dev, sm, false)) != WISP_OK) return s;
+    if (!faults.empty()) {
+      WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[0], 0), "hipStreamWaitEvent(fill)");
+      if ((s = run_ffn(ctx, faults, x_dev, sm, false)) != WISP_OK) return s;
+    }
+    FfnBatch b;
+    b.n_items = all.n_items;
+    b.max_ntok = 1;
+    for (int i = 0; i < all.n_items; ++i) b.items[i].ntok = 1;
+    LaunchTiming td = timing_begin(ctx, WISP_K_DOWN_COMBINE);
+    WISP_HIP(launch_down_combine_t1(all, ctx->shape, ctx->h, w_dev, y_dev, k, ctx->desc.has_shared, sm, td),
+             "down+combine launch");
+    timing_end(ctx, td, WISP_K_DOWN_COMBINE, ffn_bytes(ctx, b, false) + static_cast<uint64_t>(k) * 4);
+  }
+  for (size_t ci = 0; ci < nch && !fused; ++ci) {
     const ChunkPlan& cp = L.plan.chunks[ci];
     if (ci > 0 && (s = issue_fills(ctx, layer, ci)) != WISP_OK) return s;
     if (grouped) {
@@ -1109,12 +1160,14 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
     }
     if (ci + 1 < nch) WISP_HIP(hipEventRecord(L.chunk_ev[ci], sm), "hipEventRecord(chunk)");
   }
-  LaunchTiming tc = timing_begin(ctx, WISP_K_COMBINE);
-  WISP_HIP(launch_combine(T, k, ctx->desc.d_model, ctx->desc.has_shared, w_dev, ctx->buf, y_dev, sm, tc),
-           "combine launch");
-  timing_end(ctx, tc, WISP_K_COMBINE,
-             static_cast<uint64_t>(T) * ctx->desc.d_model * 4 * (k + ctx->desc.has_shared + 1) +
-                 static_cast<uint64_t>(T) * k * 4);
+  if (!fused) {
+    LaunchTiming tc = timing_begin(ctx, WISP_K_COMBINE);
+    WISP_HIP(launch_combine(T, k, ctx->desc.d_model, ctx->desc.has_shared, w_dev, ctx->buf, y_dev, sm, tc),
+             "combine launch");
+    timing_end(ctx, tc, WISP_K_COMBINE,
+               static_cast<uint64_t>(T) * ctx->desc.d_model * 4 * (k + ctx->desc.has_shared + 1) +
+                   static_cast<uint64_t>(T) * k * 4);
+  }
   WISP_HIP(hipEventRecord(L.use_ev, sm), "hipEventRecord(use)");
   L.use_ev_recorded = true;
   L.pending = false;
@@ -1140,6 +1193,7 @@ wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_
     hipStream_t sm = static_cast<hipStream_t>(stream);
     const int max_items = T * d.top_k + d.has_shared;
     const int C = ctx->cap;
+    const bool dc = ctx->fusion && T == 1 && down_combine_supported(ctx->shape);
     for (int32_t l = 0; l < d.n_layers; ++l) {
       LayerState& L = ctx->layers[l];
       if (!L.wr) return fail(WISP_E_STATE, "router weights not set for this layer");
@@ -1161,14 +1215,22 @@ wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_
                "device pager launch");
       timing_end(ctx, t2, WISP_K_ROUTER_SELECT, 0);
       LaunchTiming t3 = timing_begin(ctx, WISP_K_FFN_GATEUP);
-      LaunchTiming t4 = timing_begin(ctx, WISP_K_FFN_DOWN);
-      WISP_HIP(launch_ffn_dev(ctx->d_plan, max_items, ctx->shape, xl, ctx->h, ctx->buf, sm, t3, t4),
+      LaunchTiming t4 = dc ? LaunchTiming{} : timing_begin(ctx, WISP_K_FFN_DOWN);
+      WISP_HIP(launch_ffn_dev(ctx->d_plan, max_items, ctx->shape, xl, ctx->h, ctx->buf, !dc, sm, t3, t4),
                "device-planned FFN launch");
       timing_end(ctx, t3, WISP_K_FFN_GATEUP, 0);
-      timing_end(ctx, t4, WISP_K_FFN_DOWN, 0);
-      LaunchTiming t5 = timing_begin(ctx, WISP_K_COMBINE);
-      WISP_HIP(launch_combine(T, d.top_k, d.d_model, d.has_shared, wl, ctx->buf, yl, sm, t5), "combine launch");
-      timing_end(ctx, t5, WISP_K_COMBINE, 0);
+      if (!dc) timing_end(ctx, t4, WISP_K_FFN_DOWN, 0);
+      if (dc) {
+        LaunchTiming t5 = timing_begin(ctx, WISP_K_DOWN_COMBINE);
+        WISP_HIP(launch_down_combine_dev(ctx->d_plan, max_items, ctx->shape, ctx->h, wl, yl, d.top_k, d.has_shared, sm,
+                                         t5),
+                 "device-planned down+combine launch");
+        timing_end(ctx, t5, WISP_K_DOWN_COMBINE, 0);
+      } else {
+        LaunchTiming t5 = timing_begin(ctx, WISP_K_COMBINE);
+        WISP_HIP(launch_combine(T, d.top_k, d.d_model, d.has_shared, wl, ctx->buf, yl, sm, t5), "combine launch");
+        timing_end(ctx, t5, WISP_K_COMBINE, 0);
+      }
     }
     WISP_HIP(hipMemcpyAsync(ctx->h_stats, ctx->d_stats, sizeof(uint32_t) * 2 * d.n_layers, hipMemcpyDeviceToHost, sm),
              "stats copy");

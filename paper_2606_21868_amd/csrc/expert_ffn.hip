@@ -20,6 +20,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "kernels.hpp"
 
 namespace wisp {
@@ -411,6 +413,58 @@ struct FfnT1Batch {
   int32_t n_items;
 };
 
+// One row pass of the single-token body, split so that the weight loads can be issued early: the
+// lane's NL 16-byte chunks of row rr of the first (and, for gate/up, second) matrix ...
+template <int MODE, int LPR, int NL>
+__device__ __forceinline__ void t1_load(const uint8_t* w, uint32_t off0, uint32_t off1, size_t row_b, int rr, int sl,
+                                        uint4* a, uint4* b) {
+  const uint4* row0 = reinterpret_cast<const uint4*>(w + off0 + rr * row_b);
+  const uint4* row1 = reinterpret_cast<const uint4*>(w + off1 + rr * row_b);
+#pragma unroll
+  for (int m = 0; m < NL; ++m) {
+    a[m] = row0[m * LPR + sl];
+    if constexpr (MODE == MODE_GATEUP) b[m] = row1[m * LPR + sl];
+  }
+}
+
+// ... the lane's input chunks (issued after the weights) ...
+template <int LPR, int NL>
+__device__ __forceinline__ void t1_input(const uint4* xrow, int sl, uint4* xr) {
+#pragma unroll
+  for (int m = 0; m < NL; ++m) xr[m] = xrow[m * LPR + sl];
+}
+
+// ... and the row's dot products: one v_dot2c_f32_bf16 chain over the lane's chunks, then the
+// shuffle reduction over the LPR lanes of the row group.  Every single-token kernel computes a row
+// through this function, so a row has the same bits whichever kernel computes it.
+template <int MODE, int LPR, int NL>
+__device__ __forceinline__ void t1_dot(const uint4* a, const uint4* b, const uint4* xr, float& acc0, float& acc1) {
+  acc0 = 0.f;
+  acc1 = 0.f;
+#pragma unroll
+  for (int m = 0; m < NL; ++m) {
+    acc0 = dot2_bf16(a[m].x, xr[m].x, acc0);
+    acc0 = dot2_bf16(a[m].y, xr[m].y, acc0);
+    acc0 = dot2_bf16(a[m].z, xr[m].z, acc0);
+    acc0 = dot2_bf16(a[m].w, xr[m].w, acc0);
+    if constexpr (MODE == MODE_GATEUP) {
+      acc1 = dot2_bf16(b[m].x, xr[m].x, acc1);
+      acc1 = dot2_bf16(b[m].y, xr[m].y, acc1);
+      acc1 = dot2_bf16(b[m].z, xr[m].z, acc1);
+      acc1 = dot2_bf16(b[m].w, xr[m].w, acc1);
+    }
+  }
+#pragma unroll
+  for (int off = LPR / 2; off > 0; off >>= 1) {
+    acc0 += __shfl_xor(acc0, off, 64);
+    if constexpr (MODE == MODE_GATEUP) acc1 += __shfl_xor(acc1, off, 64);
+  }
+}
+
+__device__ __forceinline__ uint16_t swiglu_bf16(float a, float b) {
+  return f32_to_bf16_rne(a / (1.0f + __expf(-a)) * b);
+}
+
 template <int MODE, int LPR, int NL>
 __global__ void __launch_bounds__(256) ffn_rows_t1(const FfnT1Batch B, const uint8_t* __restrict__ vin, int vin_stride,
                                                    int K, int R, int rows_per_wg, int blocks_per_item, uint32_t off0,
@@ -428,43 +482,94 @@ __global__ void __launch_bounds__(256) ffn_rows_t1(const FfnT1Batch B, const uin
     const int r = rbase + sub;
     const bool valid = r < r_end;
     const int rr = valid ? r : r_begin;
-    const uint4* row0 = reinterpret_cast<const uint4*>(w + off0 + rr * row_b);
-    const uint4* row1 = reinterpret_cast<const uint4*>(w + off1 + rr * row_b);
     uint4 a[NL], b[NL], xr[NL];
-#pragma unroll
-    for (int m = 0; m < NL; ++m) {
-      a[m] = row0[m * LPR + sl];
-      if constexpr (MODE == MODE_GATEUP) b[m] = row1[m * LPR + sl];
-    }
-#pragma unroll
-    for (int m = 0; m < NL; ++m) xr[m] = xrow[m * LPR + sl];
-    float acc0 = 0.f, acc1 = 0.f;
-#pragma unroll
-    for (int m = 0; m < NL; ++m) {
-      acc0 = dot2_bf16(a[m].x, xr[m].x, acc0);
-      acc0 = dot2_bf16(a[m].y, xr[m].y, acc0);
-      acc0 = dot2_bf16(a[m].z, xr[m].z, acc0);
-      acc0 = dot2_bf16(a[m].w, xr[m].w, acc0);
-      if constexpr (MODE == MODE_GATEUP) {
-        acc1 = dot2_bf16(b[m].x, xr[m].x, acc1);
-        acc1 = dot2_bf16(b[m].y, xr[m].y, acc1);
-        acc1 = dot2_bf16(b[m].z, xr[m].z, acc1);
-        acc1 = dot2_bf16(b[m].w, xr[m].w, acc1);
-      }
-    }
-#pragma unroll
-    for (int off = LPR / 2; off > 0; off >>= 1) {
-      acc0 += __shfl_xor(acc0, off, 64);
-      if constexpr (MODE == MODE_GATEUP) acc1 += __shfl_xor(acc1, off, 64);
-    }
+    t1_load<MODE, LPR, NL>(w, off0, off1, row_b, rr, sl, a, b);
+    t1_input<LPR, NL>(xrow, sl, xr);
+    float acc0, acc1;
+    t1_dot<MODE, LPR, NL>(a, b, xr, acc0, acc1);
     if (valid && sl == 0) {
       const size_t o = static_cast<size_t>(B.out[item]) * out_stride + r;
       if constexpr (MODE == MODE_GATEUP)
-        reinterpret_cast<uint16_t*>(out)[o] = f32_to_bf16_rne(acc0 / (1.0f + __expf(-acc0)) * acc1);
+        reinterpret_cast<uint16_t*>(out)[o] = swiglu_bf16(acc0, acc1);
       else
         reinterpret_cast<float*>(out)[o] = acc0;
     }
   }
+}
+
+// ------------------------------------------------------------------------------------------
+// Down projection fused with the gate-weighted combine, for single-token steps with bf16 weights
+// (every decode layer-step at batch 1).  A workgroup owns RPW output rows for all of the step's
+// experts: wave w computes o_j for the experts w, w + 4, ... (W2 rows first, then the h slices),
+// the outputs meet in LDS and y = sum_j g_j o_j (+ the shared expert) is formed in rank order.  The
+// separate down kernel writes every o_j to HBM for a combine launch to read back; here it never
+// leaves the chip, and a layer-step needs one launch less.  Each o_j is t1_dot's chain and the sum
+// is the combine kernel's fmaf chain, so y has the same bits as down + combine.
+// ------------------------------------------------------------------------------------------
+template <int LPR, int NL, int MAXW>
+__device__ __forceinline__ void down_combine_t1(int n, const uint8_t* const* w, const int32_t* rank, const uint8_t* h,
+                                                const float* __restrict__ gates, float* __restrict__ y, int d, int I,
+                                                int k, int has_shared, uint32_t off2, float* o_lds) {
+  constexpr int RPW = 64 / LPR;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int sub = lane / LPR, sl = lane - sub * LPR;
+  const int r0 = blockIdx.x * RPW;
+  const int r = r0 + sub;
+  const int rr = r < d ? r : r0;
+  const size_t row_b = static_cast<size_t>(I) * 2;
+  uint4 a[MAXW][NL], xr[MAXW][NL];
+#pragma unroll
+  for (int q = 0; q < MAXW; ++q) {
+    const int i = wave + 4 * q;
+    if (i < n) t1_load<MODE_DOWN, LPR, NL>(w[i], off2, off2, row_b, rr, sl, a[q], a[q]);
+  }
+#pragma unroll
+  for (int q = 0; q < MAXW; ++q) {
+    const int i = wave + 4 * q;
+    if (i < n) t1_input<LPR, NL>(reinterpret_cast<const uint4*>(h + static_cast<size_t>(rank[i]) * row_b), sl, xr[q]);
+  }
+#pragma unroll
+  for (int q = 0; q < MAXW; ++q) {
+    const int i = wave + 4 * q;
+    if (i >= n) continue;
+    float acc0, acc1;
+    t1_dot<MODE_DOWN, LPR, NL>(a[q], a[q], xr[q], acc0, acc1);
+    if (sl == 0) o_lds[rank[i] * RPW + sub] = acc0;
+  }
+  __syncthreads();
+  if (tid < RPW && r0 + tid < d) {
+    float acc = 0.f;
+    for (int j = 0; j < k; ++j) acc = fmaf(gates[j], o_lds[j * RPW + tid], acc);
+    if (has_shared) acc += o_lds[k * RPW + tid];
+    y[r0 + tid] = acc;
+  }
+}
+
+// host-planned: the experts come with the launch
+template <int LPR, int NL, int MAXW>
+__global__ void __launch_bounds__(256) ffn_down_combine_t1(const FusedT1Items B, const uint8_t* __restrict__ h,
+                                                           const float* __restrict__ gates, float* __restrict__ y,
+                                                           int d, int I, int k, int has_shared, uint32_t off2) {
+  __shared__ float o_lds[9 * 64];
+  down_combine_t1<LPR, NL, MAXW>(B.n_items, B.w, B.rank, h, gates, y, d, I, k, has_shared, off2, o_lds);
+}
+
+// device-planned: the experts of the plan the device pager wrote (single-token items; the output
+// row of token 0 is the rank)
+template <int LPR, int NL, int MAXW>
+__global__ void __launch_bounds__(256) ffn_down_combine_dev(const FfnBatch* __restrict__ P, const uint8_t* __restrict__ h,
+                                                            const float* __restrict__ gates, float* __restrict__ y,
+                                                            int d, int I, int k, int has_shared, uint32_t off2) {
+  __shared__ float o_lds[9 * 64];
+  __shared__ const uint8_t* w[kMaxItems];
+  __shared__ int32_t rank[kMaxItems];
+  const int n = P->n_items;
+  if (threadIdx.x < n) {
+    w[threadIdx.x] = P->items[threadIdx.x].w;
+    rank[threadIdx.x] = P->items[threadIdx.x].out[0];
+  }
+  __syncthreads();
+  down_combine_t1<LPR, NL, MAXW>(n, w, rank, h, gates, y, d, I, k, has_shared, off2, o_lds);
 }
 
 using T1Kernel = void (*)(const FfnT1Batch, const uint8_t*, int, int, int, int, int, uint32_t, uint32_t, uint8_t*, int);
@@ -597,6 +702,67 @@ hipError_t launch_ffn_down(const FfnBatch& b, const FfnShape& s, const void* h, 
 }
 
 namespace {
+// (lanes per row, 16-byte loads per lane) of the down rows of a single-token bf16 step, or false
+bool dc_shape(const FfnShape& s, int* lpr, int* nl) {
+  const BlobLayout& L = s.blob;
+  if (L.w_dtype != DT_BF16 || s.h_dtype != DT_BF16 || L.I % 8) return false;
+  *lpr = pick_lpr(L.I / 8);
+  if (!*lpr) return false;
+  *nl = L.I / 8 / *lpr;
+  return (*lpr == 32 && *nl == 3) || (*lpr == 16 && *nl == 1) || (*lpr == 16 && *nl == 3) || (*lpr == 64 && *nl == 2);
+}
+
+template <int LPR, int NL>
+hipError_t dc_launch(bool dev, const void* items, const FfnShape& s, const void* h, const float* gates, float* y, int k,
+                     int has_shared, int max_items, hipStream_t st, const LaunchTiming& tm) {
+  const BlobLayout& L = s.blob;
+  const dim3 grid((L.d + 64 / LPR - 1) / (64 / LPR)), block(256);
+  const uint32_t off2 = static_cast<uint32_t>(L.off_w2);
+  // three experts per wave: a single-token step has at most k + 1 <= 9 experts
+  if (max_items > 12) return hipErrorInvalidValue;
+  if (dev)
+    hipExtLaunchKernelGGL(ffn_down_combine_dev<LPR, NL, 3>, grid, block, 0, st, tm.start, tm.stop, 0,
+                          static_cast<const FfnBatch*>(items), static_cast<const uint8_t*>(h), gates, y, L.d, L.I, k,
+                          has_shared, off2);
+  else
+    hipExtLaunchKernelGGL(ffn_down_combine_t1<LPR, NL, 3>, grid, block, 0, st, tm.start, tm.stop, 0,
+                          *static_cast<const FusedT1Items*>(items), static_cast<const uint8_t*>(h), gates, y, L.d, L.I,
+                          k, has_shared, off2);
+  return hipGetLastError();
+}
+
+hipError_t dc_dispatch(bool dev, const void* items, const FfnShape& s, const void* h, const float* gates, float* y,
+                       int k, int has_shared, int max_items, hipStream_t st, const LaunchTiming& tm) {
+  int lpr = 0, nl = 0;
+  if (!dc_shape(s, &lpr, &nl)) return hipErrorNotSupported;
+  if (max_items < 1 || max_items > 12 || k < 1 || k > 8) return hipErrorInvalidValue;
+  if (lpr == 32 && nl == 3) return dc_launch<32, 3>(dev, items, s, h, gates, y, k, has_shared, max_items, st, tm);
+  if (lpr == 16 && nl == 1) return dc_launch<16, 1>(dev, items, s, h, gates, y, k, has_shared, max_items, st, tm);
+  if (lpr == 16 && nl == 3) return dc_launch<16, 3>(dev, items, s, h, gates, y, k, has_shared, max_items, st, tm);
+  return dc_launch<64, 2>(dev, items, s, h, gates, y, k, has_shared, max_items, st, tm);
+}
+}  // namespace
+
+bool down_combine_supported(const FfnShape& s) {
+  int lpr = 0, nl = 0;
+  return dc_shape(s, &lpr, &nl);
+}
+
+hipError_t launch_down_combine_t1(const FusedT1Items& items, const FfnShape& s, const void* h, const float* gates,
+                                  float* y, int k, int has_shared, hipStream_t st, const LaunchTiming& tm) {
+  if (items.n_items < 1 || items.n_items > kMaxItems) return hipErrorInvalidValue;
+  for (int i = 0; i < items.n_items; ++i)
+    if (items.rank[i] < 0 || items.rank[i] > k || (items.rank[i] == k && !has_shared)) return hipErrorInvalidValue;
+  return dc_dispatch(false, &items, s, h, gates, y, k, has_shared, items.n_items, st, tm);
+}
+
+hipError_t launch_down_combine_dev(const FfnBatch* plan, int max_items, const FfnShape& s, const void* h,
+                                   const float* gates, float* y, int k, int has_shared, hipStream_t st,
+                                   const LaunchTiming& tm) {
+  return dc_dispatch(true, plan, s, h, gates, y, k, has_shared, max_items, st, tm);
+}
+
+namespace {
 // Shapes with a device-planned path: (w dtype, h dtype, d lanes/loads, I lanes/loads).
 struct DevShape { int lpr_g, nl_g, lpr_d, nl_d; };
 bool dev_shape(const FfnShape& s, DevShape* o) {
@@ -612,7 +778,8 @@ bool dev_shape(const FfnShape& s, DevShape* o) {
 }  // namespace
 
 hipError_t launch_ffn_dev(const FfnBatch* plan, int max_items, const FfnShape& s, const void* x, void* h,
-                          float* buf, hipStream_t st, const LaunchTiming& tm_gateup, const LaunchTiming& tm_down) {
+                          float* buf, bool with_down, hipStream_t st, const LaunchTiming& tm_gateup,
+                          const LaunchTiming& tm_down) {
   const BlobLayout& L = s.blob;
   DevShape ds;
   if (!dev_shape(s, &ds)) return hipErrorNotSupported;
@@ -657,7 +824,7 @@ hipError_t launch_ffn_dev(const FfnBatch* plan, int max_items, const FfnShape& s
                         static_cast<uint32_t>(L.off_w2), static_cast<uint32_t>(L.bytes - L.off_w2),
                         static_cast<uint8_t*>(h));
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || !with_down) return e;
   // down: per item slot, one row pass per workgroup
   const int rows_d = 4 * (64 / ds.lpr_d);
   const int bpi_d = (L.d + rows_d - 1) / rows_d;

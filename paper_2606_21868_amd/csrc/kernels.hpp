@@ -62,11 +62,29 @@ hipError_t launch_ffn_gateup(const FfnBatch& b, const FfnShape& s, const void* x
 // Phase 2: buf[out] = W2 h[out]; buf row stride = d (fp32).
 hipError_t launch_ffn_down(const FfnBatch& b, const FfnShape& s, const void* h, float* buf, hipStream_t st,
                            const LaunchTiming& tm);
+// Down projection fused with the combine, one token (bf16 weights and h): for the items (an expert
+// blob and the output row `rank`: its rank j < k, or k for the shared expert), o_rank = W2 h[rank]
+// and y = sum_j gates[j] o_j (j ascending) + o_k if has_shared, with the bits of launch_ffn_down +
+// launch_combine.  The items must cover every rank 0..k-1 (and k with the shared expert).
+struct FusedT1Items {
+  const uint8_t* w[kMaxItems];
+  int32_t rank[kMaxItems];
+  int32_t n_items;
+};
+bool down_combine_supported(const FfnShape& s);
+hipError_t launch_down_combine_t1(const FusedT1Items& items, const FfnShape& s, const void* h, const float* gates,
+                                  float* y, int k, int has_shared, hipStream_t st, const LaunchTiming& tm);
+// The same over the device pager's plan (single-token items; out[0] is the rank).
+hipError_t launch_down_combine_dev(const FfnBatch* plan, int max_items, const FfnShape& s, const void* h,
+                                   const float* gates, float* y, int k, int has_shared, hipStream_t st,
+                                   const LaunchTiming& tm);
+
 // Device-planned FFN of one layer-step (plan written to HBM by the device pager): gate/up, with
-// faulted experts streamed from their pinned masters into their slots by the same kernel, then
-// down into buf; the caller launches the combine.  max_items bounds the plan (T*k + shared).
+// faulted experts streamed from their pinned masters into their slots by the same kernel, then (if
+// with_down) down into buf for the caller's combine.  max_items bounds the plan (T*k + shared).
 hipError_t launch_ffn_dev(const FfnBatch* plan, int max_items, const FfnShape& s, const void* x, void* h,
-                          float* buf, hipStream_t st, const LaunchTiming& tm_gateup, const LaunchTiming& tm_down);
+                          float* buf, bool with_down, hipStream_t st, const LaunchTiming& tm_gateup,
+                          const LaunchTiming& tm_down);
 bool ffn_dev_supported(const FfnShape& s, int T, int k, int has_shared);
 
 // y[t] = sum_j w[t, j] buf[t*(k+1)+j] (j ascending) + (shared ? buf[t*(k+1)+k] : 0).

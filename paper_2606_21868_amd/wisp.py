@@ -26,9 +26,9 @@ PAGER_HOST, PAGER_DEVICE = 0, 1
 OFFLOAD_BULK, OFFLOAD_ZERO_COPY = 0, 1
 PREFETCH_OFF, PREFETCH_PREDICTOR, PREFETCH_HINTS = 0, 1, 2
 (K_ROUTER_LOGITS, K_ROUTER_SELECT, K_FFN_GATEUP, K_FFN_DOWN, K_COMBINE, K_H2D_FILL, K_GROUPED_GATEUP,
- K_GROUPED_DOWN, K_PERMUTE) = range(9)
+ K_GROUPED_DOWN, K_PERMUTE, K_DOWN_COMBINE) = range(10)
 KERNEL_CLASS_NAMES = ["router_logits", "router_select", "ffn_gateup", "ffn_down", "combine", "h2d_fill",
-                      "grouped_gateup", "grouped_down", "permute"]
+                      "grouped_gateup", "grouped_down", "permute", "down_combine"]
 
 
 class WispError(RuntimeError):
@@ -85,6 +85,7 @@ _SIGS = {
     "wisp_set_budget": [_P, _U64, ctypes.POINTER(_I)],
     "wisp_preload": [_P],
     "wisp_set_pager": [_P, _I],
+    "wisp_set_fusion": [_P, _I],
     "wisp_route_topk": [_P, _I, _P, _I, _P, _P, _P, _P],
     "wisp_page_in": [_P, _I, _P, _I, ctypes.POINTER(PageStats)],
     "wisp_moe_forward": [_P, _I, _P, _I, _P, _P, _P, ctypes.POINTER(PageStats)],
@@ -239,6 +240,10 @@ class Context:
     def set_pager(self, pager):
         """PAGER_HOST (host slot table, hipMemcpyAsync fills) or PAGER_DEVICE (slot table in HBM)."""
         check(lib().wisp_set_pager(self.h, int(pager)), "wisp_set_pager")
+
+    def set_fusion(self, on):
+        """Down projection fused with the combine for single-token steps (default on), or separate kernels."""
+        check(lib().wisp_set_fusion(self.h, int(bool(on))), "wisp_set_fusion")
 
     def route_topk(self, layer, x, T, idx, w, idx_host=None, stream=None):
         check(lib().wisp_route_topk(self.h, layer, _ptr(x), T, _ptr(idx), _ptr(w), _ptr(idx_host), _stream(stream)),
