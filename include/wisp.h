@@ -207,12 +207,14 @@ wisp_status wisp_expert_in_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, int3
 /* Copy the device bytes of `slot` of `layer` to host memory dst (M_e bytes); synchronous. */
 wisp_status wisp_read_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, void* dst);
 
-/* Down projection fused with the combine (on by default).  A layer-step of one token with bf16
- * weights whose union fits the cap runs the down projection of all its experts and the
- * gate-weighted combine in one launch (the per-expert outputs stay on chip) instead of a down launch
- * per expert group and a combine launch; the arithmetic of every row and of the combine is the
- * same, so the outputs are bit-identical either way.  on = 0 selects the separate kernels (for
- * comparison).  Applies to both pagers.  WISP_E_STATE while a page-in is pending. */
+/* Fused decode kernels (on by default).  (1) A layer-step of one token with bf16 weights whose
+ * union fits the cap runs the down projection of all its experts and the gate-weighted combine in
+ * one launch (the per-expert outputs stay on chip) instead of a down launch per expert group and a
+ * combine launch.  (2) The device pager computes the router logits and, in the workgroup that
+ * completes them, the selection and Algorithm 1 in one launch instead of two.  Every logit, row,
+ * decision and sum is computed by the same operations in the same order either way, so routing,
+ * paging and outputs are bit-identical.  on = 0 selects the separate kernels (for comparison).
+ * WISP_E_STATE while a page-in is pending. */
 wisp_status wisp_set_fusion(wisp_ctx* ctx, int32_t on);
 
 /* Kernel timing.  Launches of the classes whose bit is set in class_mask (1 << wisp_kernel_class;

@@ -149,7 +149,8 @@ struct wisp_ctx {
   FfnBatch* d_plan = nullptr;        // launch plan written by the device pager
   uint32_t* d_stats = nullptr;       // [L][2] hits, misses of the current step
   uint32_t* h_stats = nullptr;       // pinned copy
-  bool fusion = true;                // single-token steps: down projection fused with the combine
+  bool fusion = true;                // fused decode kernels (route + page; down + combine)
+  uint32_t* d_arrive = nullptr;      // route + page: logit rows completed in the running launch
   // speculative prefetch inside wisp_decode_step (host pager)
   int32_t pf_mode = WISP_PREFETCH_OFF;
   wisp_predictor* pf_pred = nullptr;
@@ -315,6 +316,7 @@ void free_ctx(wisp_ctx* c) {
                   static_cast<void*>(c->d_stats)})
     if (p) hipFree(p);
   if (c->h_stats) hipHostFree(c->h_stats);
+  if (c->d_arrive) hipFree(c->d_arrive);
   delete c;
 }
 
@@ -656,6 +658,9 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   c->e_cnt.assign(N, 0);
   c->e_off.assign(N + 1, 0);
   c->pf_mark.assign(N, 0);
+  if (hipMalloc(&p, 256) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
+  c->d_arrive = static_cast<uint32_t*>(p);
+  if (hipMemset(c->d_arrive, 0, 256) != hipSuccess) return bail(WISP_E_HIP, "hipMemset(counter)");
 
   c->pair_order.resize(static_cast<size_t>(T) * k);
   *out = c;
@@ -1201,19 +1206,31 @@ wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_
       int32_t* il = idx_dev + static_cast<size_t>(l) * T * d.top_k;
       float* wl = w_dev + static_cast<size_t>(l) * T * d.top_k;
       float* yl = y_dev + static_cast<size_t>(l) * T * d.d_model;
-      LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_LOGITS);
-      WISP_HIP(launch_router_logits(L.wr, xl, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, sm, t1),
-               "router logits launch");
-      timing_end(ctx, t1, WISP_K_ROUTER_LOGITS, static_cast<uint64_t>(d.n_experts) * d.d_model * 4);
-      LaunchTiming t2 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
-      WISP_HIP(launch_select_page(ctx->logits, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, il, wl,
-                                  ctx->d_pi + static_cast<size_t>(l) * d.n_experts,
-                                  ctx->d_pinv + static_cast<size_t>(l) * C, ctx->d_tau + static_cast<size_t>(l) * C,
-                                  ctx->d_clock + l, C, ctx->d_slot_ptr + static_cast<size_t>(l) * C, ctx->masters[l],
-                                  ctx->master_stride, L.shared_dev, d.has_shared, ctx->d_plan, ctx->d_stats + 2 * l,
-                                  sm, t2),
-               "device pager launch");
-      timing_end(ctx, t2, WISP_K_ROUTER_SELECT, 0);
+      int32_t* pi_l = ctx->d_pi + static_cast<size_t>(l) * d.n_experts;
+      int32_t* pinv_l = ctx->d_pinv + static_cast<size_t>(l) * C;
+      uint64_t* tau_l = ctx->d_tau + static_cast<size_t>(l) * C;
+      const uint64_t* slot_l = ctx->d_slot_ptr + static_cast<size_t>(l) * C;
+      if (ctx->fusion) {
+        LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
+        WISP_HIP(launch_route_page(L.wr, xl, d.x_dtype, d.d_model, ctx->logits, ctx->d_arrive, T, d.n_experts, d.top_k,
+                                   d.route, d.n_groups, d.topk_groups, il, wl, pi_l, pinv_l, tau_l, ctx->d_clock + l, C,
+                                   slot_l, ctx->masters[l], ctx->master_stride, L.shared_dev, d.has_shared,
+                                   ctx->d_plan, ctx->d_stats + 2 * l, sm, t1),
+                 "device route + pager launch");
+        timing_end(ctx, t1, WISP_K_ROUTER_SELECT, static_cast<uint64_t>(d.n_experts) * d.d_model * 4);
+      } else {
+        LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_LOGITS);
+        WISP_HIP(launch_router_logits(L.wr, xl, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, sm, t1),
+                 "router logits launch");
+        timing_end(ctx, t1, WISP_K_ROUTER_LOGITS, static_cast<uint64_t>(d.n_experts) * d.d_model * 4);
+        LaunchTiming t2 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
+        WISP_HIP(launch_select_page(ctx->logits, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, il, wl,
+                                    pi_l, pinv_l, tau_l, ctx->d_clock + l, C, slot_l, ctx->masters[l],
+                                    ctx->master_stride, L.shared_dev, d.has_shared, ctx->d_plan, ctx->d_stats + 2 * l,
+                                    sm, t2),
+                 "device pager launch");
+        timing_end(ctx, t2, WISP_K_ROUTER_SELECT, 0);
+      }
       LaunchTiming t3 = timing_begin(ctx, WISP_K_FFN_GATEUP);
       LaunchTiming t4 = dc ? LaunchTiming{} : timing_begin(ctx, WISP_K_FFN_DOWN);
       WISP_HIP(launch_ffn_dev(ctx->d_plan, max_items, ctx->shape, xl, ctx->h, ctx->buf, !dc, sm, t3, t4),

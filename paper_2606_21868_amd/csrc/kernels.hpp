@@ -132,6 +132,16 @@ hipError_t launch_select_page(const float* logits, int T, int N, int k, int rout
                               const uint8_t* shared_dev, int has_shared, FfnBatch* plan, uint32_t* stats,
                               hipStream_t st, const LaunchTiming& tm);
 
+// Device pager, fused: the router logits of T <= 4 tokens (one workgroup per expert row, as
+// launch_router_logits) and, in the workgroup that completes them, launch_select_page's work.
+// `arrive` is a zero-initialised device counter used by one stream; the kernel leaves it zero.
+hipError_t launch_route_page(const float* wr, const void* x, int x_dtype, int d, float* logits, uint32_t* arrive, int T,
+                             int N, int k, int route, int n_groups, int topk_groups, int32_t* idx, float* w,
+                             int32_t* pi, int32_t* pinv, uint64_t* tau, uint64_t* clock, int C,
+                             const uint64_t* slot_ptr, const uint8_t* master_base, uint64_t master_stride,
+                             const uint8_t* shared_dev, int has_shared, FfnBatch* plan, uint32_t* stats,
+                             hipStream_t st, const LaunchTiming& tm);
+
 // Diagnostics.
 hipError_t launch_hbm_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
 hipError_t launch_decode_fp8(const uint8_t* codes, float* out, int n, hipStream_t st);

@@ -14,6 +14,7 @@
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
+#include "router_row.hpp"
 #include "select.hpp"
 
 namespace wisp {
@@ -32,15 +33,12 @@ struct PagerShared {
   int32_t nh, nf;
 };
 
-__global__ void __launch_bounds__(256) select_page_kernel(
-    const float* __restrict__ logits, int T, int N, int k, int route, int n_groups, int topk_groups,
-    int32_t* __restrict__ idx, float* __restrict__ w, int32_t* __restrict__ pi, int32_t* __restrict__ pinv,
-    uint64_t* __restrict__ tau, uint64_t* __restrict__ clock, int C, const uint64_t* __restrict__ slot_ptr,
-    const uint8_t* master_base, uint64_t master_stride, const uint8_t* shared_dev, int has_shared,
-    FfnBatch* __restrict__ plan, uint32_t* __restrict__ stats) {
-  __shared__ PagerShared sh;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  // the table does not depend on the routing: its reads overlap the logits reads
+// The layer's slot table into LDS (it does not depend on the routing, so these reads can be issued
+// before the logits are known).
+__device__ __forceinline__ void load_table(PagerShared& sh, int N, int C, const int32_t* __restrict__ pi,
+                                           const int32_t* __restrict__ pinv, const uint64_t* __restrict__ tau,
+                                           const uint64_t* __restrict__ clock, const uint64_t* __restrict__ slot_ptr) {
+  const int tid = threadIdx.x;
   if (tid < N) sh.pi[tid] = pi[tid];
   if (tid < C) {
     sh.pinv[tid] = pinv[tid];
@@ -49,7 +47,19 @@ __global__ void __launch_bounds__(256) select_page_kernel(
   }
   if (tid == 0) sh.clock = *clock;
   sh.in_r[tid] = 0;
-  select_tokens(logits, 0, T, N, k, route, n_groups, topk_groups, sh.s);   // ends with a barrier
+}
+
+// Selection, Algorithm 1 and the launch plan for one layer-step, by one workgroup whose table is in
+// sh (load_table) and whose threads have not yet synchronised since.
+template <bool COHERENT>
+__device__ __forceinline__ void select_and_page(
+    PagerShared& sh, const float* __restrict__ logits, int T, int N, int k, int route, int n_groups, int topk_groups,
+    int32_t* __restrict__ idx, float* __restrict__ w, int32_t* __restrict__ pi, int32_t* __restrict__ pinv,
+    uint64_t* __restrict__ tau, uint64_t* __restrict__ clock, int C, const uint8_t* master_base,
+    uint64_t master_stride, const uint8_t* shared_dev, int has_shared, FfnBatch* __restrict__ plan,
+    uint32_t* __restrict__ stats) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  select_tokens<COHERENT>(logits, 0, T, N, k, route, n_groups, topk_groups, sh.s);   // ends with a barrier
   if (wave < T && lane < k) {
     idx[wave * k + lane] = sh.s.sel[wave][lane];
     w[wave * k + lane] = sh.s.gate[wave][lane];
@@ -142,7 +152,74 @@ __global__ void __launch_bounds__(256) select_page_kernel(
   }
 }
 
+__global__ void __launch_bounds__(256) select_page_kernel(
+    const float* __restrict__ logits, int T, int N, int k, int route, int n_groups, int topk_groups,
+    int32_t* __restrict__ idx, float* __restrict__ w, int32_t* __restrict__ pi, int32_t* __restrict__ pinv,
+    uint64_t* __restrict__ tau, uint64_t* __restrict__ clock, int C, const uint64_t* __restrict__ slot_ptr,
+    const uint8_t* master_base, uint64_t master_stride, const uint8_t* shared_dev, int has_shared,
+    FfnBatch* __restrict__ plan, uint32_t* __restrict__ stats) {
+  __shared__ PagerShared sh;
+  load_table(sh, N, C, pi, pinv, tau, clock, slot_ptr);
+  select_and_page<false>(sh, logits, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
+                         master_base, master_stride, shared_dev, has_shared, plan, stats);
+}
+
+// Router logits, selection and Algorithm 1 of one layer-step in one launch.  Workgroup e computes
+// logit row e (router_row, as the router kernel does), publishes it at device scope and counts
+// itself in *arrive; the workgroup whose arrival is the N-th resets the counter and runs the
+// selection and the pager on the complete logits.  No workgroup waits for another.
+template <int XT>
+__global__ void __launch_bounds__(256) route_page_kernel(
+    const float* __restrict__ wr, const void* __restrict__ x, int d, float* __restrict__ logits,
+    uint32_t* __restrict__ arrive, int T, int N, int k, int route, int n_groups, int topk_groups,
+    int32_t* __restrict__ idx, float* __restrict__ w, int32_t* __restrict__ pi, int32_t* __restrict__ pinv,
+    uint64_t* __restrict__ tau, uint64_t* __restrict__ clock, int C, const uint64_t* __restrict__ slot_ptr,
+    const uint8_t* master_base, uint64_t master_stride, const uint8_t* shared_dev, int has_shared,
+    FfnBatch* __restrict__ plan, uint32_t* __restrict__ stats) {
+  __shared__ PagerShared sh;
+  __shared__ float part[4][4];
+  __shared__ int last;
+  const int e = blockIdx.x;
+  // every workgroup loads the table (a few hundred words, mostly L2 hits), so the one that turns out
+  // to be last has it in LDS already
+  load_table(sh, N, C, pi, pinv, tau, clock, slot_ptr);
+  const float z = router_row<XT>(wr, x, 0, T, d, e, part);
+  if (static_cast<int>(threadIdx.x) < T)
+    __hip_atomic_store(logits + static_cast<size_t>(threadIdx.x) * N + e, z, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the row's stores are complete before it is counted
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t before = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    last = before + 1 == static_cast<uint32_t>(N);
+    if (last) __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!last) return;
+  select_and_page<true>(sh, logits, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
+                        master_base, master_stride, shared_dev, has_shared, plan, stats);
+}
+
 }  // namespace
+
+hipError_t launch_route_page(const float* wr, const void* x, int x_dtype, int d, float* logits, uint32_t* arrive, int T,
+                             int N, int k, int route, int n_groups, int topk_groups, int32_t* idx, float* w,
+                             int32_t* pi, int32_t* pinv, uint64_t* tau, uint64_t* clock, int C,
+                             const uint64_t* slot_ptr, const uint8_t* master_base, uint64_t master_stride,
+                             const uint8_t* shared_dev, int has_shared, FfnBatch* plan, uint32_t* stats,
+                             hipStream_t st, const LaunchTiming& tm) {
+  if (T < 1 || T > 4 || N > 256 || C > 256 || k > 8 || T * k > 32 || T * k > C || d % 4 != 0 ||
+      T * k + (has_shared ? 1 : 0) > kMaxItems)
+    return hipErrorInvalidValue;
+  if (x_dtype == DT_F32)
+    hipExtLaunchKernelGGL(route_page_kernel<DT_F32>, dim3(N), dim3(256), 0, st, tm.start, tm.stop, 0, wr, x, d, logits,
+                          arrive, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C, slot_ptr,
+                          master_base, master_stride, shared_dev, has_shared, plan, stats);
+  else
+    hipExtLaunchKernelGGL(route_page_kernel<DT_BF16>, dim3(N), dim3(256), 0, st, tm.start, tm.stop, 0, wr, x, d,
+                          logits, arrive, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
+                          slot_ptr, master_base, master_stride, shared_dev, has_shared, plan, stats);
+  return hipGetLastError();
+}
 
 hipError_t launch_select_page(const float* logits, int T, int N, int k, int route, int n_groups, int topk_groups,
                               int32_t* idx, float* w, int32_t* pi, int32_t* pinv, uint64_t* tau, uint64_t* clock,

@@ -12,60 +12,24 @@
 #include <cmath>
 
 #include "kernels.hpp"
+#include "router_row.hpp"
 #include "select.hpp"
 
 namespace wisp {
 namespace {
 
-template <int XT>
-__device__ __forceinline__ float4 load_x4(const void* x, size_t idx) {
-  if constexpr (XT == DT_F32) {
-    return *reinterpret_cast<const float4*>(static_cast<const float*>(x) + idx);
-  } else {
-    const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(x) + idx);
-    return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u),
-                       __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xFFFF0000u));
-  }
-}
-
-// Decode-sized logits: one workgroup per expert row; 256 threads split the row (16-byte loads),
-// reduce through shuffles and LDS.  Up to four tokens per pass.
+// Decode-sized logits: one workgroup per expert row (router_row in router_row.hpp), up to four
+// tokens per pass.
 template <int XT>
 __global__ void __launch_bounds__(256) router_logits_wide_kernel(const float* __restrict__ wr,
                                                                  const void* __restrict__ x, int T, int N, int d,
                                                                  float* __restrict__ logits) {
   __shared__ float part[4][4];
   const int e = blockIdx.x;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const float4* row = reinterpret_cast<const float4*>(wr + static_cast<size_t>(e) * d);
-  const int chunks = d / 4;
   for (int t0 = 0; t0 < T; t0 += 4) {
     const int ntok = min(4, T - t0);
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int c = threadIdx.x; c < chunks; c += 256) {
-      const float4 w = row[c];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        if (t >= ntok) break;
-        const float4 v = load_x4<XT>(x, static_cast<size_t>(t0 + t) * d + static_cast<size_t>(c) * 4);
-        acc[t] = fmaf(w.x, v.x, acc[t]);
-        acc[t] = fmaf(w.y, v.y, acc[t]);
-        acc[t] = fmaf(w.z, v.z, acc[t]);
-        acc[t] = fmaf(w.w, v.w, acc[t]);
-      }
-    }
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      if (t >= ntok) break;
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) acc[t] += __shfl_xor(acc[t], off, 64);
-      if (lane == 0) part[t][wave] = acc[t];
-    }
-    __syncthreads();
-    if (threadIdx.x < ntok) {
-      const int t = threadIdx.x;
-      logits[static_cast<size_t>(t0 + t) * N + e] = (part[t][0] + part[t][1]) + (part[t][2] + part[t][3]);
-    }
+    const float z = router_row<XT>(wr, x, t0, ntok, d, e, part);
+    if (threadIdx.x < ntok) logits[static_cast<size_t>(t0 + threadIdx.x) * N + e] = z;
     __syncthreads();
   }
 }

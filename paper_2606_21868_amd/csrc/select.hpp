@@ -37,7 +37,9 @@ __device__ __forceinline__ float sel_sigmoid(float z) { return 1.0f / (1.0f + __
 // Tokens t0 .. t0+3 (those < T) of logits [T, N]; all 256 threads must call it.  Thread e owns
 // expert e of every token (N <= 256).  A key packs the order-preserving bits of the logit above
 // 255 - id, so (logit desc, id asc) is plain unsigned order and every allowed key is distinct:
-// the rank of an expert is the number of larger keys.
+// the rank of an expert is the number of larger keys.  COHERENT: the logits were written by other
+// workgroups of the running kernel, so they are read at device scope.
+template <bool COHERENT = false>
 __device__ __forceinline__ void select_tokens(const float* __restrict__ logits, int t0, int T, int N, int k, int route,
                                               int n_groups, int topk_groups, SelectShared& sh) {
   const int tid = threadIdx.x;
@@ -46,7 +48,9 @@ __device__ __forceinline__ void select_tokens(const float* __restrict__ logits, 
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     if (t >= nt) break;
-    const float z = e < N ? logits[static_cast<size_t>(t0 + t) * N + e] : 0.f;
+    const float* zp = logits + static_cast<size_t>(t0 + t) * N + e;
+    float z = 0.f;
+    if (e < N) z = COHERENT ? __hip_atomic_load(zp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : *zp;
     sh.z[t][e] = z;
     sh.key[t][e] = e < N ? (static_cast<uint64_t>(order_key(z)) << 32) | static_cast<uint32_t>(255 - e) : 0ull;
   }

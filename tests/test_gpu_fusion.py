@@ -1,9 +1,11 @@
-"""GPU tests of the down projection fused with the gate-weighted combine (single-token steps).
+"""GPU tests of the fused decode kernels: the down projection fused with the gate-weighted combine
+(single-token steps, both pagers) and the device pager's router logits fused with its selection and
+Algorithm 1.
 
-The same decode steps run with the fused down+combine kernel and with the separate down and combine
-kernels, from cold tables at the same cap, on both pagers: outputs must be bit-identical (the fused
-kernel computes every row and the combine with the same operations in the same order), the fused
-kernel must be the one that ran, and the fused outputs are checked against the oracle.
+The same decode steps run with the fused kernels and with the separate ones, from cold tables at the
+same cap: routing, gates, paging decisions and outputs must be bit-identical (the fused kernels
+compute every logit, row and sum with the same operations in the same order), the fused kernel must
+be the one that ran, and the fused outputs are checked against the oracle.
 """
 import numpy as np
 import pytest
@@ -55,6 +57,8 @@ def test_fused_matches_separate_kernels_and_oracle(shape, cap, steps):
         if cap >= wl.k:
             dev = _decode(run, True, wisp.PAGER_DEVICE)
             assert dev["fused_launches"] == steps * wl.L and dev["combine_launches"] == 0
+            assert np.array_equal(dev["idx"], sep["idx"]) and np.array_equal(dev["w"].view(np.uint32), sep["w"].view(np.uint32))
+            assert np.array_equal(dev["hits"], sep["hits"]) and np.array_equal(dev["misses"], sep["misses"])
             assert np.array_equal(dev["y"].view(np.uint32), sep["y"].view(np.uint32)), "device pager: bits differ"
             sep_dev = _decode(run, False, wisp.PAGER_DEVICE)
             assert sep_dev["fused_launches"] == 0
