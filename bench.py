@@ -476,6 +476,8 @@ def main():
                                  else None)
         return tab
 
+    census_faults = {}
+
     def census(pager):
         # every class timed, on steps after the timed region (the events slow the path, so these
         # steps are not part of any throughput)
@@ -484,9 +486,26 @@ def main():
         run.ctx.set_pager(pager)
         run.ctx.reset_kernel_times()
         run.ctx.set_profiling(True)
-        run.decode(record=False, steps=min(args.census_steps, total), start=0)
+        o = run.decode(record=False, steps=min(args.census_steps, total), start=0)
         run.ctx.set_profiling(0)
+        census_faults[pager] = o
         return kernel_table()
+
+    def device_ffn_roofline(tab):
+        # the device pager's gate/up kernel reads resident experts from HBM and streams faulted ones
+        # over the host link: its floor is hit bytes / HBM peak + fault bytes / measured link, per launch
+        o = census_faults.get(wisp.PAGER_DEVICE)
+        g = tab.get("ffn_gateup")
+        if o is None or not g:
+            return None
+        gate_bytes = 2 * wl.d * wl.I * (2 if wl.w_dtype == wisp.BF16 else 4)
+        t_roof = (float(o["hits"].sum()) * gate_bytes / (HBM_PEAK_GBPS * 1e9) +
+                  float(o["misses"].sum()) * wl.blob / (link * 1e9))
+        t_meas = g["total_ms"] * 1e-3
+        return dict(kernel="ffn_gateup_dev (resident experts from HBM, faulted ones streamed from pinned host memory)",
+                    bound="hbm+link", launches=g["launches"], avg_launch_us=g["avg_us"], t_roof_s=t_roof,
+                    t_measured_s=t_meas, frac=t_roof / t_meas, link_GBps_measured=link, hbm_peak_GBps=HBM_PEAK_GBPS,
+                    source="census steps (every kernel class event-timed)")
 
     mask = {"gateup": 1 << wisp.K_FFN_GATEUP, "all": True, "none": 0}[args.kernel_timing]
     passes = {}
@@ -510,6 +529,7 @@ def main():
         el, out = timed_pass(wisp.PAGER_DEVICE, 0)
         passes["device"] = dict(tokens_per_s=wl.T * steps / el, ms_per_step=el / steps * 1e3,
                                 path_roofline=path_roofline(el, out), kernel_census=census(wisp.PAGER_DEVICE))
+        passes["device"]["ffn_roofline"] = device_ffn_roofline(passes["device"]["kernel_census"])
         log(f"device pager: {steps} steps in {el:.3f} s -> {wl.T * steps / el:.2f} tokens/s, "
             f"{passes['device']['path_roofline']['frac']:.3f} of the path roofline")
     main_pass = "device" if "device" in passes else "host"

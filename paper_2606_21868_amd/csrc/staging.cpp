@@ -74,7 +74,9 @@ BounceRing::~BounceRing() {
 hipError_t BounceRing::init(int threads) {
   for (int i = 0; i < kBuffers; ++i) {
     void* p = nullptr;
-    hipError_t e = hipHostMalloc(&p, kPieceBytes, hipHostMallocDefault);
+    // coherent (snooped) pinned memory: the host threads write a piece with ordinary stores right
+    // before the DMA engine reads it, so its reads must see the CPU caches
+    hipError_t e = hipHostMalloc(&p, kPieceBytes, hipHostMallocCoherent);
     if (e != hipSuccess) return e;
     buf_[i] = static_cast<uint8_t*>(p);
     e = hipEventCreateWithFlags(&ev_[i], hipEventDisableTiming);

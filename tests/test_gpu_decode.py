@@ -51,6 +51,14 @@ def test_qwen3_decode_full_size_sampled():
     _run_case(wl, wl.cap, wl.steps, sample_points=pts)
 
 
+@pytest.mark.parametrize("T", [1, 4])
+def test_mixtral_widths_pinned_one_layer(T):
+    # the Mixtral widths (d=4096, I=14336: 28 16-byte loads per lane in the down rows) on one layer
+    # with pinned masters; T = 1 runs the single-token kernels at these widths, T = 4 the chunked path
+    wl = WORKLOADS["mixtral-8x7b-decode"].with_(L=1, T=T)
+    _run_case(wl, 2, 6, check_all_outputs=True)
+
+
 def test_mixtral_decode_full_size_sampled():
     """The Mixtral-8x7B-shaped workload at full size (32 layers x 8 experts of 352 MB, 90.2 GB of
     masters, batch 4, C = 2): unions of up to 8 experts per layer-step against 2 slots, so every
