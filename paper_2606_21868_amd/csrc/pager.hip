@@ -27,8 +27,8 @@ struct PagerShared {
   uint64_t tau[256];
   uint64_t slot[256];
   uint64_t clock;
+  uint64_t vkey[256];    // victim order key (tau << 8 | slot) of a candidate slot, ~0 otherwise
   uint8_t in_r[256];
-  uint8_t cand[256];
   int32_t hits[32], hslot[32], faults[32], fslot[32], victim[32];
   int32_t nh, nf;
 };
@@ -89,19 +89,28 @@ __device__ __forceinline__ void select_and_page(
     }
     if (lane == 0) { sh.nh = nh; sh.nf = nf; }
   }
-  if (tid < C) {
-    const int occ = sh.pinv[tid];
-    sh.cand[tid] = occ < 0 || !sh.in_r[occ];
+  // (tau, slot) packed into one key per slot (a tick never reaches 2^56 and slots are < 256), so the
+  // victim order is plain unsigned order; non-candidates, and the padding up to a multiple of 16,
+  // get the largest key
+  const int c_pad = (C + 15) & ~15;
+  if (tid < c_pad) {
+    const int occ = tid < C ? sh.pinv[tid] : 0;
+    const bool cand = tid < C && (occ < 0 || !sh.in_r[occ]);
+    sh.vkey[tid] = cand ? (sh.tau[tid] << 8) | static_cast<uint64_t>(tid) : ~0ull;
   }
   __syncthreads();
   const int nh = sh.nh, nf = sh.nf;
-  // victims: the nf smallest (tau, slot) among the candidates, by ranks
-  if (nf > 0 && tid < C && sh.cand[tid]) {
-    const uint64_t ts = sh.tau[tid];
-    int rank = 0;
-#pragma unroll 8
-    for (int s2 = 0; s2 < C; ++s2) rank += (sh.cand[s2] && (sh.tau[s2] < ts || (sh.tau[s2] == ts && s2 < tid))) ? 1 : 0;
-    if (rank < nf) sh.victim[rank] = tid;
+  // victims: the nf smallest keys among the candidates, by ranks (branch-free broadcast reads)
+  if (nf > 0 && tid < C) {
+    const uint64_t kt = sh.vkey[tid];
+    if (kt != ~0ull) {
+      int rank = 0;
+      for (int s2 = 0; s2 < c_pad; s2 += 16) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) rank += sh.vkey[s2 + q] < kt ? 1 : 0;
+      }
+      if (rank < nf) sh.victim[rank] = tid;
+    }
   }
   __syncthreads();
   // fault i takes victim i (the victim's occupant leaves the map); every expert of R gets c + 1

@@ -33,16 +33,30 @@ __device__ __forceinline__ float router_row(const float* __restrict__ wr, const 
   const float4* row = reinterpret_cast<const float4*>(wr + static_cast<size_t>(e) * d);
   const int chunks = d / 4;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int c = threadIdx.x; c < chunks; c += 256) {
-    const float4 w = row[c];
+  // the thread's chunks c = tid, tid + 256, ... in groups of U whose row loads are all issued before
+  // the first FMA (one HBM round trip per group, not per chunk); each acc[t] is still one FMA chain
+  // in ascending chunk order
+  constexpr int U = 4;
+  for (int c0 = threadIdx.x; c0 < chunks; c0 += 256 * U) {
+    float4 w[U];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      if (t >= ntok) break;
-      const float4 v = load_x4<XT>(x, static_cast<size_t>(t0 + t) * d + static_cast<size_t>(c) * 4);
-      acc[t] = fmaf(w.x, v.x, acc[t]);
-      acc[t] = fmaf(w.y, v.y, acc[t]);
-      acc[t] = fmaf(w.z, v.z, acc[t]);
-      acc[t] = fmaf(w.w, v.w, acc[t]);
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * 256;
+      w[u] = c < chunks ? row[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * 256;
+      if (c >= chunks) break;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        if (t >= ntok) break;
+        const float4 v = load_x4<XT>(x, static_cast<size_t>(t0 + t) * d + static_cast<size_t>(c) * 4);
+        acc[t] = fmaf(w[u].x, v.x, acc[t]);
+        acc[t] = fmaf(w[u].y, v.y, acc[t]);
+        acc[t] = fmaf(w[u].z, v.z, acc[t]);
+        acc[t] = fmaf(w[u].w, v.w, acc[t]);
+      }
     }
   }
 #pragma unroll
