@@ -12,10 +12,12 @@
 // lands in the per-(token, rank) rows that the combine reads.
 //
 // Tiles: 64 rows x 64 h-columns for gate/up (the B tile holds the matching 64 rows of W1 and of
-// W3, so SwiGLU is applied in registers), 64 rows x 128 columns for down; K in steps of 32 through
-// double-buffered LDS with padded rows.  Four waves per workgroup, each a 32-row slab of the tile
-// on v_mfma_f32_32x32x16_bf16 (A lane l holds row l%32, k 8*(l/32)..+7; B lane l holds column l%32,
-// same k; D lane l holds column l%32, rows 8*(r/4) + 4*(l/32) + r%4).  Every output element is one
+// W3, so SwiGLU is applied in registers), 64 rows x 128 columns for down; K in stages of 64 through
+// one LDS buffer with padded rows, the next stage loaded into registers meanwhile (Stage below),
+// five workgroups per CU so that a launch's tiles are all resident at once.  Four waves per
+// workgroup, each a 32-row slab of the tile on v_mfma_f32_32x32x16_bf16 (A lane l holds row l%32,
+// k 8*(l/32)..+7; B lane l holds column l%32, same k; D lane l holds column l%32, rows
+// 8*(r/4) + 4*(l/32) + r%4).  Every output element is one
 // fixed-order reduction over K, independent of where its row sits in a tile or which launch holds
 // its expert, so paged and fully resident runs give identical bits.
 #include <hip/hip_ext.h>
@@ -28,12 +30,13 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));   // a plain vector: stays in registers
 
 constexpr int GM = 64;          // rows (pairs) per tile
-constexpr int GK = 32;          // K per LDS stage
-constexpr int GLD = GK + 8;     // padded LDS row, bf16 elements (80 bytes: conflict-free 16-byte reads)
 constexpr int GN_UP = 64;       // h columns per gate/up tile
 constexpr int GN_DOWN = 128;    // output columns per down tile
+constexpr int KS_UP = 64;       // K per LDS stage, gate/up (K = d): 27 KB of LDS per workgroup
+constexpr int KS_DOWN = 64;     // K per LDS stage, down (K = I)
 
 __device__ __forceinline__ uint16_t bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
@@ -118,12 +121,51 @@ __global__ void __launch_bounds__(1024) permute_pairs_kernel(const int32_t* __re
   }
 }
 
+// One K stage of a 64-row A tile and a 128-row B tile through LDS.  A thread loads 16-byte pieces
+// of TPR-thread row segments (KS bf16 = 2*KS contiguous bytes of a row per stage: whole 128-byte
+// lines for KS = 64).  The next stage's pieces are loaded into registers while the current stage
+// computes from LDS; LDS holds one stage (rows padded by 16 bytes: the 16-byte reads of 16
+// consecutive rows hit distinct banks).
+template <int KS>
+struct Stage {
+  static constexpr int TPR = KS * 2 / 16;     // threads per row segment
+  static constexpr int RPI = 256 / TPR;       // rows per load instruction
+  static constexpr int AL = GM / RPI;         // A loads per thread
+  static constexpr int BL = 128 / RPI;        // B loads per thread
+  static constexpr int LDK = KS + 8;          // LDS row stride, bf16 elements
+};
+
+template <int KS>
+__device__ __forceinline__ void stage_load(const uint16_t* const* a_ptr, const uint16_t* const* b_ptr, int kb,
+                                           u32x4_t* ra, u32x4_t* rb) {
+  // every load is unconditional (an A row past the expert's rows reads a valid row, zeroed when it is
+  // stored), so the loads issue back to back and nothing waits for them before the stage's MFMAs
+#pragma unroll
+  for (int i = 0; i < Stage<KS>::AL; ++i) ra[i] = *reinterpret_cast<const u32x4_t*>(a_ptr[i] + kb);
+#pragma unroll
+  for (int i = 0; i < Stage<KS>::BL; ++i) rb[i] = *reinterpret_cast<const u32x4_t*>(b_ptr[i] + kb);
+}
+
+template <int KS>
+__device__ __forceinline__ void stage_store(uint16_t* As, uint16_t* Bs, int tr, int tq, const bool* a_ok,
+                                            const u32x4_t* ra, const u32x4_t* rb) {
+  using S = Stage<KS>;
+#pragma unroll
+  for (int i = 0; i < S::AL; ++i)
+    *reinterpret_cast<u32x4_t*>(&As[(tr + S::RPI * i) * S::LDK + tq]) = a_ok[i] ? ra[i] : u32x4_t{0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int i = 0; i < S::BL; ++i) *reinterpret_cast<u32x4_t*>(&Bs[(tr + S::RPI * i) * S::LDK + tq]) = rb[i];
+}
+
 // H rows [off_g + m0, +64) x h columns [c0, +64) of one expert: silu(X W1^T) * (X W3^T) -> bf16.
-__global__ void __launch_bounds__(256) grouped_gateup_kernel(GroupedBatch gb, const uint16_t* __restrict__ x,
+// The B tile's rows 0..63 are W1 rows c0.., rows 64..127 the W3 rows of the same columns.
+template <int KS>
+__global__ void __launch_bounds__(256, 5) grouped_gateup_kernel(GroupedBatch gb, const uint16_t* __restrict__ x,
                                                              const int32_t* __restrict__ perm, int k, int d, int I,
                                                              uint16_t* __restrict__ hs) {
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][GM * GLD];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][2 * GN_UP * GLD];
+  using S = Stage<KS>;
+  __shared__ __attribute__((aligned(16))) uint16_t As[GM * S::LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * GN_UP * S::LDK];
   int g, mt, ct;
   tile_of(gb, I / GN_UP, g, mt, ct);
   const int rows = gb.rows[g], base = gb.row_off[g];
@@ -131,47 +173,45 @@ __global__ void __launch_bounds__(256) grouped_gateup_kernel(GroupedBatch gb, co
   const uint16_t* W1 = reinterpret_cast<const uint16_t*>(gb.w[g]);
   const uint16_t* W3 = W1 + static_cast<size_t>(I) * d;
   const int tid = threadIdx.x;
-  const int lr = tid >> 2, lk = (tid & 3) * 8;   // load row (0..63) and k offset of this thread
-  const bool a_ok = m0 + lr < rows;
-  const uint16_t* a_src = x;
-  if (a_ok) a_src = x + static_cast<size_t>(perm[base + m0 + lr] / k) * d + lk;
-  const uint16_t* g_src = W1 + static_cast<size_t>(c0 + lr) * d + lk;
-  const uint16_t* u_src = W3 + static_cast<size_t>(c0 + lr) * d + lk;
-  uint4 ra = make_uint4(0u, 0u, 0u, 0u), rg, ru;
+  const int tr = tid / S::TPR, tq = (tid % S::TPR) * 8;
+  const uint16_t* a_ptr[S::AL];
+  bool a_ok[S::AL];
+#pragma unroll
+  for (int i = 0; i < S::AL; ++i) {
+    const int r = m0 + tr + S::RPI * i;
+    a_ok[i] = r < rows;
+    a_ptr[i] = x + (a_ok[i] ? static_cast<size_t>(perm[base + r] / k) * d : 0) + tq;
+  }
+  const uint16_t* b_ptr[S::BL];
+#pragma unroll
+  for (int i = 0; i < S::BL; ++i) {
+    const int j = tr + S::RPI * i;     // B tile row
+    b_ptr[i] = (j < GN_UP ? W1 + static_cast<size_t>(c0 + j) * d : W3 + static_cast<size_t>(c0 + j - GN_UP) * d) + tq;
+  }
   const int wave = tid >> 6, lane = tid & 63, wm = wave >> 1, wn = wave & 1;
   const int fr = lane & 31, fk = (lane >> 5) * 8;
   f32x16_t accg = {}, accu = {};
-  const int nk = d / GK;
-  if (a_ok) ra = *reinterpret_cast<const uint4*>(a_src);
-  rg = *reinterpret_cast<const uint4*>(g_src);
-  ru = *reinterpret_cast<const uint4*>(u_src);
-  *reinterpret_cast<uint4*>(&As[0][lr * GLD + lk]) = ra;
-  *reinterpret_cast<uint4*>(&Bs[0][lr * GLD + lk]) = rg;
-  *reinterpret_cast<uint4*>(&Bs[0][(GN_UP + lr) * GLD + lk]) = ru;
+  const int nk = d / KS;
+  u32x4_t ra[S::AL], rb[S::BL];
+  stage_load<KS>(a_ptr, b_ptr, 0, ra, rb);
+  stage_store<KS>(As, Bs, tr, tq, a_ok, ra, rb);
   __syncthreads();
   for (int s = 0; s < nk; ++s) {
-    const int cur = s & 1;
     const bool more = s + 1 < nk;
-    if (more) {
-      const int kb = (s + 1) * GK;
-      if (a_ok) ra = *reinterpret_cast<const uint4*>(a_src + kb);
-      rg = *reinterpret_cast<const uint4*>(g_src + kb);
-      ru = *reinterpret_cast<const uint4*>(u_src + kb);
-    }
+    if (more) stage_load<KS>(a_ptr, b_ptr, (s + 1) * KS, ra, rb);
 #pragma unroll
-    for (int kk = 0; kk < GK; kk += 16) {
-      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&As[cur][(wm * 32 + fr) * GLD + kk + fk]);
-      const bf16x8_t bg = *reinterpret_cast<const bf16x8_t*>(&Bs[cur][(wn * 32 + fr) * GLD + kk + fk]);
-      const bf16x8_t bu = *reinterpret_cast<const bf16x8_t*>(&Bs[cur][(GN_UP + wn * 32 + fr) * GLD + kk + fk]);
+    for (int kk = 0; kk < KS; kk += 16) {
+      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&As[(wm * 32 + fr) * S::LDK + kk + fk]);
+      const bf16x8_t bg = *reinterpret_cast<const bf16x8_t*>(&Bs[(wn * 32 + fr) * S::LDK + kk + fk]);
+      const bf16x8_t bu = *reinterpret_cast<const bf16x8_t*>(&Bs[(GN_UP + wn * 32 + fr) * S::LDK + kk + fk]);
       accg = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bg, accg, 0, 0, 0);
       accu = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bu, accu, 0, 0, 0);
     }
     if (more) {
-      *reinterpret_cast<uint4*>(&As[cur ^ 1][lr * GLD + lk]) = ra;
-      *reinterpret_cast<uint4*>(&Bs[cur ^ 1][lr * GLD + lk]) = rg;
-      *reinterpret_cast<uint4*>(&Bs[cur ^ 1][(GN_UP + lr) * GLD + lk]) = ru;
+      __syncthreads();
+      stage_store<KS>(As, Bs, tr, tq, a_ok, ra, rb);
+      __syncthreads();
     }
-    __syncthreads();
   }
   const int hc = c0 + wn * 32 + fr;
 #pragma unroll
@@ -187,57 +227,55 @@ __global__ void __launch_bounds__(256) grouped_gateup_kernel(GroupedBatch gb, co
 
 // O rows of one expert x output columns [c0, +128): H W2^T in fp32, scattered to the rows
 // t*(k+1) + j of the pairs.
-__global__ void __launch_bounds__(256) grouped_down_kernel(GroupedBatch gb, const uint16_t* __restrict__ hs,
+template <int KS>
+__global__ void __launch_bounds__(256, 5) grouped_down_kernel(GroupedBatch gb, const uint16_t* __restrict__ hs,
                                                            const int32_t* __restrict__ perm, int k, int d, int I,
                                                            float* __restrict__ buf) {
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][GM * GLD];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][GN_DOWN * GLD];
+  using S = Stage<KS>;
+  __shared__ __attribute__((aligned(16))) uint16_t As[GM * S::LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[GN_DOWN * S::LDK];
   int g, mt, ct;
   tile_of(gb, d / GN_DOWN, g, mt, ct);
   const int rows = gb.rows[g], base = gb.row_off[g];
   const int m0 = mt * GM, c0 = ct * GN_DOWN;
   const uint16_t* W2 = reinterpret_cast<const uint16_t*>(gb.w[g]) + 2 * static_cast<size_t>(I) * d;
   const int tid = threadIdx.x;
-  const int lr = tid >> 2, lk = (tid & 3) * 8;
-  const bool a_ok = m0 + lr < rows;
-  const uint16_t* a_src = hs + static_cast<size_t>(a_ok ? base + m0 + lr : 0) * I + lk;
-  const uint16_t* b0_src = W2 + static_cast<size_t>(c0 + lr) * I + lk;
-  const uint16_t* b1_src = W2 + static_cast<size_t>(c0 + 64 + lr) * I + lk;
-  uint4 ra = make_uint4(0u, 0u, 0u, 0u), rb0, rb1;
+  const int tr = tid / S::TPR, tq = (tid % S::TPR) * 8;
+  const uint16_t* a_ptr[S::AL];
+  bool a_ok[S::AL];
+#pragma unroll
+  for (int i = 0; i < S::AL; ++i) {
+    const int r = m0 + tr + S::RPI * i;
+    a_ok[i] = r < rows;
+    a_ptr[i] = hs + static_cast<size_t>(a_ok[i] ? base + r : 0) * I + tq;
+  }
+  const uint16_t* b_ptr[S::BL];
+#pragma unroll
+  for (int i = 0; i < S::BL; ++i) b_ptr[i] = W2 + static_cast<size_t>(c0 + tr + S::RPI * i) * I + tq;
   const int wave = tid >> 6, lane = tid & 63, wm = wave >> 1, wn = wave & 1;
   const int fr = lane & 31, fk = (lane >> 5) * 8;
   f32x16_t acc0 = {}, acc1 = {};
-  const int nk = I / GK;
-  if (a_ok) ra = *reinterpret_cast<const uint4*>(a_src);
-  rb0 = *reinterpret_cast<const uint4*>(b0_src);
-  rb1 = *reinterpret_cast<const uint4*>(b1_src);
-  *reinterpret_cast<uint4*>(&As[0][lr * GLD + lk]) = ra;
-  *reinterpret_cast<uint4*>(&Bs[0][lr * GLD + lk]) = rb0;
-  *reinterpret_cast<uint4*>(&Bs[0][(64 + lr) * GLD + lk]) = rb1;
+  const int nk = I / KS;
+  u32x4_t ra[S::AL], rb[S::BL];
+  stage_load<KS>(a_ptr, b_ptr, 0, ra, rb);
+  stage_store<KS>(As, Bs, tr, tq, a_ok, ra, rb);
   __syncthreads();
   for (int s = 0; s < nk; ++s) {
-    const int cur = s & 1;
     const bool more = s + 1 < nk;
-    if (more) {
-      const int kb = (s + 1) * GK;
-      if (a_ok) ra = *reinterpret_cast<const uint4*>(a_src + kb);
-      rb0 = *reinterpret_cast<const uint4*>(b0_src + kb);
-      rb1 = *reinterpret_cast<const uint4*>(b1_src + kb);
-    }
+    if (more) stage_load<KS>(a_ptr, b_ptr, (s + 1) * KS, ra, rb);
 #pragma unroll
-    for (int kk = 0; kk < GK; kk += 16) {
-      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&As[cur][(wm * 32 + fr) * GLD + kk + fk]);
-      const bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(&Bs[cur][(wn * 64 + fr) * GLD + kk + fk]);
-      const bf16x8_t b1 = *reinterpret_cast<const bf16x8_t*>(&Bs[cur][(wn * 64 + 32 + fr) * GLD + kk + fk]);
+    for (int kk = 0; kk < KS; kk += 16) {
+      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&As[(wm * 32 + fr) * S::LDK + kk + fk]);
+      const bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(&Bs[(wn * 64 + fr) * S::LDK + kk + fk]);
+      const bf16x8_t b1 = *reinterpret_cast<const bf16x8_t*>(&Bs[(wn * 64 + 32 + fr) * S::LDK + kk + fk]);
       acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b0, acc0, 0, 0, 0);
       acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b1, acc1, 0, 0, 0);
     }
     if (more) {
-      *reinterpret_cast<uint4*>(&As[cur ^ 1][lr * GLD + lk]) = ra;
-      *reinterpret_cast<uint4*>(&Bs[cur ^ 1][lr * GLD + lk]) = rb0;
-      *reinterpret_cast<uint4*>(&Bs[cur ^ 1][(64 + lr) * GLD + lk]) = rb1;
+      __syncthreads();
+      stage_store<KS>(As, Bs, tr, tq, a_ok, ra, rb);
+      __syncthreads();
     }
-    __syncthreads();
   }
   const int oc = c0 + wn * 64 + fr;
 #pragma unroll
@@ -256,7 +294,7 @@ __global__ void __launch_bounds__(256) grouped_down_kernel(GroupedBatch gb, cons
 
 bool grouped_supported(const FfnShape& s, int has_shared) {
   return !has_shared && s.blob.w_dtype == DT_BF16 && s.x_dtype == DT_BF16 && s.h_dtype == DT_BF16 &&
-         s.blob.d % GN_DOWN == 0 && s.blob.I % GN_UP == 0 && s.blob.d % GK == 0 && s.blob.I % GK == 0;
+         s.blob.d % GN_DOWN == 0 && s.blob.I % GN_UP == 0 && s.blob.d % KS_UP == 0 && s.blob.I % KS_DOWN == 0;
 }
 
 int grouped_row_tiles(int rows) { return (rows + GM - 1) / GM; }
@@ -275,7 +313,7 @@ hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const
   if (b.n_groups <= 0) return hipSuccess;
   if (b.n_groups > kMaxGroups || !grouped_supported(s, 0)) return hipErrorInvalidValue;
   const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.I / GN_UP);
-  hipExtLaunchKernelGGL(grouped_gateup_kernel, dim3(tiles), dim3(256), 0, st, tm.start, tm.stop, 0, b,
+  hipExtLaunchKernelGGL(grouped_gateup_kernel<KS_UP>, dim3(tiles), dim3(256), 0, st, tm.start, tm.stop, 0, b,
                         static_cast<const uint16_t*>(x), perm, k, s.blob.d, s.blob.I, static_cast<uint16_t*>(hs));
   return hipGetLastError();
 }
@@ -285,7 +323,7 @@ hipError_t launch_grouped_down(const GroupedBatch& b, const FfnShape& s, const v
   if (b.n_groups <= 0) return hipSuccess;
   if (b.n_groups > kMaxGroups || !grouped_supported(s, 0)) return hipErrorInvalidValue;
   const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.d / GN_DOWN);
-  hipExtLaunchKernelGGL(grouped_down_kernel, dim3(tiles), dim3(256), 0, st, tm.start, tm.stop, 0, b,
+  hipExtLaunchKernelGGL(grouped_down_kernel<KS_DOWN>, dim3(tiles), dim3(256), 0, st, tm.start, tm.stop, 0, b,
                         static_cast<const uint16_t*>(hs), perm, k, s.blob.d, s.blob.I, buf);
   return hipGetLastError();
 }
