@@ -647,8 +647,7 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   std::memset(c->idx_tagged, 0, sizeof(uint64_t) * static_cast<size_t>(T) * k);
   c->ids_scratch.resize(static_cast<size_t>(T) * k);
   const size_t pairs_bytes = sizeof(int32_t) * static_cast<size_t>(T) * k;
-  // coherent: written by the host right before each DMA copy to the device
-  if (hipHostMalloc(&p, pairs_bytes, hipHostMallocCoherent) != hipSuccess) return bail(WISP_E_NOMEM, "pinned scratch");
+  if (hipHostMalloc(&p, pairs_bytes, hipHostMallocDefault) != hipSuccess) return bail(WISP_E_NOMEM, "pinned scratch");
   c->ids_up = static_cast<int32_t*>(p);
   if (hipMalloc(&p, pairs_bytes) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
   c->d_ids = static_cast<int32_t*>(p);

@@ -127,8 +127,52 @@ def check_outputs(run, y_gpu, points, ora_idx=None, threads=None, tokens=None):
         el = np.abs(yg - y) / np.maximum(np.abs(y), 1e-6 * scale[:, None])
         worst = max(worst, float(row_err.max()))
         worst_el = max(worst_el, float(el.max()))
+        if row_err.max() > tol:
+            for i, t in enumerate(tok.tolist()):
+                log(f"  step {s} layer {l} token {t}: experts {idx[i].tolist()} gates {np.round(g[i], 4).tolist()} "
+                    f"row-relative error {row_err[i]:.3e}")
         assert row_err.max() <= tol, f"step {s} layer {l}: row-relative error {row_err.max():.3e} > {tol}"
     return worst, worst_el
+
+
+def check_masters_unchanged(run, pairs):
+    """The master blobs of the (layer, expert) pairs still hold what the seeded generator wrote
+    (expert -1: the shared expert).  Reports the first differing 8-byte words of any that changed."""
+    from paper_2606_21868_amd import datagen as dg
+    wl = run.wl
+    changed = []
+    for l, e in sorted(set(pairs)):
+        got = run.master_blob(l, e)
+        want = dg.expert_blob(wl.seed, l, dg.SHARED_EXPERT if e < 0 else e, wl.w_dtype, wl.d, wl.I)[:got.size]
+        ne = np.flatnonzero(got != want)
+        if ne.size:
+            w0 = int(ne[0]) & ~7
+            changed.append((l, e, int(ne.size), int(ne[0]), int(ne[-1]), got[w0:w0 + 32].tobytes().hex(),
+                            want[w0:w0 + 32].tobytes().hex()))
+    for c in changed[:8]:
+        log(f"  master of layer {c[0]} expert {c[1]} changed: {c[2]} bytes in [{c[3]}, {c[4]}]; at the first: "
+            f"{c[5]} (generator: {c[6]})")
+    return changed
+
+
+def check_slots_hold_masters(run, max_bytes=4e9):
+    """Every resident slot holds its expert's master bytes (all slots when their bytes are at most
+    max_bytes, else 32 slots spread over the layers); returns the number checked."""
+    wl, cap = run.wl, run.ctx.cap()
+    pairs = [(l, s) for l in range(wl.L) for s in range(cap)]
+    if len(pairs) * run.blob_bytes > max_bytes:
+        pairs = [pairs[i] for i in np.linspace(0, len(pairs) - 1, 32).astype(int)]
+    n = 0
+    for l, s in pairs:
+        e = run.ctx.expert_in_slot(l, s)
+        if e < 0:
+            continue
+        got, want = run.ctx.read_slot(l, s, run.blob_bytes), run.master_blob(l, e)
+        ne = np.flatnonzero(got != want)
+        assert ne.size == 0, (f"layer {l} slot {s} expert {e}: {ne.size} bytes differ from the master "
+                              f"(first {int(ne[0])}, last {int(ne[-1])})")
+        n += 1
+    return n
 
 
 def run_case(wl, cap, steps, sample_points=None, check_all_outputs=False, tokens=None, expect_grouped=None,
@@ -181,9 +225,37 @@ def run_case(wl, cap, steps, sample_points=None, check_all_outputs=False, tokens
         else:
             points = [p for p in sample_points if p not in exempt]
         log(f"  outputs at {len(points)} (step, layer) points")
-        worst, worst_el = check_outputs(run, out["y"], points, ora_idx, tokens=tokens)
+        if pageable:
+            # the oracle reads the masters now, long after the fills copied them: check that they
+            # still hold the generator's bytes (up to 16 blobs used at the checked points)
+            first = sorted({(points[0][1], int(e)) for e in np.unique(ora_idx[points[0]])})
+            rest = sorted({(l, int(e)) for (st_, l) in points for e in np.unique(ora_idx[st_, l])} - set(first))
+            if wl.has_shared:
+                rest += sorted({(l, -1) for (_, l) in points})
+            n_rest = min(len(rest), max(0, 16 - len(first)))
+            used = first + [rest[i] for i in np.linspace(0, len(rest) - 1, n_rest).astype(int)] if n_rest else first
+            changed = check_masters_unchanged(run, used)
+            assert not changed, f"{len(changed)} pageable master blobs changed during the run"
+            log(f"  {len(used)} master blobs used at the checked points unchanged since generation")
+        try:
+            worst, worst_el = check_outputs(run, out["y"], points, ora_idx, tokens=tokens)
+        except AssertionError:
+            # replay the same steps from cold: a transient error (ordering) gives different bits, a
+            # reproducible one the same
+            run.ctx.masters_ready()
+            again = run.decode(record=True)
+            same = np.array_equal(again["y"].view(np.uint32), out["y"].view(np.uint32))
+            log(f"  replay from cold: outputs {'bit-identical to' if same else 'differ from'} the first run")
+            try:
+                check_outputs(run, again["y"], points, ora_idx, tokens=tokens)
+                log("  replay: every point within tolerance")
+            except AssertionError as e2:
+                log(f"  replay also fails: {e2}")
+            raise
         log(f"  worst row-relative error {worst:.3e} (elementwise {worst_el:.3e}); total misses "
             f"{int(out['misses'].sum())} of {int(out['hits'].sum() + out['misses'].sum())} references")
+        n_slots = check_slots_hold_masters(run)
+        log(f"  {n_slots} resident slots byte-equal to their masters")
         tables = [[run.ctx.slot_of(l, e) for e in range(wl.N)] for l in range(wl.L)]
         # the device pager: same trace from cold -> same decisions, same slots, same bits
         device_ok = cap >= wl.T * wl.k and wl.T <= 4 and not pageable

@@ -59,32 +59,6 @@ def test_mixtral_widths_pinned_one_layer(T):
     _run_case(wl, 2, 6, check_all_outputs=True)
 
 
-def test_mixtral_decode_full_size_sampled():
-    """The Mixtral-8x7B-shaped workload at full size (32 layers x 8 experts of 352 MB, 90.2 GB of
-    masters, batch 4, C = 2): unions of up to 8 experts per layer-step against 2 slots, so every
-    step is several chunked Algorithm 1 steps.  24 of its 256 steps (each moves ~42 GB over the host
-    link): all routing and paging decisions, outputs at sampled points, resident bit-identity.
-    The masters exceed the pinned memory a process may hold on the test machines (65 GiB), so they
-    are pageable and faults are staged through the bounce ring."""
-    wl = WORKLOADS["mixtral-8x7b-decode"]
-    steps = 24
-    pts = [(0, 0), (3, 9), (7, 31), (12, 16), (18, 4), (steps - 1, wl.L - 1)]
-    out = _run_case(wl, wl.cap, steps, sample_points=pts, pageable=True)
-    assert out["chunks"].max() > 1
-
-
-def test_deepseek_decode_full_size_sampled():
-    """The DeepSeek-V3-shaped workload at full size (16 layers x 256 fp8 experts + shared, 180.4 GB
-    of masters, C = 56 from the 40 GB budget), all 256 steps: all routing and
-    paging decisions, outputs at sampled points, resident bit-identity (C = N, 180 GB of slots).
-    Pageable masters (above the pinned-memory limit of the test machines), so the host pager only."""
-    wl = WORKLOADS["deepseek-v3-16l-decode"]
-    rng = np.random.default_rng(2)
-    pts = sorted({(int(s), int(l)) for s, l in zip(rng.integers(0, wl.steps, 6), rng.integers(0, wl.L, 6))})
-    pts += [(0, 0), (wl.steps - 1, wl.L - 1)]
-    _run_case(wl, wl.cap, wl.steps, sample_points=pts, pageable=True)
-
-
 def test_qwen3_layers_pageable_masters():
     # the staged fill path (pageable masters through the pinned bounce ring): same decisions and bits
     wl = WORKLOADS["qwen3-30b-a3b-decode"].with_(L=2)
