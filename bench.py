@@ -435,11 +435,17 @@ def main():
     run.ctx.set_fusion(not args.no_fusion)
 
     def timed_pass(pager, mask):
-        """Cold slot tables, `warmup` untimed steps, then the timed steps; returns (elapsed, stats)."""
+        """Cold slot tables, `warmup` untimed steps, then the timed steps; returns (elapsed, stats) of the
+        timed steps and (elapsed, stats) of the warmup steps, which start from the cold tables."""
         run.ctx.masters_ready()                       # every slot empty: each pass starts cold
         run.ctx.set_pager(pager)
+        warm = (0.0, None)
         if warmup:
-            run.decode(record=False, steps=warmup, start=0)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            w_out = run.decode(record=False, steps=warmup, start=0)
+            torch.cuda.synchronize()
+            warm = (time.perf_counter() - t0, w_out)
         run.ctx.reset_stats()
         run.ctx.reset_kernel_times()
         run.ctx.set_profiling(mask)
@@ -449,20 +455,33 @@ def main():
         torch.cuda.synchronize()
         el = time.perf_counter() - t1
         run.ctx.set_profiling(0)
-        return el, out
+        return el, out, warm
 
-    def path_roofline(elapsed, out):
+    def path_roofline(elapsed, out, n_steps=None):
+        n_steps = steps if n_steps is None else n_steps
         hits, misses = out["hits"], out["misses"]
         distinct = hits + misses
-        hbm_bytes = float(distinct.sum()) * wl.blob + wl.N * wl.d * 4 * wl.L * steps
+        hbm_bytes = float(distinct.sum()) * wl.blob + wl.N * wl.d * 4 * wl.L * n_steps
         link_bytes = float(misses.sum()) * wl.blob
         t_roof = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (link * 1e9)
         return dict(t_roof_s=t_roof, t_measured_s=elapsed, frac=t_roof / elapsed,
-                    roofline_tokens_per_s=wl.T * steps / t_roof, link_GBps_measured=link,
+                    roofline_tokens_per_s=wl.T * n_steps / t_roof, link_GBps_measured=link,
                     hbm_peak_GBps=HBM_PEAK_GBPS, device_copy_GBps_measured=hbm_copy,
-                    hbm_bytes_per_token=hbm_bytes / (wl.T * steps), link_bytes_per_token=link_bytes / (wl.T * steps),
-                    faults_per_token=float(misses.sum()) / (wl.T * steps),
+                    hbm_bytes_per_token=hbm_bytes / (wl.T * n_steps), link_bytes_per_token=link_bytes / (wl.T * n_steps),
+                    faults_per_token=float(misses.sum()) / (wl.T * n_steps),
                     fault_rate=float(misses.sum()) / float(distinct.sum()))
+
+    def all_steps(el, out, warm):
+        """Every step of the pass from the cold tables (compulsory faults included): the warmup steps
+        and the timed ones, each timed from its first route to its final device synchronisation."""
+        w_el, w_out = warm
+        if w_out is None:
+            return None
+        both = dict(hits=np.concatenate([w_out["hits"], out["hits"]]),
+                    misses=np.concatenate([w_out["misses"], out["misses"]]))
+        n = warmup + steps
+        return dict(steps=n, tokens_per_s=wl.T * n / (w_el + el),
+                    path_roofline=path_roofline(w_el + el, both, n))
 
     def kernel_table():
         tab = {}
@@ -511,11 +530,11 @@ def main():
     passes = {}
     roof = None
     if args.pager in ("both", "host"):
-        el, out = timed_pass(wisp.PAGER_HOST, mask)
+        el, out, warm = timed_pass(wisp.PAGER_HOST, mask)
         tk = kernel_table()
         passes["host"] = dict(tokens_per_s=wl.T * steps / el, ms_per_step=el / steps * 1e3,
-                              path_roofline=path_roofline(el, out), kernels_timed_region=tk,
-                              kernel_census=census(wisp.PAGER_HOST))
+                              path_roofline=path_roofline(el, out), all_steps=all_steps(el, out, warm),
+                              kernels_timed_region=tk, kernel_census=census(wisp.PAGER_HOST))
         log(f"host pager: {steps} steps in {el:.3f} s -> {wl.T * steps / el:.2f} tokens/s, "
             f"{passes['host']['path_roofline']['frac']:.3f} of the path roofline")
         if "ffn_gateup" in tk:
@@ -526,9 +545,10 @@ def main():
                         traffic_detail=tr, kernel="ffn_rows<bf16,bf16,gate/up> expert GEMV (W1+W3 rows), host-pager pass",
                         avg_launch_us=g["avg_us"], bytes_per_launch=g["bytes_per_launch"], launches=g["launches"])
     if args.pager in ("both", "device"):
-        el, out = timed_pass(wisp.PAGER_DEVICE, 0)
+        el, out, warm = timed_pass(wisp.PAGER_DEVICE, 0)
         passes["device"] = dict(tokens_per_s=wl.T * steps / el, ms_per_step=el / steps * 1e3,
-                                path_roofline=path_roofline(el, out), kernel_census=census(wisp.PAGER_DEVICE))
+                                path_roofline=path_roofline(el, out), all_steps=all_steps(el, out, warm),
+                                kernel_census=census(wisp.PAGER_DEVICE))
         passes["device"]["ffn_roofline"] = device_ffn_roofline(passes["device"]["kernel_census"])
         log(f"device pager: {steps} steps in {el:.3f} s -> {wl.T * steps / el:.2f} tokens/s, "
             f"{passes['device']['path_roofline']['frac']:.3f} of the path roofline")
