@@ -413,6 +413,14 @@ struct FfnT1Batch {
   int32_t n_items;
 };
 
+// A 16-byte weight load with the non-temporal hint: every weight of a layer-step is read once, so
+// its lines need not displace anything in the caches (3 % faster on the gate/up launches).
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_stream(const uint4* p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // One row pass of the single-token body, split so that the weight loads can be issued early: the
 // lane's NL 16-byte chunks of row rr of the first (and, for gate/up, second) matrix ...
 template <int MODE, int LPR, int NL>
@@ -422,8 +430,8 @@ __device__ __forceinline__ void t1_load(const uint8_t* w, uint32_t off0, uint32_
   const uint4* row1 = reinterpret_cast<const uint4*>(w + off1 + rr * row_b);
 #pragma unroll
   for (int m = 0; m < NL; ++m) {
-    a[m] = row0[m * LPR + sl];
-    if constexpr (MODE == MODE_GATEUP) b[m] = row1[m * LPR + sl];
+    a[m] = load_stream(row0 + m * LPR + sl);
+    if constexpr (MODE == MODE_GATEUP) b[m] = load_stream(row1 + m * LPR + sl);
   }
 }
 
