@@ -49,6 +49,42 @@ __device__ __forceinline__ void load_table(PagerShared& sh, int N, int C, const 
   sh.in_r[tid] = 0;
 }
 
+// The table entries of thread tid held in registers, so that loading them does not make the
+// thread wait before its next loads are issued (an LDS store of a loaded value waits for the load).
+struct TableRegs {
+  int32_t pi, pinv;
+  uint64_t tau, slot, clock;
+};
+
+__device__ __forceinline__ TableRegs load_table_regs(int N, int C, const int32_t* __restrict__ pi,
+                                                     const int32_t* __restrict__ pinv,
+                                                     const uint64_t* __restrict__ tau,
+                                                     const uint64_t* __restrict__ clock,
+                                                     const uint64_t* __restrict__ slot_ptr) {
+  const int tid = threadIdx.x;
+  TableRegs r{-1, -1, 0, 0, 0};
+  if (tid < N) r.pi = pi[tid];
+  if (tid < C) {
+    r.pinv = pinv[tid];
+    r.tau = tau[tid];
+    r.slot = slot_ptr[tid];
+  }
+  if (tid == 0) r.clock = *clock;
+  return r;
+}
+
+__device__ __forceinline__ void store_table(PagerShared& sh, int N, int C, const TableRegs& r) {
+  const int tid = threadIdx.x;
+  if (tid < N) sh.pi[tid] = r.pi;
+  if (tid < C) {
+    sh.pinv[tid] = r.pinv;
+    sh.tau[tid] = r.tau;
+    sh.slot[tid] = r.slot;
+  }
+  if (tid == 0) sh.clock = r.clock;
+  sh.in_r[tid] = 0;
+}
+
 // Selection, Algorithm 1 and the launch plan for one layer-step, by one workgroup whose table is in
 // sh (load_table) and whose threads have not yet synchronised since.
 template <bool COHERENT>
@@ -189,9 +225,10 @@ __global__ void __launch_bounds__(256) route_page_kernel(
   __shared__ float part[4][4];
   __shared__ int last;
   const int e = blockIdx.x;
-  // every workgroup loads the table (a few hundred words, mostly L2 hits), so the one that turns out
-  // to be last has it in LDS already
-  load_table(sh, N, C, pi, pinv, tau, clock, slot_ptr);
+  // every workgroup loads the table into registers first (a few hundred words, mostly L2 hits), so
+  // the one that turns out to be last has it without another round trip; the row loads follow
+  // without waiting for the table
+  const TableRegs tab = load_table_regs(N, C, pi, pinv, tau, clock, slot_ptr);
   const float z = router_row<XT>(wr, x, 0, T, d, e, part);
   if (static_cast<int>(threadIdx.x) < T)
     __hip_atomic_store(logits + static_cast<size_t>(threadIdx.x) * N + e, z, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -204,6 +241,7 @@ __global__ void __launch_bounds__(256) route_page_kernel(
   }
   __syncthreads();
   if (!last) return;
+  store_table(sh, N, C, tab);   // read after select_tokens' first barrier
   select_and_page<true>(sh, logits, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
                         master_base, master_stride, shared_dev, has_shared, plan, stats);
 }

@@ -22,8 +22,10 @@ enum { R_SOFTMAX_RENORM = 0, R_TOPK_SOFTMAX = 1, R_SIGMOID_GROUP = 2 };
 struct SelectShared {
   uint64_t key[4][256];   // (order-preserving logit << 32 | 255 - id), 0 = not allowed
   float z[4][256];
+  int cnt[4][256];        // partial ranks (N <= 128: threads e and e + 128 count halves)
   float gam[4][32];
   int sel[4][8];
+  float term[4][8];       // exp(z_j - z_0) or sigmoid(z_j) of rank j
   float gate[4][8];
 };
 
@@ -92,39 +94,63 @@ __device__ __forceinline__ void select_tokens(const float* __restrict__ logits, 
       if (t < nt && drop[t]) sh.key[t][e] = 0ull;
     __syncthreads();
   }
-  if (e < N) {
-    const int n_pad = (N + 15) & ~15;
+  // rank of expert e = the number of larger keys.  Up to 128 experts, threads e and e + 128 each
+  // count over one half of the (16-padded) row and the halves are added; beyond, thread e counts
+  // the whole row.
+  const int n_pad = (N + 15) & ~15;
+  const bool split = N <= 128;
+  const int ex = split ? (tid & 127) : tid;
+  const int h_mid = split ? ((n_pad + 31) >> 5) << 4 : n_pad;   // a multiple of 16
+  const int r0 = split && tid >= 128 ? h_mid : 0, r1 = split && tid < 128 ? h_mid : n_pad;
+  if (ex < N) {
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       if (t >= nt) break;
-      const uint64_t ke = sh.key[t][e];
-      if (ke == 0ull) continue;
+      const uint64_t ke = sh.key[t][ex];
       int rank = 0;
-      for (int e2 = 0; e2 < n_pad; e2 += 16) {
+      if (ke != 0ull) {
+        for (int e2 = r0; e2 < r1; e2 += 16) {
 #pragma unroll
-        for (int q = 0; q < 16; ++q) rank += sh.key[t][e2 + q] > ke ? 1 : 0;   // broadcast reads
+          for (int q = 0; q < 16; ++q) rank += sh.key[t][e2 + q] > ke ? 1 : 0;   // broadcast reads
+        }
       }
+      sh.cnt[t][tid] = rank;
+    }
+  }
+  __syncthreads();
+  if (e < N) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      if (t >= nt) break;
+      if (sh.key[t][e] == 0ull) continue;
+      const int rank = split ? sh.cnt[t][e] + sh.cnt[t][e + 128] : sh.cnt[t][e];
       if (rank < k) sh.sel[t][rank] = e;
+    }
+  }
+  __syncthreads();
+  // gates: the terms of all ranks in parallel, then one thread per token sums them in rank order
+  // and each rank's gate is its term times the reciprocal (the same operations as a serial loop)
+  {
+    const int t = tid >> 3, j = tid & 7;
+    if (t < nt && j < k) {
+      const float zj = sh.z[t][sh.sel[t][j]];
+      sh.term[t][j] = route == R_SIGMOID_GROUP ? sel_sigmoid(zj) : __expf(zj - sh.z[t][sh.sel[t][0]]);
     }
   }
   __syncthreads();
   if (tid < nt) {
     const int t = tid;
-    float g[8];
     float den = 0.f;
-    const float z0 = sh.z[t][sh.sel[t][0]];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       if (j >= k) break;
-      const float zj = sh.z[t][sh.sel[t][j]];
-      g[j] = route == R_SIGMOID_GROUP ? sel_sigmoid(zj) : __expf(zj - z0);
-      den += g[j];
+      den += sh.term[t][j];
     }
     const float inv = 1.0f / den;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       if (j >= k) break;
-      sh.gate[t][j] = g[j] * inv;
+      sh.gate[t][j] = sh.term[t][j] * inv;
     }
   }
   __syncthreads();
