@@ -211,7 +211,9 @@ wisp_status wisp_read_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, void* dst
  * union fits the cap runs the down projection of all its experts and the gate-weighted combine in
  * one launch (the per-expert outputs stay on chip) instead of a down launch per expert group and a
  * combine launch.  (2) The device pager computes the router logits and, in the workgroup that
- * completes them, the selection and Algorithm 1 in one launch instead of two.  Every logit, row,
+ * completes them, the selection and Algorithm 1 in one launch instead of two.  (3) wisp_route_topk
+ * (and the host pager's decode step) computes the logits of up to four tokens and, in the workgroup
+ * that completes them, their selection in one launch instead of two.  Every logit, row,
  * decision and sum is computed by the same operations in the same order either way, so routing,
  * paging and outputs are bit-identical.  on = 0 selects the separate kernels (for comparison).
  * WISP_E_STATE while a page-in is pending. */

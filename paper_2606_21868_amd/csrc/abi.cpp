@@ -896,21 +896,32 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
   if (!L.wr) return fail(WISP_E_STATE, "router weights not set for this layer");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const auto& d = ctx->desc;
-  LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_LOGITS);
-  WISP_HIP(launch_router_logits(L.wr, x_dev, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, st, t1),
-           "router logits launch");
-  timing_end(ctx, t1, WISP_K_ROUTER_LOGITS,
-             static_cast<uint64_t>(d.n_experts) * d.d_model * 4 + static_cast<uint64_t>(T) * d.d_model * ctx->x_elem() +
-                 static_cast<uint64_t>(T) * d.n_experts * 4);
   // decode: the router publishes tagged ids to host-coherent memory
   const bool publish = idx_host && T <= 4;
   const uint32_t seq = publish ? ++ctx->route_seq : 0;
-  LaunchTiming t2 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
-  WISP_HIP(launch_router_select(ctx->logits, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev,
-                                w_dev, publish ? ctx->idx_tagged : nullptr, seq, st, t2),
-           "router select launch");
-  timing_end(ctx, t2, WISP_K_ROUTER_SELECT,
-             static_cast<uint64_t>(T) * d.n_experts * 4 + static_cast<uint64_t>(T) * d.top_k * 8);
+  if (ctx->fusion && T <= 4) {
+    // logits and selection in one launch (the workgroup completing the logits selects)
+    LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
+    WISP_HIP(launch_route_select(L.wr, x_dev, d.x_dtype, d.d_model, ctx->logits, ctx->d_arrive, T, d.n_experts,
+                                 d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev, w_dev,
+                                 publish ? ctx->idx_tagged : nullptr, seq, st, t1),
+             "router logits + select launch");
+    timing_end(ctx, t1, WISP_K_ROUTER_SELECT,
+               static_cast<uint64_t>(d.n_experts) * d.d_model * 4 + static_cast<uint64_t>(T) * d.d_model * ctx->x_elem());
+  } else {
+    LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_LOGITS);
+    WISP_HIP(launch_router_logits(L.wr, x_dev, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, st, t1),
+             "router logits launch");
+    timing_end(ctx, t1, WISP_K_ROUTER_LOGITS,
+               static_cast<uint64_t>(d.n_experts) * d.d_model * 4 +
+                   static_cast<uint64_t>(T) * d.d_model * ctx->x_elem() + static_cast<uint64_t>(T) * d.n_experts * 4);
+    LaunchTiming t2 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
+    WISP_HIP(launch_router_select(ctx->logits, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev,
+                                  w_dev, publish ? ctx->idx_tagged : nullptr, seq, st, t2),
+             "router select launch");
+    timing_end(ctx, t2, WISP_K_ROUTER_SELECT,
+               static_cast<uint64_t>(T) * d.n_experts * 4 + static_cast<uint64_t>(T) * d.top_k * 8);
+  }
   if (publish) {
     const int n = T * d.top_k;
     // spin until every entry carries this call's tag: the wait on the critical path of a layer-step

@@ -120,6 +120,12 @@ hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int
                                 hipStream_t st, const LaunchTiming& tm);
 // Router selection: idx/w [T, k] by routing variant.  If idx_host is given, entry t*k+j of it (in
 // host-coherent memory) also receives (seq << 32 | id) as one 64-bit store.
+// Decode (T <= 4): router logits and selection in one launch (the workgroup completing the logits
+// selects); the same ids, gates and tagged ids as launch_router_logits + launch_router_select.  *arrive
+// is a device counter that must be 0 and is left 0.
+hipError_t launch_route_select(const float* wr, const void* x, int x_dtype, int d, float* logits, uint32_t* arrive,
+                               int T, int N, int k, int route, int n_groups, int topk_groups, int32_t* idx, float* w,
+                               uint64_t* idx_host, uint32_t seq, hipStream_t st, const LaunchTiming& tm);
 hipError_t launch_router_select(const float* logits, int T, int N, int k, int route, int n_groups, int topk_groups,
                                 int32_t* idx, float* w, uint64_t* idx_host, uint32_t seq, hipStream_t st,
                                 const LaunchTiming& tm);
