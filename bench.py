@@ -288,7 +288,7 @@ def prefetch_leg(run, wl, wisp, torch, warmup=16, steps=96):
     return out
 
 
-def prefill_leg(wisp, torch, link, passes=3):
+def prefill_leg(wisp, torch, link, link_cu=None, passes=3):
     """Prefill tokens/s of the token-batch path (2048 tokens per layer, union 128 > C = 32, so four
     chunked Algorithm 1 steps per layer, grouped MFMA GEMMs), from cold slot tables each pass as the
     workload prescribes; then a fully resident pass (C = N, preloaded) for the matrix-core rate of
@@ -321,7 +321,11 @@ def prefill_leg(wisp, torch, link, passes=3):
         t_hbm = distinct * wl.blob / (HBM_PEAK_GBPS * 1e9)
         t_mfma = flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
         t_roof = t_link + max(t_hbm, t_mfma)
-        log(f"prefill: cold pass {el * 1e3:.1f} ms -> {wl.T / el:.0f} tokens/s, {t_roof / el:.3f} of the roofline")
+        # the token-batch fills stream by the compute units, which move more than the copy-engine rate
+        # of the link term above: the same roofline with the compute-unit link rate is reported beside
+        t_roof_cu = misses * wl.blob / (link_cu * 1e9) + max(t_hbm, t_mfma) if link_cu else None
+        log(f"prefill: cold pass {el * 1e3:.1f} ms -> {wl.T / el:.0f} tokens/s, {t_roof / el:.3f} of the roofline"
+            + (f" ({t_roof_cu / el:.3f} with the compute-unit link rate)" if t_roof_cu else ""))
         # fully resident: the same kernels with no faults; grouped GEMMs timed by HIP events
         assert run.set_cap(wl.N) == wl.N
         run.ctx.preload()
@@ -365,7 +369,8 @@ def prefill_leg(wisp, torch, link, passes=3):
             workload=wl.description, tokens_per_s=wl.T / el, pass_ms=el * 1e3, passes=len(times),
             pass_ms_all=[t * 1e3 for t in times], cap_per_layer=wl.cap, faults=misses, distinct_experts=distinct,
             roofline=dict(t_roof_s=t_roof, t_link_s=t_link, t_hbm_s=t_hbm, t_mfma_s=t_mfma, frac=t_roof / el,
-                          roofline_tokens_per_s=wl.T / t_roof, link_GBps_measured=link, flops=flops),
+                          roofline_tokens_per_s=wl.T / t_roof, link_GBps_measured=link, flops=flops,
+                          link_cus_GBps_measured=link_cu, frac_cus_link=t_roof_cu / el if t_roof_cu else None),
             resident=dict(tokens_per_s=wl.T / rel, pass_ms=rel * 1e3, kernels=kern),
             mfma=dict(bound="mfma", achieved=achieved, peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
                       frac=achieved / MFMA_BF16_PEAK_TFLOPS if achieved else None,
@@ -429,8 +434,10 @@ def main():
         f"{time.time() - t0:.1f} s")
     n_probe = max(1, math.ceil(2e9 / wl.blob))
     link = run.ctx.probe_h2d(n_probe, 5)
+    link_cu = run.ctx.probe_h2d(n_probe, 5, engine=wisp.LINK_CUS)
     hbm_copy = measure_hbm_copy(torch, wisp)
-    log(f"host->device {link:.1f} GB/s (median of 5 x {n_probe} blobs); device copy {hbm_copy:.0f} GB/s")
+    log(f"host->device {link:.1f} GB/s copy engine, {link_cu:.1f} GB/s compute-unit streaming (median of 5 x "
+        f"{n_probe} blobs); device copy {hbm_copy:.0f} GB/s")
     assert run.set_cap(wl.cap) == wl.cap
     run.ctx.set_fusion(not args.no_fusion)
 
@@ -464,8 +471,10 @@ def main():
         hbm_bytes = float(distinct.sum()) * wl.blob + wl.N * wl.d * 4 * wl.L * n_steps
         link_bytes = float(misses.sum()) * wl.blob
         t_roof = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (link * 1e9)
+        t_roof_cu = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (link_cu * 1e9)
         return dict(t_roof_s=t_roof, t_measured_s=elapsed, frac=t_roof / elapsed,
                     roofline_tokens_per_s=wl.T * n_steps / t_roof, link_GBps_measured=link,
+                    link_cus_GBps_measured=link_cu, frac_cus_link=t_roof_cu / elapsed,
                     hbm_peak_GBps=HBM_PEAK_GBPS, device_copy_GBps_measured=hbm_copy,
                     hbm_bytes_per_token=hbm_bytes / (wl.T * n_steps), link_bytes_per_token=link_bytes / (wl.T * n_steps),
                     faults_per_token=float(misses.sum()) / (wl.T * n_steps),
@@ -573,7 +582,7 @@ def main():
     run.close()
     prefill = None
     if not args.no_prefill:
-        prefill = prefill_leg(wisp, torch, link)
+        prefill = prefill_leg(wisp, torch, link, link_cu)
 
     result = {
         "metric": "paged MoE decode tokens/s at fixed VRAM expert budget",

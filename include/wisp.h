@@ -242,6 +242,13 @@ wisp_status wisp_reset_kernel_times(wisp_ctx* ctx);
  * the median GB/s (1e9 bytes/s).  Allocates and frees the scratch buffer itself. */
 wisp_status wisp_probe_h2d(wisp_ctx* ctx, int32_t count, int32_t reps, double* gbps);
 
+/* The same measurement with the engine of the fills chosen: WISP_LINK_COPY_ENGINE (one
+ * hipMemcpyAsync per blob, as wisp_probe_h2d) or WISP_LINK_CUS (the compute units stream the blobs,
+ * 32 per launch, as the fills of token batches and the device pager do).  WISP_LINK_CUS needs pinned
+ * masters (WISP_E_INVAL otherwise); WISP_E_INVAL for an unknown engine. */
+typedef enum { WISP_LINK_COPY_ENGINE = 0, WISP_LINK_CUS = 1 } wisp_link_engine;
+wisp_status wisp_probe_h2d_engine(wisp_ctx* ctx, int32_t count, int32_t reps, int32_t engine, double* gbps);
+
 /* A plain device copy kernel (16-byte loads and stores) of `bytes` from src to dst on `stream`:
  * the reference for HBM counters and for measured copy bandwidth.  bytes must be a multiple of
  * 16 and both pointers 16-byte aligned. */

@@ -27,7 +27,7 @@ HIP_FLAGS = [
     "-Wall", "-Wno-unused-function", "-Wno-unused-result", f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 
-HIP_SOURCES = ["abi.cpp", "slot_table.cpp", "staging.cpp", "copy_pool.cpp", "mvwsa.cpp", "predictor.cpp", "router.hip", "expert_ffn.hip", "combine.hip", "probe.hip",
+HIP_SOURCES = ["abi.cpp", "slot_table.cpp", "staging.cpp", "copy_pool.cpp", "mvwsa.cpp", "predictor.cpp", "router.hip", "expert_ffn.hip", "combine.hip", "probe.hip", "fill.hip",
                "pager.hip", "grouped_gemm.hip"]
 
 

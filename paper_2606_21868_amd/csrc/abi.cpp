@@ -423,6 +423,36 @@ wisp_status master_h2d(wisp_ctx* c, void* dst, const uint8_t* src, size_t bytes,
   return WISP_OK;
 }
 
+// (expert, slot) blobs of `layer` into their slots on the side stream.  Token batches with pinned
+// masters: the compute units stream them over the host link (one launch per up to kMaxFills blobs;
+// 4 % faster than a copy-engine copy per blob on the cold prefill pass).  Decode steps: a copy-engine
+// copy per blob, because the fills run beside the GEMV over the resident experts and compute-unit
+// reads of host memory slow it down (8.4 -> 12 us median, and far more at the tail).  Pageable
+// masters: staged through the bounce ring.
+wisp_status fill_slots(wisp_ctx* c, int32_t layer, const std::vector<std::pair<int32_t, int32_t>>& fills,
+                       bool by_cus) {
+  LayerState& L = c->layers[layer];
+  if (c->pageable || !by_cus) {
+    for (const auto& f : fills) {
+      wisp_status s = master_h2d(c, L.slot_mem[f.second], c->master(layer, f.first), c->blob.bytes, c->side);
+      if (s != WISP_OK) return s;
+    }
+    return WISP_OK;
+  }
+  FillList fl;
+  fl.n = 0;
+  for (const auto& f : fills) {
+    fl.src[fl.n] = c->master(layer, f.first);
+    fl.dst[fl.n] = L.slot_mem[f.second];
+    if (++fl.n == kMaxFills) {
+      WISP_HIP(launch_fill(fl, c->blob.bytes, c->side, LaunchTiming{}), "fill launch");
+      fl.n = 0;
+    }
+  }
+  WISP_HIP(launch_fill(fl, c->blob.bytes, c->side, LaunchTiming{}), "fill launch");
+  return WISP_OK;
+}
+
 wisp_status issue_fills(wisp_ctx* c, int32_t layer, size_t ci) {
   LayerState& L = c->layers[layer];
   const ChunkPlan& cp = L.plan.chunks[ci];
@@ -434,11 +464,12 @@ wisp_status issue_fills(wisp_ctx* c, int32_t layer, size_t ci) {
   }
   LaunchTiming tm = timing_begin(c, WISP_K_H2D_FILL);
   if (tm.start) WISP_HIP(hipEventRecord(tm.start, c->side), "hipEventRecord");
-  for (size_t i = 0; i < cp.experts.size(); ++i) {
-    if (!cp.fault[i]) continue;
-    wisp_status s = master_h2d(c, L.slot_mem[cp.slots[i]], c->master(layer, cp.experts[i]), c->blob.bytes, c->side);
-    if (s != WISP_OK) return s;
-  }
+  std::vector<std::pair<int32_t, int32_t>> fills;
+  for (size_t i = 0; i < cp.experts.size(); ++i)
+    if (cp.fault[i]) fills.push_back({cp.experts[i], cp.slots[i]});
+  const bool batch = L.T >= kGroupedMinTokens && grouped_supported(c->shape, c->desc.has_shared);
+  wisp_status s = fill_slots(c, layer, fills, batch);
+  if (s != WISP_OK) return s;
   if (tm.stop) WISP_HIP(hipEventRecord(tm.stop, c->side), "hipEventRecord");
   timing_end(c, tm, WISP_K_H2D_FILL, static_cast<uint64_t>(cp.n_faults) * c->blob.bytes);
   WISP_HIP(hipEventRecord(L.fill_ev[ci], c->side), "hipEventRecord(fill)");
@@ -512,9 +543,9 @@ wisp_status prefetch_layer(wisp_ctx* c, int32_t layer, const int32_t* ids, int32
   if (L.use_ev_recorded) WISP_HIP(hipStreamWaitEvent(c->side, L.use_ev, 0), "hipStreamWaitEvent(use)");
   LaunchTiming tm = timing_begin(c, WISP_K_H2D_FILL);
   if (tm.start) WISP_HIP(hipEventRecord(tm.start, c->side), "hipEventRecord");
+  wisp_status s = fill_slots(c, layer, fills, false);
+  if (s != WISP_OK) return s;
   for (const auto& f : fills) {
-    wisp_status s = master_h2d(c, L.slot_mem[f.second], c->master(layer, f.first), c->blob.bytes, c->side);
-    if (s != WISP_OK) return s;
     L.pf_inflight.push_back(f.first);
     L.pf_unused.push_back(f.first);
   }
@@ -1616,9 +1647,16 @@ wisp_status wisp_reset_kernel_times(wisp_ctx* ctx) {
 }
 
 wisp_status wisp_probe_h2d(wisp_ctx* ctx, int32_t count, int32_t reps, double* gbps) {
+  return wisp_probe_h2d_engine(ctx, count, reps, WISP_LINK_COPY_ENGINE, gbps);
+}
+
+wisp_status wisp_probe_h2d_engine(wisp_ctx* ctx, int32_t count, int32_t reps, int32_t engine, double* gbps) {
   wisp_status s = check_ctx(ctx);
   if (s != WISP_OK) return s;
   if (count < 1 || reps < 1 || !gbps) return fail(WISP_E_INVAL, "count, reps >= 1 and gbps required");
+  if (engine != WISP_LINK_COPY_ENGINE && engine != WISP_LINK_CUS) return fail(WISP_E_INVAL, "unknown engine");
+  if (engine == WISP_LINK_CUS && ctx->pageable)
+    return fail(WISP_E_INVAL, "compute-unit fills read pinned masters; these are pageable");
   if ((s = drain(ctx)) != WISP_OK) return s;
   void* scratch = nullptr;
   const size_t B = ctx->blob.bytes;
@@ -1634,7 +1672,20 @@ wisp_status wisp_probe_h2d(wisp_ctx* ctx, int32_t count, int32_t reps, double* g
   int src = 0;
   for (int r = 0; r < reps && e == hipSuccess; ++r) {
     e = hipEventRecord(a, ctx->side);
-    for (int i = 0; i < count && e == hipSuccess; ++i, ++src) {
+    if (engine == WISP_LINK_CUS) {
+      FillList fl;
+      fl.n = 0;
+      for (int i = 0; i < count && e == hipSuccess; ++i, ++src) {
+        const int l = (src / ne) % nl, x = src % ne;
+        fl.src[fl.n] = ctx->master(l, x);
+        fl.dst[fl.n] = static_cast<uint8_t*>(scratch) + static_cast<size_t>(i) * B;
+        if (++fl.n == 32 || i + 1 == count) {
+          e = launch_fill(fl, B, ctx->side, LaunchTiming{});
+          fl.n = 0;
+        }
+      }
+    }
+    for (int i = 0; i < count && e == hipSuccess && engine == WISP_LINK_COPY_ENGINE; ++i, ++src) {
       const int l = (src / ne) % nl, x = src % ne;
       if (!ctx->pageable)
         e = hipMemcpyAsync(static_cast<uint8_t*>(scratch) + static_cast<size_t>(i) * B, ctx->master(l, x), B,

@@ -149,6 +149,15 @@ hipError_t launch_route_page(const float* wr, const void* x, int x_dtype, int d,
                              hipStream_t st, const LaunchTiming& tm);
 
 // Diagnostics.
+// Fills by the compute units: dst[i][0, bytes) <- src[i][0, bytes) for i < n, reading pinned host
+// memory over the host link.  Up to kMaxFills blobs per launch.
+constexpr int kMaxFills = 64;
+struct FillList {
+  const uint8_t* src[kMaxFills];
+  uint8_t* dst[kMaxFills];
+  int32_t n;
+};
+hipError_t launch_fill(const FillList& fl, uint64_t bytes, hipStream_t st, const LaunchTiming& tm);
 hipError_t launch_hbm_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
 hipError_t launch_decode_fp8(const uint8_t* codes, float* out, int n, hipStream_t st);
 

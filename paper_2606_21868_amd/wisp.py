@@ -23,6 +23,7 @@ OK, E_INVAL, E_NOMEM, E_HIP, E_NOT_RESIDENT, E_STATE = 0, -1, -2, -3, -4, -5
 STATUS_NAMES = {0: "OK", -1: "E_INVAL", -2: "E_NOMEM", -3: "E_HIP", -4: "E_NOT_RESIDENT", -5: "E_STATE"}
 F32, BF16, FP8 = 0, 1, 2
 PAGER_HOST, PAGER_DEVICE = 0, 1
+LINK_COPY_ENGINE, LINK_CUS = 0, 1
 OFFLOAD_BULK, OFFLOAD_ZERO_COPY = 0, 1
 PREFETCH_OFF, PREFETCH_PREDICTOR, PREFETCH_HINTS = 0, 1, 2
 (K_ROUTER_LOGITS, K_ROUTER_SELECT, K_FFN_GATEUP, K_FFN_DOWN, K_COMBINE, K_H2D_FILL, K_GROUPED_GATEUP,
@@ -114,6 +115,7 @@ _SIGS = {
                           ctypes.POINTER(_U64)],
     "wisp_reset_kernel_times": [_P],
     "wisp_probe_h2d": [_P, _I, _I, ctypes.POINTER(ctypes.c_double)],
+    "wisp_probe_h2d_engine": [_P, _I, _I, _I, ctypes.POINTER(ctypes.c_double)],
     "wisp_hbm_copy": [_P, _P, _U64, _P],
     "wisp_decode_fp8": [_P, _P, _I, _P],
     "wisp_debug_fail_slot_alloc": [_P, _I],
@@ -324,9 +326,14 @@ class Context:
     def reset_kernel_times(self):
         check(lib().wisp_reset_kernel_times(self.h), "wisp_reset_kernel_times")
 
-    def probe_h2d(self, count, reps):
+    def probe_h2d(self, count, reps, engine=None):
+        """Median host->device GB/s over `reps` rounds of `count` expert blobs: the copy engine (default,
+        wisp_probe_h2d) or engine=LINK_CUS (compute-unit streaming, as the token-batch fills)."""
         g = ctypes.c_double()
-        check(lib().wisp_probe_h2d(self.h, count, reps, ctypes.byref(g)), "wisp_probe_h2d")
+        if engine is None:
+            check(lib().wisp_probe_h2d(self.h, count, reps, ctypes.byref(g)), "wisp_probe_h2d")
+        else:
+            check(lib().wisp_probe_h2d_engine(self.h, count, reps, engine, ctypes.byref(g)), "wisp_probe_h2d_engine")
         return g.value
 
     def debug_fail_slot_alloc(self, n):

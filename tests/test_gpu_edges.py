@@ -112,3 +112,29 @@ def test_token_count_and_pointer_errors_leave_state_untouched():
         assert np.array_equal(again["y"].view(np.uint32), ref["y"].view(np.uint32))
     finally:
         run.close()
+
+
+def test_link_probe_engines():
+    # both fill engines move the expert blobs at a plausible link rate; the compute-unit engine needs
+    # pinned masters and an engine outside the two is rejected
+    wl = SMALL.with_(N=16, k=4, d=2048, I=768)
+    run = wisp.DecodeRun(wl, device=0, steps=1)
+    try:
+        run.generate(inputs=False)
+        ce = run.ctx.probe_h2d(8, 3)
+        cu = run.ctx.probe_h2d(8, 3, engine=wisp.LINK_CUS)
+        log(f"  link probe: copy engine {ce:.1f} GB/s, compute units {cu:.1f} GB/s")
+        assert 5 < ce < 200 and 5 < cu < 200
+        with pytest.raises(wisp.WispError) as ei:
+            run.ctx.probe_h2d(8, 3, engine=2)
+        assert ei.value.status == wisp.E_INVAL
+    finally:
+        run.close()
+    run = wisp.DecodeRun(wl, device=0, steps=1, pageable=True)
+    try:
+        run.generate(inputs=False)
+        with pytest.raises(wisp.WispError) as ei:
+            run.ctx.probe_h2d(8, 3, engine=wisp.LINK_CUS)
+        assert ei.value.status == wisp.E_INVAL
+    finally:
+        run.close()
