@@ -375,8 +375,8 @@ def prefill_leg(wisp, torch, link, link_cu=None, passes=3):
             mfma=dict(bound="mfma", achieved=achieved, peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
                       frac=achieved / MFMA_BF16_PEAK_TFLOPS if achieved else None,
                       kernels="grouped gate/up + down (bf16 v_mfma_f32_32x32x16), resident pass"),
-            # at ~4096 rows per 32-expert launch the grouped GEMMs do ~100 FLOP per weight byte, below
-            # the bf16 ridge (2.5 PFLOP/s / 8 TB/s = 312): HBM is their bound
+            # at ~128 rows per expert the grouped GEMMs do ~100 FLOP per weight byte, below the bf16
+            # ridge (2.5 PFLOP/s / 8 TB/s = 312): HBM is their bound
             hbm=dict(bound="hbm", achieved=gbytes / (gms * 1e-3) / 1e9 if gms > 0 else None, peak=HBM_PEAK_GBPS,
                      unit="GB/s", frac=gbytes / (gms * 1e-3) / 1e9 / HBM_PEAK_GBPS if gms > 0 else None,
                      kernels="grouped gate/up + down, algorithmic bytes (weights once, rows in and out)"))

@@ -1123,11 +1123,11 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
       }
       const uint64_t ng = static_cast<uint64_t>(gb.n_groups);
       LaunchTiming t1 = timing_begin(ctx, WISP_K_GROUPED_GATEUP);
-      WISP_HIP(launch_grouped_gateup(gb, ctx->shape, x_dev, ctx->d_perm, k, ctx->h, sm, t1), "grouped gate/up launch");
+      WISP_HIP(launch_grouped_gateup(gb, ctx->shape, x_dev, T, ctx->d_perm, k, ctx->h, sm, t1), "grouped gate/up launch");
       timing_end(ctx, t1, WISP_K_GROUPED_GATEUP, ng * 2 * dI * B.elem + nrows * (B.d + B.I) * 2,
                  nrows * 2 * 2 * dI);
       LaunchTiming t2 = timing_begin(ctx, WISP_K_GROUPED_DOWN);
-      WISP_HIP(launch_grouped_down(gb, ctx->shape, ctx->h, ctx->d_perm, k, ctx->buf, sm, t2), "grouped down launch");
+      WISP_HIP(launch_grouped_down(gb, ctx->shape, ctx->h, T, ctx->d_perm, k, ctx->buf, sm, t2), "grouped down launch");
       timing_end(ctx, t2, WISP_K_GROUPED_DOWN, ng * dI * B.elem + nrows * (B.I * 2 + B.d * 4), nrows * 2 * dI);
     }
     return WISP_OK;

@@ -93,8 +93,9 @@ hipError_t launch_combine(int T, int k, int d, int has_shared, const float* w, c
 
 // Token batches (prefill): grouped GEMMs on the matrix cores over slot-indirected experts.
 // The (token, rank) pairs p = t*k + j are ordered by expert (stable); expert g of a launch owns
-// rows [row_off, row_off + rows) of that order.  Up to kMaxGroups experts per launch.
-constexpr int kMaxGroups = 32;
+// rows [row_off, row_off + rows) of that order.  Up to kMaxGroups experts per launch (the batch is a
+// 2.5 KB kernel argument).
+constexpr int kMaxGroups = 128;
 constexpr int kGroupedMinTokens = 16;   // token batches from this size take the grouped GEMMs
 struct GroupedBatch {
   const uint8_t* w[kMaxGroups];   // the expert's blob in its HBM slot
@@ -108,12 +109,13 @@ int grouped_row_tiles(int rows);
 // perm[off_e + i] = the i-th pair (ascending) routed to expert e; off_e = pairs of experts < e.
 hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t* perm, hipStream_t st,
                                 const LaunchTiming& tm);
-// hs[row] = bf16(silu(W1 x[t]) * (W3 x[t])) for every row of the batch's experts (row in sorted order).
-hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const void* x, const int32_t* perm, int k,
-                                 void* hs, hipStream_t st, const LaunchTiming& tm);
+// hs[row] = bf16(silu(W1 x[t]) * (W3 x[t])) for every row of the batch's experts (row in sorted order);
+// x holds n_tok token rows, hs n_tok * k pair rows.
+hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const void* x, int n_tok,
+                                 const int32_t* perm, int k, void* hs, hipStream_t st, const LaunchTiming& tm);
 // buf[t*(k+1)+j] = W2 hs[row] for the pair p = t*k+j of every row.
-hipError_t launch_grouped_down(const GroupedBatch& b, const FfnShape& s, const void* hs, const int32_t* perm, int k,
-                               float* buf, hipStream_t st, const LaunchTiming& tm);
+hipError_t launch_grouped_down(const GroupedBatch& b, const FfnShape& s, const void* hs, int n_tok, const int32_t* perm,
+                               int k, float* buf, hipStream_t st, const LaunchTiming& tm);
 
 // Router: logits[t, e] = W_r[e] . x[t] (fp32 accumulate).
 hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int T, int N, int d, float* logits,
