@@ -553,6 +553,17 @@ def main():
                         traffic=tr["bytes_per_launch"] if tr else None,
                         traffic_detail=tr, kernel="ffn_rows<bf16,bf16,gate/up> expert GEMV (W1+W3 rows), host-pager pass",
                         avg_launch_us=g["avg_us"], bytes_per_launch=g["bytes_per_launch"], launches=g["launches"])
+            # what a plain streaming read of the same bytes per launch takes on this GPU: the floor of
+            # any kernel that must read them in one launch of this size
+            nb = int(g["bytes_per_launch"]) // 16 * 16
+            us = wisp.probe_hbm_read(nb, 400)
+            floor = nb / (us * 1e-6) / 1e9
+            roof["read_floor"] = dict(
+                bytes_per_launch=nb, us_per_launch=us, GBps=floor, frac_of_peak=floor / HBM_PEAK_GBPS,
+                method="plain streaming-read kernel, 400 launches back to back over windows of a 2 GiB buffer")
+            roof["frac_of_read_floor"] = g["GBps"] / floor
+            log(f"gate/up GEMV: {g['GBps']:.0f} GB/s in the timed region; a plain read of the same {nb / 1e6:.1f} MB per "
+                f"launch: {us:.2f} us = {floor:.0f} GB/s ({g['GBps'] / floor:.3f} of it)")
     if args.pager in ("both", "device"):
         el, out, warm = timed_pass(wisp.PAGER_DEVICE, 0)
         passes["device"] = dict(tokens_per_s=wl.T * steps / el, ms_per_step=el / steps * 1e3,

@@ -254,6 +254,14 @@ wisp_status wisp_probe_h2d_engine(wisp_ctx* ctx, int32_t count, int32_t reps, in
  * 16 and both pointers 16-byte aligned. */
 wisp_status wisp_hbm_copy(const void* src, void* dst, uint64_t bytes, void* stream);
 
+/* The read floor of a launch size: `launches` back-to-back launches of a plain streaming-read kernel
+ * (16-byte non-temporal loads, 16 KB per workgroup, nothing stored), each reading `bytes` from its
+ * own window of a device buffer of at least 2 GiB, so that no launch finds its bytes in the 256 MB
+ * last-level cache; returns the mean time per launch in microseconds.  bytes in [16, 4 GiB] and a
+ * multiple of 16, launches >= 1 (WISP_E_INVAL otherwise).  Allocates, uses and frees its own buffer
+ * and stream (WISP_E_NOMEM when the buffer does not fit). */
+wisp_status wisp_probe_hbm_read(uint64_t bytes, int32_t launches, double* us_per_launch);
+
 /* Decode n fp8 E4M3 codes to fp32 on the device with the same conversion the FFN kernels use
  * (for checking the hardware conversion against the format definition). */
 wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n, void* stream);

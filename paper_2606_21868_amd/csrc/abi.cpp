@@ -1717,6 +1717,45 @@ wisp_status wisp_hbm_copy(const void* src, void* dst, uint64_t bytes, void* stre
   return WISP_OK;
 }
 
+wisp_status wisp_probe_hbm_read(uint64_t bytes, int32_t launches, double* us_per_launch) {
+  if (bytes < 16 || bytes % 16 || bytes > (1ull << 32) || launches < 1 || !us_per_launch)
+    return fail(WISP_E_INVAL, "bytes in [16, 4 GiB] and a multiple of 16, launches >= 1, result pointer required");
+  // enough windows that a launch never reads what the last-level cache (256 MB) still holds
+  const uint64_t nwin = std::max<uint64_t>(4, ((2ull << 30) + bytes - 1) / bytes);
+  void* buf = nullptr;
+  uint32_t* sink = nullptr;
+  if (hipMalloc(&buf, nwin * bytes) != hipSuccess || hipMalloc(reinterpret_cast<void**>(&sink), 256) != hipSuccess) {
+    hipGetLastError();
+    if (buf) hipFree(buf);
+    return fail(WISP_E_NOMEM, "read probe allocation failed");
+  }
+  hipStream_t st = nullptr;
+  hipEvent_t a = nullptr, b = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreate(&a);
+  if (e == hipSuccess) e = hipEventCreate(&b);
+  if (e == hipSuccess) e = hipMemsetAsync(buf, 0, nwin * bytes, st);
+  const uint8_t* base = static_cast<const uint8_t*>(buf);
+  uint64_t w = 0;
+  for (int i = 0; i < 8 && e == hipSuccess; ++i, ++w) e = launch_hbm_read(base + (w % nwin) * bytes, bytes, sink, st);
+  if (e == hipSuccess) e = hipEventRecord(a, st);
+  for (int i = 0; i < launches && e == hipSuccess; ++i, ++w)
+    e = launch_hbm_read(base + (w % nwin) * bytes, bytes, sink, st);
+  if (e == hipSuccess) e = hipEventRecord(b, st);
+  if (e == hipSuccess) e = hipEventSynchronize(b);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+  if (st) hipStreamSynchronize(st);
+  if (a) hipEventDestroy(a);
+  if (b) hipEventDestroy(b);
+  if (st) hipStreamDestroy(st);
+  hipFree(sink);
+  hipFree(buf);
+  if (e != hipSuccess) return fail(WISP_E_HIP, std::string("read probe: ") + hipGetErrorString(e));
+  *us_per_launch = static_cast<double>(ms) * 1e3 / launches;
+  return WISP_OK;
+}
+
 wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n, void* stream) {
   if (!codes_dev || !out_dev || n < 0) return fail(WISP_E_INVAL, "bad argument");
   WISP_HIP(launch_decode_fp8(codes_dev, out_dev, n, static_cast<hipStream_t>(stream)), "decode launch");

@@ -1,5 +1,6 @@
-// A plain device copy with 16-byte loads and stores: the yardstick for HBM byte counters
-// (FETCH_SIZE / WRITE_SIZE per copied byte) and for the achievable copy bandwidth.
+// Yardsticks: a plain device copy with 16-byte loads and stores (for HBM byte counters, FETCH_SIZE /
+// WRITE_SIZE per copied byte, and the achievable copy bandwidth), and a plain streaming read (the
+// read time of a launch of a given size, the floor of any kernel that must read those bytes).
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
@@ -13,7 +14,34 @@ __global__ void __launch_bounds__(256) hbm_copy_kernel(const uint4* __restrict__
   for (size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) dst[i] = src[i];
 }
 
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// Each thread issues its four 16-byte non-temporal loads before using any; a workgroup covers 16 KB.
+// The loaded words are folded into one value that is stored only if it equals an arbitrary constant,
+// so the loads cannot be dropped and the kernel writes (almost) nothing.
+__global__ void __launch_bounds__(256) hbm_read_kernel(const u32x4_t* __restrict__ src, size_t n, uint32_t* sink) {
+  const size_t base = static_cast<size_t>(blockIdx.x) * 1024 + threadIdx.x;
+  u32x4_t a[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const size_t i = base + static_cast<size_t>(m) * 256;
+    a[m] = i < n ? __builtin_nontemporal_load(src + i) : u32x4_t{0u, 0u, 0u, 0u};
+  }
+  uint32_t acc = 0;
+#pragma unroll
+  for (int m = 0; m < 4; ++m) acc ^= a[m].x ^ a[m].y ^ a[m].z ^ a[m].w;
+  if (acc == 0x9e3779b9u) sink[0] = acc;
+}
+
 }  // namespace
+
+hipError_t launch_hbm_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t st) {
+  if (bytes == 0) return hipSuccess;
+  const size_t n = bytes / 16;
+  hipLaunchKernelGGL(hbm_read_kernel, dim3(static_cast<unsigned>((n + 1023) / 1024)), dim3(256), 0, st,
+                     static_cast<const u32x4_t*>(src), n, sink);
+  return hipGetLastError();
+}
 
 hipError_t launch_hbm_copy(const void* src, void* dst, size_t bytes, hipStream_t st) {
   if (bytes == 0) return hipSuccess;

@@ -117,6 +117,7 @@ _SIGS = {
     "wisp_probe_h2d": [_P, _I, _I, ctypes.POINTER(ctypes.c_double)],
     "wisp_probe_h2d_engine": [_P, _I, _I, _I, ctypes.POINTER(ctypes.c_double)],
     "wisp_hbm_copy": [_P, _P, _U64, _P],
+    "wisp_probe_hbm_read": [_U64, _I, ctypes.POINTER(ctypes.c_double)],
     "wisp_decode_fp8": [_P, _P, _I, _P],
     "wisp_debug_fail_slot_alloc": [_P, _I],
     "wisp_predictor_create": [_I, _I, _I, ctypes.c_double, ctypes.POINTER(_P)],
@@ -404,6 +405,14 @@ class Predictor:
         check(lib().wisp_predictor_predict(self.h, int(layer), int(depth), ids.ctypes.data, ctypes.byref(n),
                                            sc.ctypes.data), "wisp_predictor_predict")
         return ids[:n.value].copy(), sc[:n.value].copy()
+
+
+def probe_hbm_read(nbytes, launches):
+    """Mean microseconds per launch of a plain streaming read of nbytes (a multiple of 16), launched
+    back to back over windows of a buffer beyond the last-level cache (wisp_probe_hbm_read)."""
+    us = ctypes.c_double()
+    check(lib().wisp_probe_hbm_read(int(nbytes), int(launches), ctypes.byref(us)), "wisp_probe_hbm_read")
+    return us.value
 
 
 def hbm_copy(src, dst, nbytes, stream=None):

@@ -67,6 +67,13 @@ def test_invalid_descriptions_rejected_before_any_gpu_call():
         wisp.Context(d)
 
 
+def test_read_probe_rejects_bad_sizes_before_any_gpu_call():
+    for nbytes, launches in ((0, 1), (15, 1), (24, 1), ((1 << 32) + 16, 1), (4096, 0)):
+        with pytest.raises(wisp.WispError) as ei:
+            wisp.probe_hbm_read(nbytes, launches)
+        assert ei.value.status == wisp.E_INVAL, (nbytes, launches)
+
+
 def _set_trace(rng, N, steps, refs, rho):
     cur = list(rng.choice(N, refs, replace=False))
     out = []

@@ -138,3 +138,14 @@ def test_link_probe_engines():
         assert ei.value.status == wisp.E_INVAL
     finally:
         run.close()
+
+
+def test_read_floor_probe():
+    # a plain streaming read: positive times at a plausible HBM rate, longer for four times the bytes
+    small = wisp.probe_hbm_read(27_566_080, 100)
+    large = wisp.probe_hbm_read(4 * 27_566_080, 100)
+    log(f"  read floor: 27.6 MB in {small:.2f} us, 110.3 MB in {large:.2f} us per launch")
+    for nbytes, us in ((27_566_080, small), (4 * 27_566_080, large)):
+        rate = nbytes / (us * 1e-6) / 1e9
+        assert 500 < rate < 8000, (nbytes, us, rate)
+    assert large > small
