@@ -121,6 +121,13 @@ struct wisp_ctx {
   int32_t* d_perm = nullptr;         // [max_tokens * k]
   hipEvent_t ids_ev = nullptr;       // the last upload has been read
   bool ids_ev_recorded = false;
+  // the permutation of a token batch, computed from the device ids right after routing (while the
+  // host pages the layer in) and used by the next wisp_moe_forward of that layer with the same ids
+  hipEvent_t perm_ev = nullptr;      // the last early permutation is done
+  hipEvent_t perm_use_ev = nullptr;  // the last grouped launches that read d_perm are done
+  bool perm_ev_recorded = false, perm_use_recorded = false;
+  int32_t perm_layer = -1, perm_T = 0;
+  std::vector<int32_t> perm_ids;     // the ids the early permutation was computed from
   std::vector<int32_t> e_cnt, e_off; // pairs per expert and their first sorted row
   std::vector<int32_t> pair_order;   // pairs sorted by expert (host copy, for the per-item path)
   // routing-blind static offload (comparison arm)
@@ -311,6 +318,8 @@ void free_ctx(wisp_ctx* c) {
   if (c->d_ids) hipFree(c->d_ids);
   if (c->d_perm) hipFree(c->d_perm);
   if (c->ids_ev) hipEventDestroy(c->ids_ev);
+  if (c->perm_ev) hipEventDestroy(c->perm_ev);
+  if (c->perm_use_ev) hipEventDestroy(c->perm_use_ev);
   for (void* p : {static_cast<void*>(c->d_pi), static_cast<void*>(c->d_pinv), static_cast<void*>(c->d_tau),
                   static_cast<void*>(c->d_clock), static_cast<void*>(c->d_slot_ptr), static_cast<void*>(c->d_plan),
                   static_cast<void*>(c->d_stats)})
@@ -684,7 +693,9 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   c->d_ids = static_cast<int32_t*>(p);
   if (hipMalloc(&p, pairs_bytes) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
   c->d_perm = static_cast<int32_t*>(p);
-  if (hipEventCreateWithFlags(&c->ids_ev, hipEventDisableTiming) != hipSuccess)
+  if (hipEventCreateWithFlags(&c->ids_ev, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->perm_ev, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->perm_use_ev, hipEventDisableTiming) != hipSuccess)
     return bail(WISP_E_HIP, "hipEventCreate failed");
   c->e_cnt.assign(N, 0);
   c->e_off.assign(N + 1, 0);
@@ -976,12 +987,29 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
     const size_t nb = sizeof(int32_t) * static_cast<size_t>(T) * d.top_k;
     WISP_HIP(hipMemcpyAsync(ctx->idx_pinned, idx_dev, nb, hipMemcpyDeviceToHost, st), "hipMemcpyAsync(idx)");
     WISP_HIP(hipEventRecord(ctx->route_ev, st), "hipEventRecord(route)");
+    // a token batch for the grouped FFN: its pairs are ordered by expert now, from the device ids,
+    // while the host waits for the ids and pages the layer in (after the last reader of the order)
+    const bool early = T >= kGroupedMinTokens && grouped_supported(ctx->shape, d.has_shared);
+    if (early) {
+      ctx->perm_layer = -1;
+      if (ctx->perm_use_recorded) WISP_HIP(hipStreamWaitEvent(st, ctx->perm_use_ev, 0), "hipStreamWaitEvent(perm use)");
+      LaunchTiming tp = timing_begin(ctx, WISP_K_PERMUTE);
+      WISP_HIP(launch_permute_pairs(idx_dev, T * d.top_k, d.n_experts, ctx->d_perm, st, tp), "permute launch");
+      timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(T) * d.top_k * 8);
+      WISP_HIP(hipEventRecord(ctx->perm_ev, st), "hipEventRecord(perm)");
+      ctx->perm_ev_recorded = true;
+    }
     // spin: this wait is on the critical path of every layer-step
     hipError_t q;
     while ((q = hipEventQuery(ctx->route_ev)) == hipErrorNotReady) {
     }
     if (q != hipSuccess) return fail(WISP_E_HIP, std::string("route event: ") + hipGetErrorString(q));
     std::memcpy(idx_host, ctx->idx_pinned, nb);
+    if (early) {
+      ctx->perm_ids.assign(ctx->idx_pinned, ctx->idx_pinned + static_cast<size_t>(T) * d.top_k);
+      ctx->perm_layer = layer;
+      ctx->perm_T = T;
+    }
     if (ctx->profiling) harvest(ctx, false);
   }
   return WISP_OK;
@@ -1063,7 +1091,8 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
   for (int32_t p = 0; p < n_pairs; ++p) ++cnt[L.ids[p]];
   off[0] = 0;
   for (int e = 0; e < N; ++e) off[e + 1] = off[e] + cnt[e];
-  {
+  const bool grouped = T >= kGroupedMinTokens && grouped_supported(ctx->shape, ctx->desc.has_shared);
+  if (!grouped) {   // the per-item launches list their pairs; the grouped ones read the device order
     std::vector<int32_t> fill(off.begin(), off.end() - 1);
     for (int32_t p = 0; p < n_pairs; ++p) ctx->pair_order[fill[L.ids[p]]++] = p;
   }
@@ -1085,18 +1114,24 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
       L.pf_inflight.clear();
     }
   }
-  const bool grouped = T >= kGroupedMinTokens && grouped_supported(ctx->shape, ctx->desc.has_shared);
   if (grouped) {
-    // the ids go to the device once; the permutation kernel orders the pairs by expert there
-    if (ctx->ids_ev_recorded) WISP_HIP(hipEventSynchronize(ctx->ids_ev), "hipEventSynchronize(ids)");
-    std::memcpy(ctx->ids_up, L.ids.data(), sizeof(int32_t) * n_pairs);
-    WISP_HIP(hipMemcpyAsync(ctx->d_ids, ctx->ids_up, sizeof(int32_t) * n_pairs, hipMemcpyHostToDevice, sm),
-             "hipMemcpyAsync(ids)");
-    WISP_HIP(hipEventRecord(ctx->ids_ev, sm), "hipEventRecord(ids)");
-    ctx->ids_ev_recorded = true;
-    LaunchTiming tp = timing_begin(ctx, WISP_K_PERMUTE);
-    WISP_HIP(launch_permute_pairs(ctx->d_ids, n_pairs, N, ctx->d_perm, sm, tp), "permute launch");
-    timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(n_pairs) * 8);
+    // the permutation wisp_route_topk computed for this layer, if it came from the ids paged in
+    const bool early = ctx->perm_layer == layer && ctx->perm_T == T &&
+                       std::memcmp(ctx->perm_ids.data(), L.ids.data(), sizeof(int32_t) * n_pairs) == 0;
+    ctx->perm_layer = -1;   // used once; the launches below overwrite it otherwise
+    if (ctx->perm_ev_recorded) WISP_HIP(hipStreamWaitEvent(sm, ctx->perm_ev, 0), "hipStreamWaitEvent(perm)");
+    if (!early) {
+      // the ids go to the device; the permutation kernel orders the pairs by expert there
+      if (ctx->ids_ev_recorded) WISP_HIP(hipEventSynchronize(ctx->ids_ev), "hipEventSynchronize(ids)");
+      std::memcpy(ctx->ids_up, L.ids.data(), sizeof(int32_t) * n_pairs);
+      WISP_HIP(hipMemcpyAsync(ctx->d_ids, ctx->ids_up, sizeof(int32_t) * n_pairs, hipMemcpyHostToDevice, sm),
+               "hipMemcpyAsync(ids)");
+      WISP_HIP(hipEventRecord(ctx->ids_ev, sm), "hipEventRecord(ids)");
+      ctx->ids_ev_recorded = true;
+      LaunchTiming tp = timing_begin(ctx, WISP_K_PERMUTE);
+      WISP_HIP(launch_permute_pairs(ctx->d_ids, n_pairs, N, ctx->d_perm, sm, tp), "permute launch");
+      timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(n_pairs) * 8);
+    }
   }
   const BlobLayout& B = ctx->blob;
   const uint64_t dI = static_cast<uint64_t>(B.d) * B.I;
@@ -1217,6 +1252,10 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
   }
   WISP_HIP(hipEventRecord(L.use_ev, sm), "hipEventRecord(use)");
   L.use_ev_recorded = true;
+  if (grouped) {
+    WISP_HIP(hipEventRecord(ctx->perm_use_ev, sm), "hipEventRecord(perm use)");
+    ctx->perm_use_recorded = true;
+  }
   L.pending = false;
   if (st) {
     st->hits = L.plan.hits;

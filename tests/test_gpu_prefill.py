@@ -9,7 +9,8 @@ the bf16 tolerance, and bit-identity with the fully resident run (C = N).
 import numpy as np
 import pytest
 
-from parity import run_case
+from parity import log, run_case
+from paper_2606_21868_amd import wisp
 from paper_2606_21868_amd.workloads import WORKLOADS
 
 torch = pytest.importorskip("torch")
@@ -55,3 +56,44 @@ def test_prefill_full_size_sampled():
     points = [(0, 0), (0, 17), (0, 30), (0, wl.L - 1)]
     out = run_case(wl, wl.cap, 1, sample_points=points, tokens=tokens, expect_grouped=True)
     assert int(out["misses"].sum()) == int((out["hits"] + out["misses"]).sum())   # a cold pass: all compulsory
+
+
+def test_prefill_layer_calls_in_any_order():
+    """wisp_route_topk orders a token batch's pairs by expert for the next forward of its layer.
+    Routing both layers before paging either (on a second stream) leaves the first layer's order
+    overwritten, so its forward orders the pairs itself: every order of the calls gives the bits of
+    wisp_decode_step."""
+    wl = WORKLOADS["qwen3-30b-a3b-prefill"].with_(L=2, T=64, d=256, I=128, N=16, k=4)
+    log(f"[case] layer calls in any order {wl.name} L={wl.L} T={wl.T}")
+    run = wisp.DecodeRun(wl, device=0, steps=1)
+    try:
+        run.generate()
+        run.set_cap(wl.N)
+        run.ctx.preload()
+        ref = run.decode(record=True, steps=1)
+        T, L, k = wl.T, wl.L, wl.k
+        s2 = torch.cuda.Stream(device=run.dev)
+        for order in ("route all, then page and forward", "route, page, forward per layer"):
+            idx = torch.zeros((L, T, k), dtype=torch.int32, device=run.dev)
+            w = torch.zeros((L, T, k), dtype=torch.float32, device=run.dev)
+            y = torch.zeros((L, T, wl.d), dtype=torch.float32, device=run.dev)
+            ids = [np.zeros(T * k, np.int32) for _ in range(L)]
+            torch.cuda.synchronize(run.dev)
+            if order.startswith("route all"):
+                for l in range(L):
+                    run.ctx.route_topk(l, run.x_dev[0, l], T, idx[l], w[l], ids[l], s2)
+                run.stream.wait_stream(s2)
+                for l in range(L):
+                    run.ctx.page_in(l, ids[l], T)
+                    run.ctx.moe_forward(l, run.x_dev[0, l], T, w[l], y[l], run.stream)
+            else:
+                for l in range(L):
+                    run.ctx.route_topk(l, run.x_dev[0, l], T, idx[l], w[l], ids[l], run.stream)
+                    run.ctx.page_in(l, ids[l], T)
+                    run.ctx.moe_forward(l, run.x_dev[0, l], T, w[l], y[l], run.stream)
+            run.stream.synchronize()
+            assert np.array_equal(idx.cpu().numpy(), ref["idx"][0]), order
+            assert np.array_equal(y.cpu().numpy().view(np.uint32), ref["y"][0].view(np.uint32)), order
+            log(f"  {order}: bit-identical to wisp_decode_step")
+    finally:
+        run.close()
