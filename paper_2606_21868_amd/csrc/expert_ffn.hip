@@ -473,35 +473,59 @@ __device__ __forceinline__ uint16_t swiglu_bf16(float a, float b) {
   return f32_to_bf16_rne(a / (1.0f + __expf(-a)) * b);
 }
 
+// One pass of the single-token body over rows [rbase, rbase + RPW) of the item's matrix.
 template <int MODE, int LPR, int NL>
-__global__ void __launch_bounds__(256) ffn_rows_t1(const FfnT1Batch B, const uint8_t* __restrict__ vin, int vin_stride,
-                                                   int K, int R, int rows_per_wg, int blocks_per_item, uint32_t off0,
-                                                   uint32_t off1, uint8_t* __restrict__ out, int out_stride) {
+__device__ __forceinline__ void t1_pass(const uint8_t* w, const uint4* xrow, int K, int rbase, int r_end, int r_first,
+                                        uint32_t off0, uint32_t off1, uint8_t* __restrict__ out, size_t out_row) {
   constexpr int RPW = 64 / LPR;
-  const int item = blockIdx.x / blocks_per_item;
-  const int rb = blockIdx.x - item * blocks_per_item;
-  const int r_begin = rb * rows_per_wg, r_end = min(R, r_begin + rows_per_wg);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63;
   const int sub = lane / LPR, sl = lane - sub * LPR;
-  const uint8_t* w = B.w[item];
   const size_t row_b = static_cast<size_t>(K) * 2;
+  const int r = rbase + sub;
+  const bool valid = r < r_end;
+  const int rr = valid ? r : r_first;
+  uint4 a[NL], b[NL], xr[NL];
+  t1_load<MODE, LPR, NL>(w, off0, off1, row_b, rr, sl, a, b);
+  t1_input<LPR, NL>(xrow, sl, xr);
+  float acc0, acc1;
+  t1_dot<MODE, LPR, NL>(a, b, xr, acc0, acc1);
+  if (valid && sl == 0) {
+    if constexpr (MODE == MODE_GATEUP)
+      reinterpret_cast<uint16_t*>(out)[out_row + r] = swiglu_bf16(acc0, acc1);
+    else
+      reinterpret_cast<float*>(out)[out_row + r] = acc0;
+  }
+  (void)RPW;
+}
+
+// Grid (row blocks, items): the item is blockIdx.y.  A kernel that follows another kernel starts
+// with cold instruction and scalar caches, so every dependent round trip before its first weight
+// load shows in its duration.  With ONE_PASS (a workgroup's rows_per_wg = 4 * RPW rows, one pass of
+// its four waves: every batch-1 decode launch) the body is straight-line, and the workgroup's
+// scalar loads, its item's blob address among them, go out together before anything waits.
+template <int MODE, int LPR, int NL, bool ONE_PASS>
+__global__ void __launch_bounds__(256) ffn_rows_t1(const FfnT1Batch B, const uint8_t* __restrict__ vin, int vin_stride,
+                                                   int K, int R, int rows_per_wg, uint32_t off0, uint32_t off1,
+                                                   uint8_t* __restrict__ out, int out_stride) {
+  constexpr int RPW = 64 / LPR;
+  const int item = blockIdx.y;
+  const int wave = threadIdx.x >> 6;
+  const uint8_t* w = B.w[item];
   const uint4* xrow = reinterpret_cast<const uint4*>(vin + static_cast<size_t>(B.row[item]) * vin_stride * 2);
-  for (int rbase = r_begin + wave * RPW; rbase < r_end; rbase += 4 * RPW) {
-    const int r = rbase + sub;
-    const bool valid = r < r_end;
-    const int rr = valid ? r : r_begin;
-    uint4 a[NL], b[NL], xr[NL];
-    t1_load<MODE, LPR, NL>(w, off0, off1, row_b, rr, sl, a, b);
-    t1_input<LPR, NL>(xrow, sl, xr);
-    float acc0, acc1;
-    t1_dot<MODE, LPR, NL>(a, b, xr, acc0, acc1);
-    if (valid && sl == 0) {
-      const size_t o = static_cast<size_t>(B.out[item]) * out_stride + r;
-      if constexpr (MODE == MODE_GATEUP)
-        reinterpret_cast<uint16_t*>(out)[o] = swiglu_bf16(acc0, acc1);
-      else
-        reinterpret_cast<float*>(out)[o] = acc0;
-    }
+  const size_t out_row = static_cast<size_t>(B.out[item]) * out_stride;
+  if constexpr (ONE_PASS) {
+    // K = LPR * NL chunks of 8 bf16 and rows_per_wg = 4 * RPW are fixed by the instantiation, so
+    // nothing but R waits on a kernel argument before the addresses are formed
+    constexpr int KC = LPR * NL * 8;
+    const int r_begin = blockIdx.x * 4 * RPW;
+    t1_pass<MODE, LPR, NL>(w, xrow, KC, r_begin + wave * RPW, min(R, r_begin + 4 * RPW), r_begin, off0, off1, out,
+                           out_row);
+    (void)K;
+    (void)rows_per_wg;
+  } else {
+    const int r_begin = blockIdx.x * rows_per_wg, r_end = min(R, r_begin + rows_per_wg);
+    for (int rbase = r_begin + wave * RPW; rbase < r_end; rbase += 4 * RPW)
+      t1_pass<MODE, LPR, NL>(w, xrow, K, rbase, r_end, r_begin, off0, off1, out, out_row);
   }
 }
 
@@ -514,35 +538,77 @@ __global__ void __launch_bounds__(256) ffn_rows_t1(const FfnT1Batch B, const uin
 // leaves the chip, and a layer-step needs one launch less.  Each o_j is t1_dot's chain and the sum
 // is the combine kernel's fmaf chain, so y has the same bits as down + combine.
 // ------------------------------------------------------------------------------------------
-template <int LPR, int NL, int MAXW>
-__device__ __forceinline__ void down_combine_t1(int n, const uint8_t* const* w, const int32_t* rank, const uint8_t* h,
-                                                const float* __restrict__ gates, float* __restrict__ y, int d, int I,
-                                                int k, int has_shared, uint32_t off2, float* o_lds) {
+// Where the items of a single-token down + combine come from: the launch's kernel argument (host
+// pager) or the plan the device pager wrote to HBM (read straight from there: a scalar load of
+// memory another kernel wrote is coherent, since every kernel starts with its caches invalidated).
+struct ArgItems {
+  const FusedT1Items& b;
+  __device__ int n() const { return b.n_items; }
+  __device__ const uint8_t* w(int i) const { return b.w[i]; }
+  __device__ int32_t rank(int i) const { return b.rank[i]; }
+};
+struct PlanItems {
+  const FfnBatch* p;
+  __device__ int n() const { return p->n_items; }
+  __device__ const uint8_t* w(int i) const { return p->items[i].w; }
+  __device__ int32_t rank(int i) const { return p->items[i].out[0]; }   // single-token items: the rank
+};
+
+template <int LPR, int NL, int MAXW, typename Items>
+__device__ __forceinline__ void down_combine_t1(const Items& items, const uint8_t* h, const float* __restrict__ gates,
+                                                float* __restrict__ y, int d, int I, int k, int has_shared,
+                                                uint32_t off2, float* o_lds) {
   constexpr int RPW = 64 / LPR;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  static_assert(4 * MAXW <= kMaxItems, "the item arrays hold every index read below");
+  static_assert(MAXW == 3, "the scalar hold below names three experts per wave");
+  // The wave index is uniform, so the experts' addresses and ranks are scalar values.  They are read
+  // (entries past n exist in both item arrays and are never dereferenced) together with the other scalars
+  // the loads need, and held in scalar registers by one empty asm statement, so the workgroup waits
+  // once for all of them; otherwise the compiler sinks each into its branch below and the branches
+  // wait one after the other.  I is LPR * NL * 8 for every instantiation (the launcher's shapes).
+  constexpr size_t row_b = static_cast<size_t>(LPR) * NL * 16;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int sub = lane / LPR, sl = lane - sub * LPR;
+  uint32_t lo[MAXW], hi[MAXW];
+  int32_t rq[MAXW];
+#pragma unroll
+  for (int q = 0; q < MAXW; ++q) {
+    const uint64_t p = reinterpret_cast<uint64_t>(items.w(wave + 4 * q));
+    lo[q] = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(p));
+    hi[q] = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(p >> 32));
+    rq[q] = __builtin_amdgcn_readfirstlane(items.rank(wave + 4 * q));
+  }
+  int n_s = __builtin_amdgcn_readfirstlane(items.n()), d_s = d;
+  uint32_t off2_s = off2;
+  asm volatile("" : "+s"(lo[0]), "+s"(hi[0]), "+s"(rq[0]), "+s"(lo[1]), "+s"(hi[1]), "+s"(rq[1]), "+s"(lo[2]),
+               "+s"(hi[2]), "+s"(rq[2]), "+s"(n_s), "+s"(d_s), "+s"(off2_s));
+  typedef const __attribute__((address_space(1))) uint8_t* global_bytes;
+  const uint8_t* wq[MAXW];
+#pragma unroll
+  for (int q = 0; q < MAXW; ++q)   // back to global-memory pointers, so the loads stay global loads
+    wq[q] = (const uint8_t*)reinterpret_cast<global_bytes>((static_cast<uint64_t>(hi[q]) << 32) | lo[q]);
   const int r0 = blockIdx.x * RPW;
   const int r = r0 + sub;
-  const int rr = r < d ? r : r0;
-  const size_t row_b = static_cast<size_t>(I) * 2;
+  const int rr = r < d_s ? r : r0;
+  (void)I;
   uint4 a[MAXW][NL], xr[MAXW][NL];
 #pragma unroll
   for (int q = 0; q < MAXW; ++q) {
     const int i = wave + 4 * q;
-    if (i < n) t1_load<MODE_DOWN, LPR, NL>(w[i], off2, off2, row_b, rr, sl, a[q], a[q]);
+    if (i < n_s) t1_load<MODE_DOWN, LPR, NL>(wq[q], off2_s, off2_s, row_b, rr, sl, a[q], a[q]);
   }
 #pragma unroll
   for (int q = 0; q < MAXW; ++q) {
     const int i = wave + 4 * q;
-    if (i < n) t1_input<LPR, NL>(reinterpret_cast<const uint4*>(h + static_cast<size_t>(rank[i]) * row_b), sl, xr[q]);
+    if (i < n_s) t1_input<LPR, NL>(reinterpret_cast<const uint4*>(h + static_cast<size_t>(rq[q]) * row_b), sl, xr[q]);
   }
 #pragma unroll
   for (int q = 0; q < MAXW; ++q) {
     const int i = wave + 4 * q;
-    if (i >= n) continue;
+    if (i >= n_s) continue;
     float acc0, acc1;
     t1_dot<MODE_DOWN, LPR, NL>(a[q], a[q], xr[q], acc0, acc1);
-    if (sl == 0) o_lds[rank[i] * RPW + sub] = acc0;
+    if (sl == 0) o_lds[rq[q] * RPW + sub] = acc0;
   }
   __syncthreads();
   if (tid < RPW && r0 + tid < d) {
@@ -559,7 +625,7 @@ __global__ void __launch_bounds__(256) ffn_down_combine_t1(const FusedT1Items B,
                                                            const float* __restrict__ gates, float* __restrict__ y,
                                                            int d, int I, int k, int has_shared, uint32_t off2) {
   __shared__ float o_lds[9 * 64];
-  down_combine_t1<LPR, NL, MAXW>(B.n_items, B.w, B.rank, h, gates, y, d, I, k, has_shared, off2, o_lds);
+  down_combine_t1<LPR, NL, MAXW>(ArgItems{B}, h, gates, y, d, I, k, has_shared, off2, o_lds);
 }
 
 // device-planned: the experts of the plan the device pager wrote (single-token items; the output
@@ -569,22 +635,14 @@ __global__ void __launch_bounds__(256) ffn_down_combine_dev(const FfnBatch* __re
                                                             const float* __restrict__ gates, float* __restrict__ y,
                                                             int d, int I, int k, int has_shared, uint32_t off2) {
   __shared__ float o_lds[9 * 64];
-  __shared__ const uint8_t* w[kMaxItems];
-  __shared__ int32_t rank[kMaxItems];
-  const int n = P->n_items;
-  if (threadIdx.x < n) {
-    w[threadIdx.x] = P->items[threadIdx.x].w;
-    rank[threadIdx.x] = P->items[threadIdx.x].out[0];
-  }
-  __syncthreads();
-  down_combine_t1<LPR, NL, MAXW>(n, w, rank, h, gates, y, d, I, k, has_shared, off2, o_lds);
+  down_combine_t1<LPR, NL, MAXW>(PlanItems{P}, h, gates, y, d, I, k, has_shared, off2, o_lds);
 }
 
-using T1Kernel = void (*)(const FfnT1Batch, const uint8_t*, int, int, int, int, int, uint32_t, uint32_t, uint8_t*, int);
+using T1Kernel = void (*)(const FfnT1Batch, const uint8_t*, int, int, int, int, uint32_t, uint32_t, uint8_t*, int);
 
-T1Kernel pick_t1(int mode, int lpr, int nl) {
+T1Kernel pick_t1(int mode, int lpr, int nl, bool one_pass) {
 #define WISP_T1(M, L, N) \
-  if (mode == M && lpr == L && nl == N) return &ffn_rows_t1<M, L, N>;
+  if (mode == M && lpr == L && nl == N) return one_pass ? &ffn_rows_t1<M, L, N, true> : &ffn_rows_t1<M, L, N, false>;
   WISP_T1(MODE_GATEUP, 64, 4) WISP_T1(MODE_GATEUP, 64, 8) WISP_T1(MODE_DOWN, 32, 3) WISP_T1(MODE_DOWN, 64, 28)
   WISP_T1(MODE_DOWN, 32, 1) WISP_T1(MODE_DOWN, 16, 1) WISP_T1(MODE_DOWN, 16, 3) WISP_T1(MODE_GATEUP, 32, 1)
   WISP_T1(MODE_GATEUP, 16, 3)
@@ -674,7 +732,7 @@ hipError_t launch_rows(int mode, const FfnBatch& b, const FfnShape& s, const voi
   const uint32_t off0 = static_cast<uint32_t>(mode == MODE_GATEUP ? L.off_w1 : L.off_w2);
   const uint32_t off1 = static_cast<uint32_t>(mode == MODE_GATEUP ? L.off_w3 : L.off_w2);
   if (b.max_ntok == 1 && WT == DT_BF16 && IT == DT_BF16) {
-    if (T1Kernel k1 = pick_t1(mode, lpr, nl)) {
+    if (T1Kernel k1 = pick_t1(mode, lpr, nl, rows_per_wg == step)) {
       FfnT1Batch t1;
       t1.n_items = b.n_items;
       for (int i = 0; i < b.n_items; ++i) {
@@ -682,9 +740,9 @@ hipError_t launch_rows(int mode, const FfnBatch& b, const FfnShape& s, const voi
         t1.row[i] = mode == MODE_GATEUP ? b.items[i].tok[0] : b.items[i].out[0];
         t1.out[i] = b.items[i].out[0];
       }
-      dim3 grid(static_cast<unsigned>(b.n_items * bpi)), block(256);
+      dim3 grid(static_cast<unsigned>(bpi), static_cast<unsigned>(b.n_items)), block(256);
       hipExtLaunchKernelGGL(k1, grid, block, 0, st, tm.start, tm.stop, 0, t1, static_cast<const uint8_t*>(vin),
-                            vin_stride, K, R, rows_per_wg, bpi, off0, off1, static_cast<uint8_t*>(out), out_stride);
+                            vin_stride, K, R, rows_per_wg, off0, off1, static_cast<uint8_t*>(out), out_stride);
       return hipGetLastError();
     }
   }
