@@ -61,15 +61,18 @@ __device__ __forceinline__ TableRegs load_table_regs(int N, int C, const int32_t
                                                      const uint64_t* __restrict__ tau,
                                                      const uint64_t* __restrict__ clock,
                                                      const uint64_t* __restrict__ slot_ptr) {
+  // every thread loads (indices clamped into the tables) and keeps only its own entries: with no
+  // load behind a branch, the loads go out together and nothing waits for them here
   const int tid = threadIdx.x;
-  TableRegs r{-1, -1, 0, 0, 0};
-  if (tid < N) r.pi = pi[tid];
-  if (tid < C) {
-    r.pinv = pinv[tid];
-    r.tau = tau[tid];
-    r.slot = slot_ptr[tid];
-  }
-  if (tid == 0) r.clock = *clock;
+  const int ie = min(tid, N - 1), is = min(tid, C - 1);
+  const int32_t v_pi = pi[ie], v_pinv = pinv[is];
+  const uint64_t v_tau = tau[is], v_slot = slot_ptr[is], v_clock = *clock;
+  TableRegs r;
+  r.pi = tid < N ? v_pi : -1;
+  r.pinv = tid < C ? v_pinv : -1;
+  r.tau = tid < C ? v_tau : 0;
+  r.slot = tid < C ? v_slot : 0;
+  r.clock = tid == 0 ? v_clock : 0;
   return r;
 }
 

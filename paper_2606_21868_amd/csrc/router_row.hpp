@@ -35,15 +35,22 @@ __device__ __forceinline__ float router_row(const float* __restrict__ wr, const 
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   // the thread's chunks c = tid, tid + 256, ... in groups of U whose row loads are all issued before
   // the first FMA (one HBM round trip per group, not per chunk); each acc[t] is still one FMA chain
-  // in ascending chunk order
+  // in ascending chunk order.  The first group covers every d up to 256 * U * 4 = 4096; it runs
+  // outside the loop so that its row loads also overlap with whatever the caller issued before
+  // (inside a loop they would wait for those first).
   constexpr int U = 4;
-  for (int c0 = threadIdx.x; c0 < chunks; c0 += 256 * U) {
-    float4 w[U];
+  auto group = [&](int c0) {
+    float4 wv[U], xf[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int c = c0 + u * 256;
-      w[u] = c < chunks ? row[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      wv[u] = c < chunks ? row[c] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
+    // the first token's inputs go out with the row (a chunk past the last reads the last one again:
+    // in bounds, never used), so a single-token step waits once
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      xf[u] = load_x4<XT>(x, static_cast<size_t>(t0) * d + static_cast<size_t>(min(c0 + u * 256, chunks - 1)) * 4);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int c = c0 + u * 256;
@@ -51,14 +58,17 @@ __device__ __forceinline__ float router_row(const float* __restrict__ wr, const 
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         if (t >= ntok) break;
-        const float4 v = load_x4<XT>(x, static_cast<size_t>(t0 + t) * d + static_cast<size_t>(c) * 4);
-        acc[t] = fmaf(w[u].x, v.x, acc[t]);
-        acc[t] = fmaf(w[u].y, v.y, acc[t]);
-        acc[t] = fmaf(w[u].z, v.z, acc[t]);
-        acc[t] = fmaf(w[u].w, v.w, acc[t]);
+        const float4 v =
+            t == 0 ? xf[u] : load_x4<XT>(x, static_cast<size_t>(t0 + t) * d + static_cast<size_t>(c) * 4);
+        acc[t] = fmaf(wv[u].x, v.x, acc[t]);
+        acc[t] = fmaf(wv[u].y, v.y, acc[t]);
+        acc[t] = fmaf(wv[u].z, v.z, acc[t]);
+        acc[t] = fmaf(wv[u].w, v.w, acc[t]);
       }
     }
-  }
+  };
+  group(threadIdx.x);
+  for (int c0 = threadIdx.x + 256 * U; c0 < chunks; c0 += 256 * U) group(c0);
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     if (t >= ntok) break;
