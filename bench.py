@@ -360,6 +360,9 @@ def prefill_leg(wisp, torch, link, link_cu=None, passes=3):
                 gms += t["total_ms"]
             kern[wisp.KERNEL_CLASS_NAMES[kc]] = e
         achieved = gflops / (gms * 1e-3) / 1e12 if gms > 0 else None
+        mfma_peak = wisp.probe_mfma(10)   # the vendor's dense bf16 peak, checked on this chip
+        log(f"prefill: matrix cores sustain {mfma_peak:.0f} TFLOP/s of dense bf16 on register operands "
+            f"({mfma_peak / MFMA_BF16_PEAK_TFLOPS:.3f} of the 2.5 PFLOP/s peak)")
         rtimes.sort()
         rel = rtimes[len(rtimes) // 2]
         log(f"prefill: resident pass {rel * 1e3:.2f} ms -> {wl.T / rel:.0f} tokens/s; grouped GEMMs "
@@ -374,7 +377,9 @@ def prefill_leg(wisp, torch, link, link_cu=None, passes=3):
             resident=dict(tokens_per_s=wl.T / rel, pass_ms=rel * 1e3, kernels=kern),
             mfma=dict(bound="mfma", achieved=achieved, peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
                       frac=achieved / MFMA_BF16_PEAK_TFLOPS if achieved else None,
-                      kernels="grouped gate/up + down (bf16 v_mfma_f32_32x32x16), resident pass"),
+                      kernels="grouped gate/up + down (bf16 v_mfma_f32_32x32x16), resident pass",
+                      peak_measured=mfma_peak, frac_of_measured_peak=achieved / mfma_peak if achieved else None,
+                      peak_method="wisp_probe_mfma: register-only v_mfma_f32_32x32x16_bf16 stream, 8 waves per SIMD"),
             # at ~128 rows per expert the grouped GEMMs do ~100 FLOP per weight byte, below the bf16
             # ridge (2.5 PFLOP/s / 8 TB/s = 312): HBM is their bound
             hbm=dict(bound="hbm", achieved=gbytes / (gms * 1e-3) / 1e9 if gms > 0 else None, peak=HBM_PEAK_GBPS,

@@ -265,6 +265,12 @@ wisp_status wisp_hbm_copy(const void* src, void* dst, uint64_t bytes, void* stre
  * and stream (WISP_E_NOMEM when the buffer does not fit). */
 wisp_status wisp_probe_hbm_read(uint64_t bytes, int32_t launches, double* us_per_launch);
 
+/* The dense bf16 matrix-core rate the current device sustains: `launches` back-to-back launches of a
+ * kernel whose waves (eight per SIMD) issue only v_mfma_f32_32x32x16_bf16 on register operands, four
+ * independent chains per wave; returns TFLOP/s (1e12 flops/s, 2*32*32*16 flops per instruction).
+ * launches >= 1 (WISP_E_INVAL otherwise).  Allocates and frees a 256-byte sink and its own stream. */
+wisp_status wisp_probe_mfma(int32_t launches, double* tflops);
+
 /* Decode n fp8 E4M3 codes to fp32 on the device with the same conversion the FFN kernels use
  * (for checking the hardware conversion against the format definition). */
 wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n, void* stream);

@@ -1795,6 +1795,41 @@ wisp_status wisp_probe_hbm_read(uint64_t bytes, int32_t launches, double* us_per
   return WISP_OK;
 }
 
+wisp_status wisp_probe_mfma(int32_t launches, double* tflops) {
+  if (launches < 1 || !tflops) return fail(WISP_E_INVAL, "launches >= 1 and a result pointer required");
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    return fail(WISP_E_HIP, "device attributes");
+  const int wgs = cus * 8, iters = 2048;   // eight waves per SIMD, ≈1 ms per launch
+  float* sink = nullptr;
+  if (hipMalloc(reinterpret_cast<void**>(&sink), 256) != hipSuccess) {
+    hipGetLastError();
+    return fail(WISP_E_NOMEM, "probe sink allocation failed");
+  }
+  hipStream_t st = nullptr;
+  hipEvent_t a = nullptr, b = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreate(&a);
+  if (e == hipSuccess) e = hipEventCreate(&b);
+  for (int i = 0; i < 2 && e == hipSuccess; ++i) e = launch_mfma_peak(wgs, iters, sink, st);
+  if (e == hipSuccess) e = hipEventRecord(a, st);
+  for (int i = 0; i < launches && e == hipSuccess; ++i) e = launch_mfma_peak(wgs, iters, sink, st);
+  if (e == hipSuccess) e = hipEventRecord(b, st);
+  if (e == hipSuccess) e = hipEventSynchronize(b);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+  if (st) hipStreamSynchronize(st);
+  if (a) hipEventDestroy(a);
+  if (b) hipEventDestroy(b);
+  if (st) hipStreamDestroy(st);
+  hipFree(sink);
+  if (e != hipSuccess) return fail(WISP_E_HIP, std::string("matrix-core probe: ") + hipGetErrorString(e));
+  const double flops = static_cast<double>(launches) * wgs * 4 /* waves */ * iters * 4 /* chains */ * 2.0 * 32 * 32 * 16;
+  *tflops = flops / (static_cast<double>(ms) * 1e-3) / 1e12;
+  return WISP_OK;
+}
+
 wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n, void* stream) {
   if (!codes_dev || !out_dev || n < 0) return fail(WISP_E_INVAL, "bad argument");
   WISP_HIP(launch_decode_fp8(codes_dev, out_dev, n, static_cast<hipStream_t>(stream)), "decode launch");

@@ -163,6 +163,8 @@ hipError_t launch_fill(const FillList& fl, uint64_t bytes, hipStream_t st, const
 hipError_t launch_hbm_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
 // A streaming read of `bytes` (a multiple of 16) from src; sink receives at most one word.
 hipError_t launch_hbm_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t st);
+// wgs workgroups of 256 threads, each wave 4 * iters bf16 32x32x16 matrix-core instructions on registers.
+hipError_t launch_mfma_peak(int wgs, int iters, float* sink, hipStream_t st);
 hipError_t launch_decode_fp8(const uint8_t* codes, float* out, int n, hipStream_t st);
 
 }  // namespace wisp

@@ -1,6 +1,7 @@
 // Yardsticks: a plain device copy with 16-byte loads and stores (for HBM byte counters, FETCH_SIZE /
-// WRITE_SIZE per copied byte, and the achievable copy bandwidth), and a plain streaming read (the
-// read time of a launch of a given size, the floor of any kernel that must read those bytes).
+// WRITE_SIZE per copied byte, and the achievable copy bandwidth), a plain streaming read (the read
+// time of a launch of a given size, the floor of any kernel that must read those bytes), and a
+// register-only stream of bf16 matrix-core instructions (the dense bf16 rate the chip sustains).
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
@@ -33,7 +34,38 @@ __global__ void __launch_bounds__(256) hbm_read_kernel(const u32x4_t* __restrict
   if (acc == 0x9e3779b9u) sink[0] = acc;
 }
 
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// Every wave runs `iters` rounds of four independent v_mfma_f32_32x32x16_bf16 chains on register
+// operands (2 * 32 * 32 * 16 flops each); nothing touches memory but a store that happens only if
+// the folded result equals an arbitrary constant.
+__global__ void __launch_bounds__(256) mfma_peak_kernel(int iters, float* sink) {
+  bf16x8_t a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = static_cast<__bf16>(static_cast<float>((threadIdx.x + i) & 7) * 0.125f);
+    b[i] = static_cast<__bf16>(static_cast<float>((threadIdx.x * 3 + i) & 7) * 0.0625f);
+  }
+  f32x16_t c0 = {}, c1 = {}, c2 = {}, c3 = {};
+  for (int it = 0; it < iters; ++it) {
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a, c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, a, c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, b, c3, 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) s += c0[r] + c1[r] + c2[r] + c3[r];
+  if (s == 1234.5f) sink[0] = s;
+}
+
 }  // namespace
+
+hipError_t launch_mfma_peak(int wgs, int iters, float* sink, hipStream_t st) {
+  hipLaunchKernelGGL(mfma_peak_kernel, dim3(static_cast<unsigned>(wgs)), dim3(256), 0, st, iters, sink);
+  return hipGetLastError();
+}
 
 hipError_t launch_hbm_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t st) {
   if (bytes == 0) return hipSuccess;

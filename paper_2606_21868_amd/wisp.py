@@ -118,6 +118,7 @@ _SIGS = {
     "wisp_probe_h2d_engine": [_P, _I, _I, _I, ctypes.POINTER(ctypes.c_double)],
     "wisp_hbm_copy": [_P, _P, _U64, _P],
     "wisp_probe_hbm_read": [_U64, _I, ctypes.POINTER(ctypes.c_double)],
+    "wisp_probe_mfma": [_I, ctypes.POINTER(ctypes.c_double)],
     "wisp_decode_fp8": [_P, _P, _I, _P],
     "wisp_debug_fail_slot_alloc": [_P, _I],
     "wisp_predictor_create": [_I, _I, _I, ctypes.c_double, ctypes.POINTER(_P)],
@@ -413,6 +414,13 @@ def probe_hbm_read(nbytes, launches):
     us = ctypes.c_double()
     check(lib().wisp_probe_hbm_read(int(nbytes), int(launches), ctypes.byref(us)), "wisp_probe_hbm_read")
     return us.value
+
+
+def probe_mfma(launches):
+    """Dense bf16 matrix-core TFLOP/s the device sustains on register operands (wisp_probe_mfma)."""
+    tf = ctypes.c_double()
+    check(lib().wisp_probe_mfma(int(launches), ctypes.byref(tf)), "wisp_probe_mfma")
+    return tf.value
 
 
 def hbm_copy(src, dst, nbytes, stream=None):

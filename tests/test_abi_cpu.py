@@ -67,6 +67,12 @@ def test_invalid_descriptions_rejected_before_any_gpu_call():
         wisp.Context(d)
 
 
+def test_matrix_core_probe_rejects_bad_counts_before_any_gpu_call():
+    with pytest.raises(wisp.WispError) as ei:
+        wisp.probe_mfma(0)
+    assert ei.value.status == wisp.E_INVAL
+
+
 def test_read_probe_rejects_bad_sizes_before_any_gpu_call():
     for nbytes, launches in ((0, 1), (15, 1), (24, 1), ((1 << 32) + 16, 1), (4096, 0)):
         with pytest.raises(wisp.WispError) as ei:

@@ -149,3 +149,13 @@ def test_read_floor_probe():
         rate = nbytes / (us * 1e-6) / 1e9
         assert 500 < rate < 8000, (nbytes, us, rate)
     assert large > small
+
+
+def test_matrix_core_probe():
+    # the register-only bf16 MFMA stream runs near the chip's dense peak (2.5 PFLOP/s at 2.4 GHz)
+    tf = wisp.probe_mfma(3)
+    log(f"  matrix cores: {tf:.0f} TFLOP/s dense bf16")
+    assert 500 < tf < 2800, tf
+    with pytest.raises(wisp.WispError) as ei:
+        wisp.probe_mfma(0)
+    assert ei.value.status == wisp.E_INVAL
