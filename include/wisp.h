@@ -141,7 +141,8 @@ wisp_status wisp_set_pager(wisp_ctx* ctx, int32_t pager);
 /* Route T tokens of `layer`: x_dev [T, d] (x_dtype) -> idx_dev [T, k] int32 and w_dev [T, k] fp32
  * on `stream`, ranks ordered (score desc, expert id asc).  If idx_host is not NULL the call
  * waits for the indices and copies them there (T*k int32): this is the one device->host
- * synchronisation of a layer-step, needed because the pager runs on the host.  For a token batch
+ * synchronisation of a layer-step, needed because the pager runs on the host (the selection kernel
+ * writes the ids, tagged with a per-call sequence number, straight to host-coherent memory).  For a token batch
  * that takes the grouped FFN, the call also enqueues, after the copy, the ordering of the (token,
  * rank) pairs by expert from idx_dev; the next wisp_moe_forward of this layer uses that order when
  * it is handed the same ids through wisp_page_in, and otherwise orders the pairs itself. */

@@ -99,11 +99,9 @@ struct wisp_ctx {
   int32_t cap = 0;
   std::vector<LayerState> layers;
   hipStream_t side = nullptr;
-  hipEvent_t route_ev = nullptr;
   float* logits = nullptr;
   void* h = nullptr;
   float* buf = nullptr;
-  int32_t* idx_pinned = nullptr;     // pinned staging for the copy-based id transfer
   uint64_t* idx_tagged = nullptr;    // host-coherent (seq << 32 | id) words written by the router
   uint32_t route_seq = 0;
   int32_t profile_mask = 0;          // kernel classes timed when profiling
@@ -308,12 +306,11 @@ void free_ctx(wisp_ctx* c) {
     if (p) c->pageable ? (void)munmap(p, c->master_stride) : (void)hipHostFree(p);
   for (auto& t : c->timed) { hipEventDestroy(t.a); hipEventDestroy(t.b); }
   for (auto e : c->ev_pool) hipEventDestroy(e);
-  if (c->route_ev) hipEventDestroy(c->route_ev);
   if (c->side) hipStreamDestroy(c->side);
   if (c->logits) hipFree(c->logits);
   if (c->h) hipFree(c->h);
   if (c->buf) hipFree(c->buf);
-  if (c->idx_pinned) hipHostFree(c->idx_pinned);
+  if (c->idx_tagged) hipHostFree(c->idx_tagged);
   if (c->ids_up) hipHostFree(c->ids_up);
   if (c->d_ids) hipFree(c->d_ids);
   if (c->d_perm) hipFree(c->d_perm);
@@ -670,8 +667,6 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   }
   if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess)
     return bail(WISP_E_HIP, "hipStreamCreateWithFlags failed");
-  if (hipEventCreateWithFlags(&c->route_ev, hipEventDisableTiming) != hipSuccess)
-    return bail(WISP_E_HIP, "hipEventCreate failed");
   void* p = nullptr;
   if (hipMalloc(&p, sizeof(float) * static_cast<size_t>(T) * N) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
   c->logits = static_cast<float*>(p);
@@ -679,11 +674,9 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   if (hipMalloc(&c->h, rows * desc->d_ff * c->h_elem()) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
   if (hipMalloc(&p, rows * desc->d_model * sizeof(float)) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
   c->buf = static_cast<float*>(p);
-  const size_t ids_bytes = round_up(sizeof(int32_t) * static_cast<size_t>(T) * k, 256);
-  if (hipHostMalloc(&p, ids_bytes + sizeof(uint64_t) * static_cast<size_t>(T) * k, hipHostMallocCoherent) != hipSuccess)
+  if (hipHostMalloc(&p, sizeof(uint64_t) * static_cast<size_t>(T) * k, hipHostMallocCoherent) != hipSuccess)
     return bail(WISP_E_NOMEM, "pinned scratch");
-  c->idx_pinned = static_cast<int32_t*>(p);
-  c->idx_tagged = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(p) + ids_bytes);
+  c->idx_tagged = static_cast<uint64_t*>(p);
   std::memset(c->idx_tagged, 0, sizeof(uint64_t) * static_cast<size_t>(T) * k);
   c->ids_scratch.resize(static_cast<size_t>(T) * k);
   const size_t pairs_bytes = sizeof(int32_t) * static_cast<size_t>(T) * k;
@@ -938,8 +931,10 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
   if (!L.wr) return fail(WISP_E_STATE, "router weights not set for this layer");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const auto& d = ctx->desc;
-  // decode: the router publishes tagged ids to host-coherent memory
-  const bool publish = idx_host && T <= 4;
+  // the ids reach the host through host-coherent memory: the selection writes each one as a 64-bit
+  // word tagged with this call's sequence number, so the host needs no copy, event or fence (a copy
+  // queue's start latency was ≈10 µs of every token batch's layer-step)
+  const bool publish = idx_host != nullptr;
   const uint32_t seq = publish ? ++ctx->route_seq : 0;
   if (ctx->fusion && T <= 4) {
     // logits and selection in one launch (the workgroup completing the logits selects)
@@ -966,6 +961,18 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
   }
   if (publish) {
     const int n = T * d.top_k;
+    // a token batch for the grouped FFN: its pairs are ordered by expert now, from the device ids,
+    // while the host waits for the ids and pages the layer in (after the last reader of the order)
+    const bool early = T >= kGroupedMinTokens && grouped_supported(ctx->shape, d.has_shared);
+    if (early) {
+      ctx->perm_layer = -1;
+      if (ctx->perm_use_recorded) WISP_HIP(hipStreamWaitEvent(st, ctx->perm_use_ev, 0), "hipStreamWaitEvent(perm use)");
+      LaunchTiming tp = timing_begin(ctx, WISP_K_PERMUTE);
+      WISP_HIP(launch_permute_pairs(idx_dev, n, d.n_experts, ctx->d_perm, st, tp), "permute launch");
+      timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(n) * 8);
+      WISP_HIP(hipEventRecord(ctx->perm_ev, st), "hipEventRecord(perm)");
+      ctx->perm_ev_recorded = true;
+    }
     // spin until every entry carries this call's tag: the wait on the critical path of a layer-step
     uint64_t spins = 0;
     for (int i = 0; i < n; ++i) {
@@ -982,31 +989,8 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
       }
       idx_host[i] = static_cast<int32_t>(v & 0xFFFFFFFFu);
     }
-    if (ctx->profiling) harvest(ctx, false);
-  } else if (idx_host) {
-    const size_t nb = sizeof(int32_t) * static_cast<size_t>(T) * d.top_k;
-    WISP_HIP(hipMemcpyAsync(ctx->idx_pinned, idx_dev, nb, hipMemcpyDeviceToHost, st), "hipMemcpyAsync(idx)");
-    WISP_HIP(hipEventRecord(ctx->route_ev, st), "hipEventRecord(route)");
-    // a token batch for the grouped FFN: its pairs are ordered by expert now, from the device ids,
-    // while the host waits for the ids and pages the layer in (after the last reader of the order)
-    const bool early = T >= kGroupedMinTokens && grouped_supported(ctx->shape, d.has_shared);
     if (early) {
-      ctx->perm_layer = -1;
-      if (ctx->perm_use_recorded) WISP_HIP(hipStreamWaitEvent(st, ctx->perm_use_ev, 0), "hipStreamWaitEvent(perm use)");
-      LaunchTiming tp = timing_begin(ctx, WISP_K_PERMUTE);
-      WISP_HIP(launch_permute_pairs(idx_dev, T * d.top_k, d.n_experts, ctx->d_perm, st, tp), "permute launch");
-      timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(T) * d.top_k * 8);
-      WISP_HIP(hipEventRecord(ctx->perm_ev, st), "hipEventRecord(perm)");
-      ctx->perm_ev_recorded = true;
-    }
-    // spin: this wait is on the critical path of every layer-step
-    hipError_t q;
-    while ((q = hipEventQuery(ctx->route_ev)) == hipErrorNotReady) {
-    }
-    if (q != hipSuccess) return fail(WISP_E_HIP, std::string("route event: ") + hipGetErrorString(q));
-    std::memcpy(idx_host, ctx->idx_pinned, nb);
-    if (early) {
-      ctx->perm_ids.assign(ctx->idx_pinned, ctx->idx_pinned + static_cast<size_t>(T) * d.top_k);
+      ctx->perm_ids.assign(idx_host, idx_host + n);
       ctx->perm_layer = layer;
       ctx->perm_T = T;
     }
