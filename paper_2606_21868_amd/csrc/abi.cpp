@@ -1010,9 +1010,11 @@ wisp_status wisp_page_in(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, 
   LayerState& L = ctx->layers[layer];
   if (L.pending) return fail(WISP_E_STATE, "previous page-in of this layer not consumed by wisp_moe_forward");
   const int32_t n = T * ctx->desc.top_k;
-  for (int32_t i = 0; i < n; ++i)
-    if (ids_host[i] < 0 || ids_host[i] >= ctx->desc.n_experts) return fail(WISP_E_INVAL, "expert id out of range");
   if (!L.pf_unused.empty()) {
+    // the prefetch bookkeeping indexes by id: validate first (otherwise the slot table's step validates
+    // every id before it changes anything)
+    for (int32_t i = 0; i < n; ++i)
+      if (ids_host[i] < 0 || ids_host[i] >= ctx->desc.n_experts) return fail(WISP_E_INVAL, "expert id out of range");
     // prefetched experts this page-in routes to while they are still resident
     std::vector<uint8_t>& mk = ctx->pf_mark;
     for (int32_t e : L.pf_unused) mk[e] = 1;
