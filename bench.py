@@ -14,12 +14,14 @@ Reported beside the throughput:
                  bytes per launch / average launch time from HIP events over the timed region,
                  against the 8 TB/s HBM peak;
   path_roofline  the whole path against T_roof = sum over layer-steps of HBM bytes / 8 TB/s +
-                 fault bytes / measured host-link bandwidth (exact fault counts of the run);
+                 fault bytes / measured host-link bandwidth of the engine that moves them (compute-unit
+                 streaming for the device pager, the copy engine for the host pager; exact fault counts
+                 of the run);
   cpu_baseline   the fp64 CPU oracle (fully resident layer) on a bounded sample of the same
                  workload, on this host's cores;
-  sweep          at per-layer caps 8..128, the pager against static layer-level offload (whole layers
-                 resident, the rest copied in bulk each step) and zero-copy offload (the routed experts
-                 of non-resident layers read over the link each step) at the same VRAM expert budget;
+  sweep          at per-layer caps 8..128, the pager against static layer-level offload at the same VRAM
+                 expert budget: zero-copy (the routed experts of non-resident layers read over the link
+                 each step; the paper-analogue comparison) and bulk (the rest copied whole each step);
   controller     the live dual-resize (App. B): a fixed split's idle KV moved to expert slots by the
                  control law, decode tokens/s before and after;
   prefetch       speculative prefetch (Sec. 4) at caps 8/16/32: off, the online co-activation predictor
@@ -126,10 +128,11 @@ SWEEP_CAPS = (8, 16, 32, 64, 128)
 def sweep_leg(run, wl, wisp, torch, warmup=16, steps=96, offload_steps=3):
     """Iso-VRAM sweep over the expert budget (the analogue of the paper's Fig. 3 and Table 1): at each
     per-layer cap C the budget is C * L * M_e bytes, spent three ways on the same steps and kernels:
-    the pager (device pager, cold start; preloaded when C = N, where every expert fits), static
-    layer-level offload (whole layers resident, every other layer copied in bulk each step, as the
-    paper describes the baseline), and zero-copy offload (whole layers resident, the routed experts of
-    the other layers read over the host link each step, nothing cached)."""
+    the pager (device pager, cold start; preloaded when C = N, where every expert fits), zero-copy
+    offload (whole layers resident, the routed experts of the other layers read over the host link each
+    step, nothing cached: the bytes per token the paper's measured static-offload rates imply, so the
+    paper-analogue comparison), and bulk offload (whole layers resident, every other layer copied in
+    bulk each step: the layer-grained reading of the baseline, a lower bound)."""
     steps = min(steps, run.steps - warmup)
     out = []
 
@@ -162,12 +165,13 @@ def sweep_leg(run, wl, wisp, torch, warmup=16, steps=96, offload_steps=3):
             run.ctx.offload_end()
         st, zc = arms["static_offload"], arms["zero_copy_offload"]
         out.append(dict(cap=cap, budget_GB=budget / 1e9, paged_tokens_per_s=paged, paged_preloaded=cap == wl.N,
-                        static_offload_tokens_per_s=st[0], static_resident_layers=st[1],
                         zero_copy_offload_tokens_per_s=zc[0], zero_copy_resident_layers=zc[1],
-                        speedup_vs_static=paged / st[0], speedup_vs_zero_copy=paged / zc[0]))
-        log(f"sweep C={cap:3d} ({budget / 1e9:5.1f} GB): paged {paged:7.2f} tokens/s; static offload {st[0]:7.2f} "
-            f"({st[1]} resident layers) -> {paged / st[0]:5.1f}x; zero-copy offload {zc[0]:7.2f} ({zc[1]}) -> "
-            f"{paged / zc[0]:4.1f}x")
+                        speedup_vs_zero_copy=paged / zc[0],
+                        bulk_offload_tokens_per_s=st[0], bulk_resident_layers=st[1],
+                        speedup_vs_bulk=paged / st[0]))
+        log(f"sweep C={cap:3d} ({budget / 1e9:5.1f} GB): paged {paged:7.2f} tokens/s; zero-copy offload {zc[0]:7.2f} "
+            f"({zc[1]} resident layers) -> {paged / zc[0]:4.1f}x; bulk offload {st[0]:7.2f} ({st[1]}) -> "
+            f"{paged / st[0]:5.1f}x")
     return out
 
 
@@ -288,7 +292,7 @@ def prefetch_leg(run, wl, wisp, torch, warmup=16, steps=96):
     return out
 
 
-def prefill_leg(wisp, torch, link, link_cu=None, passes=3):
+def prefill_leg(wisp, torch, link, link_cu, passes=3):
     """Prefill tokens/s of the token-batch path (2048 tokens per layer, union 128 > C = 32, so four
     chunked Algorithm 1 steps per layer, grouped MFMA GEMMs), from cold slot tables each pass as the
     workload prescribes; then a fully resident pass (C = N, preloaded) for the matrix-core rate of
@@ -317,15 +321,15 @@ def prefill_leg(wisp, torch, link, link_cu=None, passes=3):
         distinct = int((out["hits"] + out["misses"]).sum())
         pairs = wl.T * wl.k
         flops = 6.0 * wl.d * wl.I * pairs * wl.L
-        t_link = misses * wl.blob / (link * 1e9)
+        # the token-batch fills stream by the compute units: the link term is the compute-unit rate; the
+        # same roofline at the copy-engine rate is reported beside it
+        t_link = misses * wl.blob / (link_cu * 1e9)
         t_hbm = distinct * wl.blob / (HBM_PEAK_GBPS * 1e9)
         t_mfma = flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
         t_roof = t_link + max(t_hbm, t_mfma)
-        # the token-batch fills stream by the compute units, which move more than the copy-engine rate
-        # of the link term above: the same roofline with the compute-unit link rate is reported beside
-        t_roof_cu = misses * wl.blob / (link_cu * 1e9) + max(t_hbm, t_mfma) if link_cu else None
-        log(f"prefill: cold pass {el * 1e3:.1f} ms -> {wl.T / el:.0f} tokens/s, {t_roof / el:.3f} of the roofline"
-            + (f" ({t_roof_cu / el:.3f} with the compute-unit link rate)" if t_roof_cu else ""))
+        t_roof_ce = misses * wl.blob / (link * 1e9) + max(t_hbm, t_mfma)
+        log(f"prefill: cold pass {el * 1e3:.1f} ms -> {wl.T / el:.0f} tokens/s, {t_roof / el:.3f} of the roofline "
+            f"(compute-unit link rate; {t_roof_ce / el:.3f} at the copy-engine rate)")
         # fully resident: the same kernels with no faults; grouped GEMMs timed by HIP events
         assert run.set_cap(wl.N) == wl.N
         run.ctx.preload()
@@ -372,8 +376,9 @@ def prefill_leg(wisp, torch, link, link_cu=None, passes=3):
             workload=wl.description, tokens_per_s=wl.T / el, pass_ms=el * 1e3, passes=len(times),
             pass_ms_all=[t * 1e3 for t in times], cap_per_layer=wl.cap, faults=misses, distinct_experts=distinct,
             roofline=dict(t_roof_s=t_roof, t_link_s=t_link, t_hbm_s=t_hbm, t_mfma_s=t_mfma, frac=t_roof / el,
-                          roofline_tokens_per_s=wl.T / t_roof, link_GBps_measured=link, flops=flops,
-                          link_cus_GBps_measured=link_cu, frac_cus_link=t_roof_cu / el if t_roof_cu else None),
+                          roofline_tokens_per_s=wl.T / t_roof, link_engine="compute_units",
+                          link_GBps_measured=link_cu, flops=flops,
+                          side=dict(link_engine="copy_engine", link_GBps_measured=link, frac=t_roof_ce / el)),
             resident=dict(tokens_per_s=wl.T / rel, pass_ms=rel * 1e3, kernels=kern),
             mfma=dict(bound="mfma", achieved=achieved, peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
                       frac=achieved / MFMA_BF16_PEAK_TFLOPS if achieved else None,
@@ -469,23 +474,29 @@ def main():
         run.ctx.set_profiling(0)
         return el, out, warm
 
-    def path_roofline(elapsed, out, n_steps=None):
+    def path_roofline(elapsed, out, n_steps=None, engine="copy_engine"):
+        """T_roof with the link term at the measured rate of the engine that moves this pass's faults:
+        the copy engine (hipMemcpyAsync, host pager) or the compute units (the device pager streams
+        faulted experts with its own loads).  The other engine's rate is reported beside it."""
         n_steps = steps if n_steps is None else n_steps
         hits, misses = out["hits"], out["misses"]
         distinct = hits + misses
         hbm_bytes = float(distinct.sum()) * wl.blob + wl.N * wl.d * 4 * wl.L * n_steps
         link_bytes = float(misses.sum()) * wl.blob
-        t_roof = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (link * 1e9)
-        t_roof_cu = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (link_cu * 1e9)
+        rate = {"copy_engine": link, "compute_units": link_cu}
+        other = "compute_units" if engine == "copy_engine" else "copy_engine"
+        t_roof = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (rate[engine] * 1e9)
+        t_roof_other = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (rate[other] * 1e9)
         return dict(t_roof_s=t_roof, t_measured_s=elapsed, frac=t_roof / elapsed,
-                    roofline_tokens_per_s=wl.T * n_steps / t_roof, link_GBps_measured=link,
-                    link_cus_GBps_measured=link_cu, frac_cus_link=t_roof_cu / elapsed,
+                    roofline_tokens_per_s=wl.T * n_steps / t_roof, link_engine=engine,
+                    link_GBps_measured=rate[engine],
+                    side=dict(link_engine=other, link_GBps_measured=rate[other], frac=t_roof_other / elapsed),
                     hbm_peak_GBps=HBM_PEAK_GBPS, device_copy_GBps_measured=hbm_copy,
                     hbm_bytes_per_token=hbm_bytes / (wl.T * n_steps), link_bytes_per_token=link_bytes / (wl.T * n_steps),
                     faults_per_token=float(misses.sum()) / (wl.T * n_steps),
                     fault_rate=float(misses.sum()) / float(distinct.sum()))
 
-    def all_steps(el, out, warm):
+    def all_steps(el, out, warm, engine):
         """Every step of the pass from the cold tables (compulsory faults included): the warmup steps
         and the timed ones, each timed from its first route to its final device synchronisation."""
         w_el, w_out = warm
@@ -495,7 +506,7 @@ def main():
                     misses=np.concatenate([w_out["misses"], out["misses"]]))
         n = warmup + steps
         return dict(steps=n, tokens_per_s=wl.T * n / (w_el + el),
-                    path_roofline=path_roofline(w_el + el, both, n))
+                    path_roofline=path_roofline(w_el + el, both, n, engine))
 
     def kernel_table():
         tab = {}
@@ -532,12 +543,14 @@ def main():
         if o is None or not g:
             return None
         gate_bytes = 2 * wl.d * wl.I * (2 if wl.w_dtype == wisp.BF16 else 4)
+        # the faulted experts stream by the kernel's own loads: the link term is the compute-unit rate
         t_roof = (float(o["hits"].sum()) * gate_bytes / (HBM_PEAK_GBPS * 1e9) +
-                  float(o["misses"].sum()) * wl.blob / (link * 1e9))
+                  float(o["misses"].sum()) * wl.blob / (link_cu * 1e9))
         t_meas = g["total_ms"] * 1e-3
         return dict(kernel="ffn_gateup_dev (resident experts from HBM, faulted ones streamed from pinned host memory)",
                     bound="hbm+link", launches=g["launches"], avg_launch_us=g["avg_us"], t_roof_s=t_roof,
-                    t_measured_s=t_meas, frac=t_roof / t_meas, link_GBps_measured=link, hbm_peak_GBps=HBM_PEAK_GBPS,
+                    t_measured_s=t_meas, frac=t_roof / t_meas, link_engine="compute_units",
+                    link_GBps_measured=link_cu, hbm_peak_GBps=HBM_PEAK_GBPS,
                     source="census steps (every kernel class event-timed)")
 
     mask = {"gateup": 1 << wisp.K_FFN_GATEUP, "all": True, "none": 0}[args.kernel_timing]
@@ -547,7 +560,8 @@ def main():
         el, out, warm = timed_pass(wisp.PAGER_HOST, mask)
         tk = kernel_table()
         passes["host"] = dict(tokens_per_s=wl.T * steps / el, ms_per_step=el / steps * 1e3,
-                              path_roofline=path_roofline(el, out), all_steps=all_steps(el, out, warm),
+                              path_roofline=path_roofline(el, out, engine="copy_engine"),
+                              all_steps=all_steps(el, out, warm, "copy_engine"),
                               kernels_timed_region=tk, kernel_census=census(wisp.PAGER_HOST))
         log(f"host pager: {steps} steps in {el:.3f} s -> {wl.T * steps / el:.2f} tokens/s, "
             f"{passes['host']['path_roofline']['frac']:.3f} of the path roofline")
@@ -572,7 +586,8 @@ def main():
     if args.pager in ("both", "device"):
         el, out, warm = timed_pass(wisp.PAGER_DEVICE, 0)
         passes["device"] = dict(tokens_per_s=wl.T * steps / el, ms_per_step=el / steps * 1e3,
-                                path_roofline=path_roofline(el, out), all_steps=all_steps(el, out, warm),
+                                path_roofline=path_roofline(el, out, engine="compute_units"),
+                                all_steps=all_steps(el, out, warm, "compute_units"),
                                 kernel_census=census(wisp.PAGER_DEVICE))
         passes["device"]["ffn_roofline"] = device_ffn_roofline(passes["device"]["kernel_census"])
         log(f"device pager: {steps} steps in {el:.3f} s -> {wl.T * steps / el:.2f} tokens/s, "

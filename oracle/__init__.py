@@ -38,6 +38,8 @@ def lib():
         L.oracle_expert.argtypes = [_p, _i, _i, _i, _i, _p, _p, _p]
         L.oracle_moe_layer.argtypes = [_i, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _i, _p, _i, _p, _p, _p,
                                        _p, _p]
+        L.oracle_moe_layer_routed.argtypes = [_i, _i, _i, _i, _i, _i, _p, _p, _p, _i, _p, _i, _p, _p, _p]
+        L.oracle_route_gates.argtypes = [_i, _i, _i, _p, _i, _p, _i, _p, _p]
         L.oracle_lru_new.argtypes = [_i, _i]
         L.oracle_lru_new.restype = _p
         L.oracle_lru_free.argtypes = [_p]
@@ -114,6 +116,40 @@ def moe_layer(variant, blobs, Wr, x, k, I, w_dtype, shared_blob=None, n_groups=1
                            x_dtype_of(x), x.ctypes.data, T, idx.ctypes.data, g.ctypes.data, y.ctypes.data,
                            mg.ctypes.data, gmg.ctypes.data)
     return idx, g, y, mg, gmg
+
+
+def route_gates(variant, Wr, x, idx):
+    """Gates of a given routed set idx[k] (rank order) of one token, by the variant's rule."""
+    Wr = np.ascontiguousarray(Wr, dtype=np.float32)
+    x = np.ascontiguousarray(x)
+    idx = np.ascontiguousarray(np.asarray(idx, dtype=np.int32).ravel())
+    N, d = Wr.shape
+    if idx.min(initial=0) < 0 or idx.max(initial=0) >= N:
+        raise ValueError("expert id out of range")
+    g = np.zeros(idx.size, np.float64)
+    lib().oracle_route_gates(variant, N, d, Wr.ctypes.data, x_dtype_of(x), x.ctypes.data, idx.size,
+                             idx.ctypes.data, g.ctypes.data)
+    return g
+
+
+def moe_layer_routed(variant, blobs, Wr, x, idx, I, w_dtype, shared_blob=None):
+    """The fully resident layer evaluated on a given routing idx [T, k] (rank order) instead of the
+    oracle's own selection: gates by the variant's rule over that set, combine in that order.
+    Returns (gates [T,k], y [T,d] fp64)."""
+    Wr = np.ascontiguousarray(Wr, dtype=np.float32)
+    x = np.ascontiguousarray(x)
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    N, d = Wr.shape
+    T, k = idx.shape
+    if x.shape[0] != T or idx.min(initial=0) < 0 or idx.max(initial=0) >= N:
+        raise ValueError("routing does not match the tokens or the expert count")
+    arr = (ctypes.c_void_p * N)(*[_ptr(b) for b in blobs])
+    g = np.zeros((T, k), np.float64)
+    y = np.zeros((T, d), np.float64)
+    sh = _ptr(shared_blob) if shared_blob is not None else None
+    lib().oracle_moe_layer_routed(variant, N, d, I, k, w_dtype, arr, sh, Wr.ctypes.data, x_dtype_of(x),
+                                  x.ctypes.data, T, idx.ctypes.data, g.ctypes.data, y.ctypes.data)
+    return g, y
 
 
 class LRU:

@@ -121,6 +121,45 @@ static int select_topk(const double* score, const int* allowed, int N, int k, in
   return n;
 }
 
+/* z = W_r x in fp64 and the selection score of every expert: p = softmax(z) (variant 0), z
+ * itself (variant 1) or s = sigmoid(z) (variant 2). */
+static void route_scores(int variant, int N, int d, const float* Wr, int x_dtype, const void* x, double* z,
+                         double* sc) {
+  for (int e = 0; e < N; ++e) {
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) acc += (double)Wr[(size_t)e * d + c] * load_x(x_dtype, x, (size_t)c);
+    z[e] = acc;
+  }
+  if (variant == ROUTE_SOFTMAX_RENORM) {
+    double m = z[0];
+    for (int e = 1; e < N; ++e) m = z[e] > m ? z[e] : m;
+    double den = 0.0;
+    for (int e = 0; e < N; ++e) den += exp(z[e] - m);
+    for (int e = 0; e < N; ++e) sc[e] = exp(z[e] - m) / den;
+  } else if (variant == ROUTE_TOPK_SOFTMAX) {
+    for (int e = 0; e < N; ++e) sc[e] = z[e];
+  } else {
+    for (int e = 0; e < N; ++e) sc[e] = 1.0 / (1.0 + exp(-z[e]));
+  }
+}
+
+/* Gates of the routed set idx[k] (in its rank order): softmax of the set's logits (variant 1),
+ * else the set's scores renormalised to sum 1 (p for variant 0, s for variant 2). */
+static void gates_of_set(int variant, const double* z, const double* sc, const int32_t* idx, int k,
+                         double* gates) {
+  if (variant == ROUTE_TOPK_SOFTMAX) {
+    double m = z[idx[0]];
+    for (int j = 1; j < k; ++j) m = z[idx[j]] > m ? z[idx[j]] : m;
+    double den = 0.0;
+    for (int j = 0; j < k; ++j) den += exp(z[idx[j]] - m);
+    for (int j = 0; j < k; ++j) gates[j] = exp(z[idx[j]] - m) / den;
+  } else {
+    double den = 0.0;
+    for (int j = 0; j < k; ++j) den += sc[idx[j]];
+    for (int j = 0; j < k; ++j) gates[j] = sc[idx[j]] / den;
+  }
+}
+
 /*
  * Route one token.  z = W_r x in fp64 (W_r [N, d] fp32).
  *   variant 0, softmax then renormalise: p = softmax(z) over all N; R = top-k of p;
@@ -139,23 +178,10 @@ void oracle_route(int variant, int N, int d, int k, int n_groups, int topk_group
                   double* margin, double* group_margin) {
   double* z = (double*)malloc(sizeof(double) * (size_t)N);
   double* sc = (double*)malloc(sizeof(double) * (size_t)N);
-  for (int e = 0; e < N; ++e) {
-    double acc = 0.0;
-    for (int c = 0; c < d; ++c) acc += (double)Wr[(size_t)e * d + c] * load_x(x_dtype, x, (size_t)c);
-    z[e] = acc;
-  }
+  route_scores(variant, N, d, Wr, x_dtype, x, z, sc);
   int* allowed = NULL;
   double gm = INFINITY;
-  if (variant == ROUTE_SOFTMAX_RENORM) {
-    double m = z[0];
-    for (int e = 1; e < N; ++e) m = z[e] > m ? z[e] : m;
-    double den = 0.0;
-    for (int e = 0; e < N; ++e) den += exp(z[e] - m);
-    for (int e = 0; e < N; ++e) sc[e] = exp(z[e] - m) / den;
-  } else if (variant == ROUTE_TOPK_SOFTMAX) {
-    for (int e = 0; e < N; ++e) sc[e] = z[e];
-  } else {
-    for (int e = 0; e < N; ++e) sc[e] = 1.0 / (1.0 + exp(-z[e]));
+  if (variant == ROUTE_SIGMOID_GROUP) {
     int gsize = N / n_groups;
     double* gscore = (double*)malloc(sizeof(double) * (size_t)n_groups);
     for (int g = 0; g < n_groups; ++g) {
@@ -181,17 +207,7 @@ void oracle_route(int variant, int N, int d, int k, int n_groups, int topk_group
   for (int j = 0; j < k; ++j) idx[j] = sel[j];
   if (margin) *margin = ns > k ? sc[sel[k - 1]] - sc[sel[k]] : INFINITY;
   if (group_margin) *group_margin = gm;
-  if (variant == ROUTE_TOPK_SOFTMAX) {
-    double m = z[idx[0]];
-    for (int j = 1; j < k; ++j) m = z[idx[j]] > m ? z[idx[j]] : m;
-    double den = 0.0;
-    for (int j = 0; j < k; ++j) den += exp(z[idx[j]] - m);
-    for (int j = 0; j < k; ++j) gates[j] = exp(z[idx[j]] - m) / den;
-  } else {
-    double den = 0.0;
-    for (int j = 0; j < k; ++j) den += sc[idx[j]];
-    for (int j = 0; j < k; ++j) gates[j] = sc[idx[j]] / den;
-  }
+  gates_of_set(variant, z, sc, idx, k, gates);
   if (sel_score) memcpy(sel_score, sc, sizeof(double) * (size_t)N);
   free(sel);
   free(allowed);
@@ -257,6 +273,55 @@ void oracle_moe_layer(int variant, int N, int d, int I, int k, int n_groups, int
       for (int r = 0; r < d; ++r) yt[r] += o[r];
     }
   }
+  free(o);
+}
+
+/* Gates of a given routed set idx[k] of one token (the rule of oracle_moe_layer_routed), without
+ * the expert outputs. */
+void oracle_route_gates(int variant, int N, int d, const float* Wr, int x_dtype, const void* x, int k,
+                        const int32_t* idx, double* gates) {
+  double* z = (double*)malloc(sizeof(double) * (size_t)N);
+  double* sc = (double*)malloc(sizeof(double) * (size_t)N);
+  route_scores(variant, N, d, Wr, x_dtype, x, z, sc);
+  gates_of_set(variant, z, sc, idx, k, gates);
+  free(sc);
+  free(z);
+}
+
+/*
+ * The same layer for a routed set given by the caller instead of the oracle's own selection:
+ * idx [T, k] in rank order.  The gates follow the routing variant's rule applied to that set
+ * (softmax of its logits for variant 1, its renormalised p or s otherwise), the combine runs in
+ * the given rank order, and the shared expert is added as in oracle_moe_layer.  Used where two
+ * selections are both correct (a near-tie at the k-th score): the output of the set a kernel chose
+ * is then compared with this definition evaluated on that set.  Outputs gates [T, k], y [T, d].
+ */
+void oracle_moe_layer_routed(int variant, int N, int d, int I, int k, int w_dtype, const void* const* blobs,
+                             const void* shared_blob, const float* Wr, int x_dtype, const void* x, int T,
+                             const int32_t* idx, double* gates, double* y) {
+  size_t xs = x_dtype == 0 ? 4 : 2;
+  double* o = (double*)malloc(sizeof(double) * (size_t)d);
+  double* z = (double*)malloc(sizeof(double) * (size_t)N);
+  double* sc = (double*)malloc(sizeof(double) * (size_t)N);
+  for (int t = 0; t < T; ++t) {
+    const void* xt = (const char*)x + (size_t)t * d * xs;
+    const int32_t* it = idx + (size_t)t * k;
+    double* gt = gates + (size_t)t * k;
+    route_scores(variant, N, d, Wr, x_dtype, xt, z, sc);
+    gates_of_set(variant, z, sc, it, k, gt);
+    double* yt = y + (size_t)t * d;
+    for (int r = 0; r < d; ++r) yt[r] = 0.0;
+    for (int j = 0; j < k; ++j) {
+      oracle_expert(blobs[it[j]], w_dtype, d, I, x_dtype, xt, o, NULL);
+      for (int r = 0; r < d; ++r) yt[r] += gt[j] * o[r];
+    }
+    if (shared_blob) {
+      oracle_expert(shared_blob, w_dtype, d, I, x_dtype, xt, o, NULL);
+      for (int r = 0; r < d; ++r) yt[r] += o[r];
+    }
+  }
+  free(sc);
+  free(z);
   free(o);
 }
 

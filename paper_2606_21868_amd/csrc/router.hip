@@ -184,15 +184,19 @@ __global__ void __launch_bounds__(256) route_select_kernel(const float* __restri
   const float z = router_row<XT>(wr, x, 0, T, d, e, part);
   if (static_cast<int>(threadIdx.x) < T)
     __hip_atomic_store(logits + static_cast<size_t>(threadIdx.x) * N + e, z, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the row's stores are complete before it is counted
+  // The storing threads (t < T <= 4) are in wave 0 with thread 0; the barrier orders their stores
+  // before thread 0's arrival, whose release at agent scope publishes the row to every workgroup of
+  // the device that acquires the count.
   __syncthreads();
   if (threadIdx.x == 0) {
-    const uint32_t before = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t before = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     last = before + 1 == static_cast<uint32_t>(N);
     if (last) __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
   if (!last) return;
+  // every thread of the last workgroup: its later loads see all N published rows
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   select_tokens<true>(logits, 0, T, N, k, route, n_groups, topk_groups, sh);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (wave < T && lane < k) {

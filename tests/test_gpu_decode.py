@@ -43,11 +43,13 @@ def test_batch4_small_cap_chunks():
 
 def test_qwen3_decode_full_size_sampled():
     """The benchmarked workload at full size and in the benchmarked launch configuration: every
-    routing decision and every paging count against the oracle; outputs at sampled points."""
+    routing decision and every paging count against the oracle; outputs at 256 sampled (step, layer)
+    points plus every exempt token."""
     wl = WORKLOADS["qwen3-30b-a3b-decode"]
     rng = np.random.default_rng(0)
-    pts = sorted({(int(s), int(l)) for s, l in zip(rng.integers(0, wl.steps, 24), rng.integers(0, wl.L, 24))})
-    pts += [(0, 0), (wl.steps - 1, wl.L - 1)]
+    flat = rng.choice(wl.steps * wl.L, size=256, replace=False)
+    pts = sorted({(int(f) // wl.L, int(f) % wl.L) for f in flat} | {(0, 0), (wl.steps - 1, wl.L - 1)})
+    assert len(pts) >= 256
     _run_case(wl, wl.cap, wl.steps, sample_points=pts)
 
 

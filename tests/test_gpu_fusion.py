@@ -10,7 +10,7 @@ be the one that ran, and the fused outputs are checked against the oracle.
 import numpy as np
 import pytest
 
-from parity import check_outputs, check_pager, check_routing, log, oracle_routing
+from parity import check_run, log
 from paper_2606_21868_amd import wisp
 from paper_2606_21868_amd.workloads import WORKLOADS
 
@@ -66,11 +66,8 @@ def test_fused_matches_separate_kernels_and_oracle(shape, cap, steps):
         assert np.array_equal(fus["idx"], sep["idx"])
         assert np.array_equal(fus["hits"], sep["hits"]) and np.array_equal(fus["misses"], sep["misses"])
         assert np.array_equal(fus["y"].view(np.uint32), sep["y"].view(np.uint32)), "fused down+combine changed bits"
-        ora_idx, _, margin, gmargin, scores = oracle_routing(run, steps)
-        exempt, _ = check_routing(wl, fus["idx"], ora_idx, margin, gmargin, scores)
-        check_pager(wl, cap, fus["idx"], fus["hits"], fus["misses"])
-        pts = [(s, l) for s in range(0, steps, max(1, steps // 6)) for l in range(wl.L) if (s, l) not in exempt]
-        worst, _ = check_outputs(run, fus["y"], pts, ora_idx)
+        pts = [(s, l) for s in range(0, steps, max(1, steps // 6)) for l in range(wl.L)]
+        _, _, _, worst, _ = check_run(run, fus, steps, pts, cap=cap)
         log(f"  fused == separate bit for bit over {steps * wl.L} layer-steps, both pagers; worst row-relative "
             f"error vs oracle {worst:.2e}")
     finally:

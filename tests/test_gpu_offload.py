@@ -1,11 +1,12 @@
-"""GPU tests of the routing-blind static-offload arm (the comparison of the paper's iso-VRAM
-evaluation, Sec. 5.2): at a VRAM expert budget it keeps whole layers resident and streams every
-other layer's experts in bulk each step.  It runs the same router, expert and combine kernels as
-the pager, so its routing and outputs must equal the paged run's bit for bit."""
+"""GPU tests of the routing-blind static-offload arms (the comparison of the paper's iso-VRAM
+evaluation, Sec. 5.2): at a VRAM expert budget they keep whole layers resident and stream every
+other layer's experts in bulk each step (bulk) or read them over the link (zero-copy).  Each arm's
+routing, gates and outputs are checked against the oracle on their own, and since it runs the same
+router, expert and combine kernels as the pager, they must also equal the paged run's bit for bit."""
 import numpy as np
 import pytest
 
-from parity import log
+from parity import check_run, log
 from paper_2606_21868_amd.workloads import WORKLOADS
 
 torch = pytest.importorskip("torch")
@@ -32,6 +33,8 @@ def test_offload_matches_paged_bits(mode, budget_layers, resident):
         r = run.ctx.offload_begin(budget_layers * _layer_bytes(run), mode)
         assert r == resident
         off = run.offload(record=True)
+        _, exempt, _, worst, _ = check_run(run, off, steps, [(s, l) for s in range(steps) for l in range(wl.L)])
+        log(f"  offload arm against the oracle: routing, gates, outputs at every layer-step (worst {worst:.2e})")
         assert np.array_equal(off["idx"], paged["idx"])
         assert np.array_equal(off["y"].view(np.uint32), paged["y"].view(np.uint32)), "offload arm changed bits"
         # a second run continues the copy sequence across calls
@@ -86,9 +89,13 @@ def test_offload_full_size_bits():
             r = run.ctx.offload_begin(wl.cap * wl.L * run.blob_bytes, mode)
             assert r == resident
             off = run.offload(record=True)
+            # streamed and resident layers both sampled: layers < r are resident, the rest streamed
+            pts = [(0, 0), (0, r - 1), (1, r), (1, 30), (2, wl.L - 1), (2, 17)]
+            _, _, _, worst, _ = check_run(run, off, 3, pts)
             assert np.array_equal(off["idx"], paged["idx"])
             assert np.array_equal(off["y"].view(np.uint32), paged["y"].view(np.uint32))
             run.ctx.offload_end()
-            log(f"  full size, {'zero-copy' if mode else 'bulk'}: {r} resident layers, bit-identical to the paged run")
+            log(f"  full size, {'zero-copy' if mode else 'bulk'}: {r} resident layers; routing, gates and outputs at "
+                f"{len(pts)} points against the oracle (worst {worst:.2e}); bit-identical to the paged run")
     finally:
         run.close()

@@ -16,7 +16,7 @@ import pytest
 
 import oracle
 from oracle.predictor import CoActivation
-from parity import check_outputs, check_pager, check_routing, log, oracle_routing
+from parity import check_run, log
 from paper_2606_21868_amd import wisp
 from paper_2606_21868_amd.workloads import WORKLOADS
 
@@ -71,11 +71,8 @@ def test_prefetch_keeps_bits_and_matches_the_oracle_replay(cap):
         run.generate()
         assert run.set_cap(cap) == cap
         off = run.decode(record=True)
-        ora_idx, _, margin, gmargin, scores = oracle_routing(run, steps)
-        exempt, _ = check_routing(wl, off["idx"], ora_idx, margin, gmargin, scores)
-        check_pager(wl, cap, off["idx"], off["hits"], off["misses"])
         pts = [(0, 0), (steps // 2, 1), (steps - 1, wl.L - 1)]
-        check_outputs(run, off["y"], [p for p in pts if p not in exempt], ora_idx)
+        check_run(run, off, steps, pts, cap=cap)
         log(f"  prefetch off: {int(off['misses'].sum())} faults, checked against the oracle")
 
         # the online predictor

@@ -11,7 +11,7 @@ Mixtral-width case faults 352 MB blobs (eleven pieces) in chunked Algorithm 1 st
 import numpy as np
 import pytest
 
-from parity import check_outputs, check_routing, log, oracle_routing
+from parity import check_run, log
 from paper_2606_21868_amd import wisp
 from paper_2606_21868_amd.workloads import WORKLOADS
 
@@ -39,11 +39,12 @@ def test_staged_fills_land_intact_every_step(name, shape, cap, steps):
         masters = {}
         y = np.zeros((steps, wl.L, wl.T, wl.d), np.float32)
         idx = np.zeros((steps, wl.L, wl.T, wl.k), np.int32)
+        w = np.zeros((steps, wl.L, wl.T, wl.k), np.float32)
         occ = [[-1] * cap for _ in range(wl.L)]
         filled = 0
         for s in range(steps):
             out = run.decode(record=True, steps=1, start=s)
-            y[s], idx[s] = out["y"][0], out["idx"][0]
+            y[s], idx[s], w[s] = out["y"][0], out["idx"][0], out["w"][0]
             for l in range(wl.L):
                 for slot in range(cap):
                     e = run.ctx.expert_in_slot(l, slot)
@@ -56,10 +57,8 @@ def test_staged_fills_land_intact_every_step(name, shape, cap, steps):
                     assert diff is None, (f"step {s} layer {l} slot {slot} expert {e}: bytes {diff[0]}..{diff[1]} "
                                           f"differ ({diff[2]} bytes) from the master")
                     filled += 1
-        ora_idx, _, margin, gmargin, scores = oracle_routing(run, steps)
-        exempt, _ = check_routing(wl, idx, ora_idx, margin, gmargin, scores)
-        pts = [(s, l) for s in range(steps) for l in range(wl.L) if (s, l) not in exempt]
-        worst, _ = check_outputs(run, y, pts, ora_idx)
+        pts = [(s, l) for s in range(steps) for l in range(wl.L)]
+        _, _, _, worst, _ = check_run(run, dict(idx=idx, w=w, y=y), steps, pts)
         log(f"  {filled} filled slots byte-equal to their masters; outputs within tolerance (worst {worst:.2e})")
     finally:
         run.close()

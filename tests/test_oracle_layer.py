@@ -158,3 +158,77 @@ def test_shared_expert_adds_with_weight_one():
     _, _, y_wo, _, _ = oracle.moe_layer(wl.route, blobs, Wr, xs[0], wl.k, wl.I, wl.w_dtype, None, 8, 4)
     np.testing.assert_allclose(y_with[0] - y_wo[0], oracle.expert(shared, wl.w_dtype, wl.d, wl.I, xs[0, 0]),
                                rtol=1e-9, atol=1e-14)
+
+
+def _textbook_gates_of_set(wl, Wr, xv, order):
+    """Gates of a given routed set by the variant's rule, from numpy logits."""
+    z = Wr.astype(np.float64) @ xv
+    if wl.route == oracle.ROUTE_SOFTMAX_RENORM:
+        p = np.exp(z - z.max())
+        p /= p.sum()
+        return p[order] / p[order].sum()
+    if wl.route == oracle.ROUTE_TOPK_SOFTMAX:
+        e = np.exp(z[order] - z[order].max())
+        return e / e.sum()
+    s = 1 / (1 + np.exp(-z))
+    return s[order] / s[order].sum()
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_routed_layer_matches_textbook(name):
+    """The layer evaluated on a routed set chosen by someone else (what a kernel may pick at a
+    near-tie): the k-th expert swapped for the (k+1)-th candidate, and a random set in a random
+    order.  Gates by the variant's rule over that set, combine in that order, from numpy."""
+    wl = SMALL[name]
+    blobs, Wr, xs, shared = _layer_inputs(wl, wl.T, 2)
+    rng = np.random.default_rng(7)
+    dec = [_decode_blob(b, wl.w_dtype, wl.d, wl.I) for b in blobs]
+    dec_sh = _decode_blob(shared, wl.w_dtype, wl.d, wl.I) if shared is not None else None
+    for s in range(xs.shape[0]):
+        x = xs[s]
+        own, g_own, y_own, _, _ = oracle.moe_layer(wl.route, blobs, Wr, x, wl.k, wl.I, wl.w_dtype, shared,
+                                                   wl.n_groups, wl.topk_groups)
+        # the oracle's own routing reproduces the plain layer
+        g_r, y_r = oracle.moe_layer_routed(wl.route, blobs, Wr, x, own, wl.I, wl.w_dtype, shared)
+        np.testing.assert_array_equal(g_r, g_own)
+        np.testing.assert_array_equal(y_r, y_own)
+        other = np.empty_like(own)
+        for t in range(wl.T):
+            sc = oracle.route(wl.route, Wr, x[t], wl.k, wl.n_groups, wl.topk_groups)[2]
+            nxt = [e for e in np.lexsort((np.arange(wl.N), -sc)) if e not in own[t]][0]
+            other[t] = own[t]
+            other[t, -1] = nxt
+            if s == 1:
+                other[t] = rng.permutation(wl.N)[:wl.k]
+        g, y = oracle.moe_layer_routed(wl.route, blobs, Wr, x, other, wl.I, wl.w_dtype, shared)
+        for t in range(wl.T):
+            xv = _x_f64(x[t])
+            gw = _textbook_gates_of_set(wl, Wr, xv, other[t])
+            np.testing.assert_allclose(g[t], gw, rtol=1e-12)
+            assert abs(g[t].sum() - 1.0) < 1e-12
+            yw = sum(gw[j] * _textbook_expert(*dec[other[t, j]], xv) for j in range(wl.k))
+            if dec_sh is not None:
+                yw = yw + _textbook_expert(*dec_sh, xv)
+            np.testing.assert_allclose(y[t], yw, rtol=1e-9, atol=1e-12 * np.abs(yw).max())
+            # a different set gives a different output: the given routing is really used
+            assert np.abs(y[t] - y_own[t]).max() > 0
+
+
+def test_routed_layer_rejects_bad_ids():
+    wl = SMALL["qwen3-small"]
+    blobs, Wr, xs, _ = _layer_inputs(wl, 1, 1)
+    with pytest.raises(ValueError):
+        oracle.moe_layer_routed(wl.route, blobs, Wr, xs[0], np.full((1, wl.k), wl.N), wl.I, wl.w_dtype)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_route_gates_of_a_given_set(name):
+    wl = SMALL[name]
+    blobs, Wr, xs, shared = _layer_inputs(wl, wl.T, 1)
+    rng = np.random.default_rng(3)
+    for t in range(wl.T):
+        idx, g, _, _, _ = oracle.route(wl.route, Wr, xs[0, t], wl.k, wl.n_groups, wl.topk_groups)
+        np.testing.assert_array_equal(oracle.route_gates(wl.route, Wr, xs[0, t], idx), g)
+        other = rng.permutation(wl.N)[:wl.k]
+        np.testing.assert_allclose(oracle.route_gates(wl.route, Wr, xs[0, t], other),
+                                   _textbook_gates_of_set(wl, Wr, _x_f64(xs[0, t]), other), rtol=1e-12)
