@@ -22,8 +22,11 @@ Reported beside the throughput:
   sweep          at per-layer caps 8..128, the pager against static layer-level offload at the same VRAM
                  expert budget: zero-copy (the routed experts of non-resident layers read over the link
                  each step; the paper-analogue comparison) and bulk (the rest copied whole each step);
-  controller     the live dual-resize (App. B): a fixed split's idle KV moved to expert slots by the
-                 control law, decode tokens/s before and after;
+  controller     the online dual-resize (Sec. 3.5, App. B) over a KV-occupancy trace with regime
+                 shifts: moves made at drained barriers, decode tokens/s per regime against the fixed
+                 split;
+  configurator   MV-WSA's startup split (Eqs. 3-5) from the miss curve of the GPU's own routing trace,
+                 run and compared with the curve's fault prediction;
   prefetch       speculative prefetch (Sec. 4) at caps 8/16/32: off, the online co-activation predictor
                  (App. E), and perfect hints (each step's true routing), on the host pager;
   prefill        the Qwen3-30B-A3B-shaped prefill chunk (2048 tokens per layer, same weights and
@@ -46,6 +49,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+PINNED_LIMIT_BYTES = 60e9           # pinned host memory one process may hold on the test machines (65 GiB)
 MFMA_BF16_PEAK_TFLOPS = 2500.0      # dense bf16 matrix-core peak of the MI355X
 PREFILL_WORKLOAD = "qwen3-30b-a3b-prefill"
 TRAFFIC_SUMMARIES = {k: os.path.join(ROOT, "profiles", f"{k}_qwen3-30b-a3b-decode_hbm_traffic.txt")
@@ -102,24 +106,27 @@ def measured_traffic(workload, kname):
 
 
 def cpu_baseline(run, wl, start_step, max_tokens=24, budget_s=15.0):
-    """The oracle as it stands: fully resident fp64 layer, all layers of consecutive decode steps."""
+    """The oracle as it stands: fully resident fp64 layer, layer after layer of consecutive decode
+    steps, until max_tokens tokens or the time budget; a partial step counts its share of layers."""
     import oracle
     threads = oracle.num_threads()
     t0 = time.perf_counter()
-    tokens = 0
+    layers = 0
     s = start_step
-    while tokens < max_tokens and s < run.x_host.shape[1]:
-        for l in range(wl.L):
-            oracle.moe_layer(wl.route, run.master_ptrs(l), run.wr_host[l], run.x_host[l, s], wl.k, wl.I, wl.w_dtype,
-                             run.shared_ptr(l), wl.n_groups, wl.topk_groups)
-        tokens += wl.T
-        s += 1
+    while layers < max_tokens // wl.T * wl.L and s < run.x_host.shape[1]:
+        l = layers % wl.L
+        oracle.moe_layer(wl.route, run.master_ptrs(l), run.wr_host[l], run.x_host[l, s], wl.k, wl.I, wl.w_dtype,
+                         run.shared_ptr(l), wl.n_groups, wl.topk_groups)
+        layers += 1
+        if layers % wl.L == 0:
+            s += 1
         if time.perf_counter() - t0 > budget_s:
             break
     dt = time.perf_counter() - t0
+    tokens = layers / wl.L * wl.T
     return dict(value=tokens / dt, unit="tokens/s", cores=threads, kind="oracle",
-                sample=f"{tokens // wl.T} decode step(s) x {wl.L} layers x batch {wl.T} "
-                       f"(fully resident fp64 layer, weights read from the same pinned host masters), {dt:.1f} s")
+                sample=f"{layers} layer-steps ({layers / wl.L:.2f} decode steps of {wl.L} layers) x batch {wl.T} "
+                       f"(fully resident fp64 layer, weights read from the same host masters), {dt:.1f} s")
 
 
 SWEEP_CAPS = (8, 16, 32, 64, 128)
@@ -154,7 +161,12 @@ def sweep_leg(run, wl, wisp, torch, warmup=16, steps=96, offload_steps=3):
             run.ctx.preload()
         run.ctx.set_pager(wisp.PAGER_DEVICE)
         run.decode(record=False, steps=warmup, start=0, stats=False)
-        paged = timed(lambda n: run.decode(record=False, steps=n, start=warmup, stats=False), steps)
+        faults = {}
+
+        def paged_run(n):
+            faults["n"] = int(run.decode(record=False, steps=n, start=warmup)["misses"].sum())
+
+        paged = timed(paged_run, steps)
         run.ctx.set_pager(wisp.PAGER_HOST)
         arms = {}
         for mode, name in ((wisp.OFFLOAD_BULK, "static_offload"), (wisp.OFFLOAD_ZERO_COPY, "zero_copy_offload")):
@@ -165,6 +177,7 @@ def sweep_leg(run, wl, wisp, torch, warmup=16, steps=96, offload_steps=3):
             run.ctx.offload_end()
         st, zc = arms["static_offload"], arms["zero_copy_offload"]
         out.append(dict(cap=cap, budget_GB=budget / 1e9, paged_tokens_per_s=paged, paged_preloaded=cap == wl.N,
+                        paged_faults_per_token=faults["n"] / (wl.T * steps),
                         zero_copy_offload_tokens_per_s=zc[0], zero_copy_resident_layers=zc[1],
                         speedup_vs_zero_copy=paged / zc[0],
                         bulk_offload_tokens_per_s=st[0], bulk_resident_layers=st[1],
@@ -175,72 +188,175 @@ def sweep_leg(run, wl, wisp, torch, warmup=16, steps=96, offload_steps=3):
     return out
 
 
-# Qwen3-30B-A3B KV cache: 48 layers x (K, V) x 4 KV heads x 128 x bf16 per token, 16-token blocks
-KV_BLOCK_BYTES = 16 * 48 * 2 * 4 * 128 * 2
-KV_POOL_GIB = 2.79          # the fixed split's KV pool in the paper's live run
-KV_PEAK_FRACTION = 0.44     # its observed peak occupancy
-KV_HEADROOM = 0.2
+def configurator_leg(run, wl, wisp, torch, link_cu, warmup=16, steps=96):
+    """MV-WSA's startup configurator (Sec. 3.3-3.4, Eqs. 3-5) fed by the GPU's own routing.  The expert
+    miss curve m_exp(C) is the sum over layers of the library's reuse-distance curve of the routing the
+    pager recorded over the whole run (with its upper bound beside it); the KV side is a stand-in: a
+    demand of D blocks, each block short of
+    it recomputed every step (m_kv = max(0, demand - kappa), c_kv = KV_RECOMPUTE_S per block), with the
+    admission floor of Eq. 4 for four sessions of 4096 tokens.  c_exp = M_e / the measured compute-unit
+    link rate.  The KV demand is the peak of the occupancy model's tool-call regime (the representative
+    trace of the offline mode).  The chosen split is then run (device pager, cold) and its faults
+    compared with the curve's prediction."""
+    import numpy as np
 
-
-def controller_leg(run, wl, wisp, torch, warmup=16, steps=96):
-    """The live dual-resize of Sec. 3.5 / App. B on the decode workload: a fixed split (cap 32 and a
-    2.79 GiB KV pool of real device memory) serves a burst whose KV peaks at 44 % of the pool; at the
-    drained barrier the control law (Eqs. 6-8) moves the idle KV to expert slots and the move is
-    applied (KV shrunk first, then the scratch grown).  Decode tokens/s are timed before and after on
-    the same steps (the KV cache itself is simulated: its bytes are held, not read)."""
-    steps = min(steps, run.steps - warmup)
+    from paper_2606_21868_amd.workloads import kv_occupancy_trace
     a = wl.L * wl.blob
     b = KV_BLOCK_BYTES
     kv0 = int(KV_POOL_GIB * (1 << 30)) // b
     B = wl.cap * a + kv0 * b
-
-    def measure():
-        run.ctx.set_pager(wisp.PAGER_HOST)
-        run.ctx.masters_ready()
-        run.ctx.set_pager(wisp.PAGER_DEVICE)
-        run.decode(record=False, steps=warmup, start=0, stats=False)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        run.decode(record=False, steps=steps, start=warmup, stats=False)
-        torch.cuda.synchronize()
-        return wl.T * steps / (time.perf_counter() - t0)
-
+    demand = int(kv_occupancy_trace([(160, "tool")], kv0, seed=0).max())
+    run.ctx.set_pager(wisp.PAGER_HOST)
+    run.ctx.masters_ready()
+    assert run.set_cap(wl.cap) == wl.cap
+    run.ctx.set_pager(wisp.PAGER_DEVICE)
+    rec = run.decode(record=True, steps=run.steps, start=0)
+    S = run.steps
+    lo = np.zeros(wl.N + 1)
+    up = np.zeros(wl.N + 1)
+    for l in range(wl.L):
+        c_lo, c_up = wisp.miss_curve(rec["idx"][:, l].reshape(S, -1), wl.N, upper=True)
+        lo += c_lo
+        up += c_up
+    m_exp = np.round(lo / S).astype(np.uint64)                  # expert faults per decode step
+    kv_min = 4 * math.ceil(4096 / 16)
+    m_kv = np.maximum(0, demand - np.arange(demand + 1)).astype(np.float64)
+    c_exp = wl.blob / (link_cu * 1e9)
+    split = wisp.mvwsa_configure(B, a, b, kv_min, c_exp, KV_RECOMPUTE_S, m_exp, m_kv)
+    cap = split["cap"]
+    run.ctx.set_pager(wisp.PAGER_HOST)
+    run.ctx.masters_ready()
+    assert run.set_cap(cap) == cap
+    run.ctx.set_pager(wisp.PAGER_DEVICE)
+    run.decode(record=False, steps=warmup, start=0, stats=False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    o = run.decode(record=False, steps=steps, start=warmup)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
     run.ctx.set_pager(wisp.PAGER_HOST)
     assert run.set_cap(wl.cap) == wl.cap
-    pool = wisp.KvPool(b, kv0)
-    try:
-        fixed = measure()
+    whole = rec["misses"].sum()
+    res = dict(budget_GiB=B / (1 << 30), kv_block_bytes=b, kv_demand_blocks=demand, kv_min_blocks=kv_min,
+               c_exp_s=c_exp, c_kv_s=KV_RECOMPUTE_S, split=split, kv_GiB=split["kv_blocks"] * b / (1 << 30),
+               curve_faults_per_step=dict(C={int(c): [float(lo[c] / S), float(up[c] / S)]
+                                             for c in (8, 16, 32, 64, 128, cap) if c <= wl.N}),
+               recorded_cap=wl.cap, recorded_faults_per_step=float(whole / S),
+               recorded_within_curves=bool(lo[wl.cap] <= whole <= up[wl.cap]),
+               chosen=dict(cap=cap, tokens_per_s=wl.T * steps / el,
+                           faults_per_step=float(o["misses"].sum()) / steps,
+                           curve_bounds_per_step=[float(lo[cap] / S), float(up[cap] / S)]))
+    log(f"configurator: B {B / (1 << 30):.2f} GiB -> cap {cap} / KV {res['kv_GiB']:.2f} GiB (f = {split['f']:.3f}, "
+        f"floor binding {split['floor_binding']}); decode {res['chosen']['tokens_per_s']:.2f} tokens/s, "
+        f"{res['chosen']['faults_per_step']:.1f} faults per step (curve {lo[cap] / S:.1f}..{up[cap] / S:.1f})")
+    return res
+
+
+# Qwen3-30B-A3B KV cache: 48 layers x (K, V) x 4 KV heads x 128 x bf16 per token, 16-token blocks
+KV_BLOCK_BYTES = 16 * 48 * 2 * 4 * 128 * 2
+KV_POOL_GIB = 2.79          # the fixed split's KV pool in the paper's live run
+KV_HEADROOM = 0.2
+KV_DEAD_ZONE = 2            # experts per layer
+KV_RECOMPUTE_S = 16 / 91000.0   # recomputing one 16-token block at the resident prefill rate
+CONTROLLER_BARRIER_EVERY = 32
+CONTROLLER_REGIMES = (("tool", 160), ("long", 160), ("tool", 160))
+
+
+def controller_leg(run, wl, wisp, torch, warmup=16):
+    """The online dual-resize of Sec. 3.5 / App. B on the decode workload (device pager).  A seeded
+    KV-occupancy trace with regime shifts (four sessions; short tool-call bursts, then long-context
+    turns, then bursts again) is observed step by step; every CONTROLLER_BARRIER_EVERY steps, at a
+    drained barrier, the controller takes the peak since the last barrier and applies the control law
+    (Eqs. 6-8, headroom KV_HEADROOM, dead-zone KV_DEAD_ZONE) to the expert scratch and a KV pool of real
+    device memory (the KV cache itself is simulated: its bytes are held, not read).  The same steps run
+    on the fixed split (cap 32, 2.79 GiB of KV).  Per regime: decode tokens/s of both, and the steps
+    whose occupancy exceeded the pool in place (requests that would be preempted)."""
+    import numpy as np
+
+    from paper_2606_21868_amd.workloads import kv_occupancy_trace
+    a = wl.L * wl.blob
+    b = KV_BLOCK_BYTES
+    kv0 = int(KV_POOL_GIB * (1 << 30)) // b
+    B = wl.cap * a + kv0 * b
+    every = CONTROLLER_BARRIER_EVERY
+    steps = sum(n for _, n in CONTROLLER_REGIMES)
+    steps = min(steps, (run.steps - warmup) // every * every)
+    occ = kv_occupancy_trace([(n, k) for k, n in CONTROLLER_REGIMES], kv0, seed=0)[:steps]
+    regime = np.concatenate([[k] * n for k, n in CONTROLLER_REGIMES])[:steps]
+
+    def pass_(live):
         run.ctx.set_pager(wisp.PAGER_HOST)
-        cap, kv, move = wisp.resize_target(B, a, b, 0, KV_HEADROOM, 1, wl.N, 1, int(KV_PEAK_FRACTION * kv0), wl.cap)
-        t0 = time.perf_counter()
-        if move:
-            wisp.dual_resize(run.ctx, pool, cap, kv)
-        move_s = time.perf_counter() - t0
-        dyn = measure()
-        res = dict(budget_GiB=B / (1 << 30), kv_block_bytes=b,
-                   fixed=dict(cap=wl.cap, kv_GiB=kv0 * b / (1 << 30), tokens_per_s=fixed),
-                   dynamic=dict(cap=run.ctx.cap(), kv_GiB=pool.blocks * b / (1 << 30), tokens_per_s=dyn),
-                   move_seconds=move_s, decode_speedup=dyn / fixed)
-        log(f"controller: cap {wl.cap} / KV {kv0 * b / (1 << 30):.2f} GiB -> cap {run.ctx.cap()} / KV "
-            f"{pool.blocks * b / (1 << 30):.2f} GiB (move {move_s * 1e3:.0f} ms); decode {fixed:.2f} -> {dyn:.2f} "
-            f"tokens/s ({dyn / fixed:.3f}x)")
-        return res
-    finally:
-        pool.close()
+        assert run.set_cap(wl.cap) == wl.cap
+        run.ctx.masters_ready()
+        pool = wisp.KvPool(b, kv0)
+        ctl = wisp.Controller(B, a, b, 0, KV_HEADROOM, 1, wl.N, KV_DEAD_ZONE, wl.cap, kv0) if live else None
+        try:
+            run.ctx.set_pager(wisp.PAGER_DEVICE)
+            run.decode(record=False, steps=warmup, start=0, stats=False)
+            win_s, moves, over = [], [], np.zeros(steps, bool)
+            for s0 in range(0, steps, every):
+                kv_now = pool.blocks
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                run.decode(record=False, steps=every, start=warmup + s0, stats=False)
+                torch.cuda.synchronize()
+                win_s.append(time.perf_counter() - t0)
+                over[s0:s0 + every] = occ[s0:s0 + every] > kv_now
+                if ctl is not None:
+                    for t in range(s0, s0 + every):
+                        ctl.observe(int(occ[t]))
+                    t1 = time.perf_counter()
+                    cap, kv, moved, peak = ctl.barrier(run.ctx, pool)       # drains, then moves
+                    dt = time.perf_counter() - t1
+                    if moved:
+                        moves.append(dict(step=s0 + every, peak_blocks=peak, cap=cap, kv_GiB=kv * b / (1 << 30),
+                                          moved=moved, seconds=dt))
+            per = {}
+            for k, _ in CONTROLLER_REGIMES:
+                idx = [i for i in range(len(win_s)) if regime[i * every] == k]
+                per[k] = dict(tokens_per_s=wl.T * every * len(idx) / sum(win_s[i] for i in idx),
+                              steps_over_pool=int(sum(over[i * every:(i + 1) * every].sum() for i in idx)))
+            return dict(tokens_per_s=wl.T * steps / sum(win_s), per_regime=per, moves=moves,
+                        final_cap=run.ctx.cap(), final_kv_GiB=pool.blocks * b / (1 << 30))
+        finally:
+            if ctl is not None:
+                ctl.close()
+            pool.close()
+
+    fixed = pass_(False)
+    live = pass_(True)
+    run.ctx.set_pager(wisp.PAGER_HOST)
+    assert run.set_cap(wl.cap) == wl.cap
+    res = dict(budget_GiB=B / (1 << 30), kv_block_bytes=b, barrier_every=every, headroom=KV_HEADROOM,
+               dead_zone=KV_DEAD_ZONE, regimes=[dict(kind=k, steps=n) for k, n in CONTROLLER_REGIMES],
+               fixed=fixed, online=live, decode_speedup=live["tokens_per_s"] / fixed["tokens_per_s"])
+    log(f"controller: fixed split {fixed['tokens_per_s']:.2f} tokens/s, online {live['tokens_per_s']:.2f} "
+        f"({res['decode_speedup']:.3f}x); moves " + ", ".join(f"step {m['step']}: cap {m['cap']}" for m in live["moves"])
+        + "; per regime " + ", ".join(f"{k} {v['tokens_per_s']:.1f} vs {fixed['per_regime'][k]['tokens_per_s']:.1f} "
+                                       f"(over pool {v['steps_over_pool']} vs {fixed['per_regime'][k]['steps_over_pool']})"
+                                       for k, v in live["per_regime"].items()))
+    return res
 
 
 PREFETCH_CAPS = (8, 16, 32)
 PREFETCH_HORIZON = 4
 PREFETCH_GAMMA = 0.5
+PREFETCH_HINT_PRECISIONS = (1.0, 0.5, 0.25)
 
 
 def prefetch_leg(run, wl, wisp, torch, warmup=16, steps=96):
     """Speculative prefetch (Sec. 4) on the decode workload, host pager, per-layer caps 8/16/32: no
     prefetch; the online co-activation predictor of App. E (fresh each arm, top-k of each layer
     prefetched before it is routed, source layers within PREFETCH_HORIZON, decay PREFETCH_GAMMA); and
-    perfect hints (each step's true routing).  Tokens/s, demand faults and prefetch copies per
-    token, and the predictor's precision (prefetched experts the next step used / copies)."""
+    hints of a controlled precision (each step's true routing with a fraction 1 - p of the ids replaced
+    by experts the step does not use, p in PREFETCH_HINT_PRECISIONS; p = 1 is a perfect predictor).
+    The synthetic hidden states carry no cross-layer signal, so the co-activation predictor is near
+    chance here; the hint arms stand in for predictors of the paper's quality (about 0.5 next-expert
+    precision, App. E).  Tokens/s, demand faults and prefetch copies per token, and the measured
+    precision (copies the step then used / copies issued)."""
     import numpy as np
+
+    from paper_2606_21868_amd.workloads import degraded_hints
     steps = min(steps, run.steps - warmup)
     out = []
     run.ctx.set_pager(wisp.PAGER_HOST)
@@ -250,15 +366,16 @@ def prefetch_leg(run, wl, wisp, torch, warmup=16, steps=96):
         assert run.set_cap(cap) == cap
         arms = {}
         trace = None
-        for arm in ("off", "predictor", "perfect"):
+        for arm in ("off", "predictor") + tuple(f"hints_p{p:g}" for p in PREFETCH_HINT_PRECISIONS):
             run.ctx.masters_ready()
             pred = None
+            hints = None
             if arm == "predictor":
                 pred = wisp.Predictor(wl.L, wl.N, PREFETCH_HORIZON, PREFETCH_GAMMA)
                 run.ctx.set_prefetch(wisp.PREFETCH_PREDICTOR, pred, wl.k)
-            elif arm == "perfect":
+            elif arm.startswith("hints"):
                 run.ctx.set_prefetch(wisp.PREFETCH_HINTS)
-            hints = trace.reshape(trace.shape[0], wl.L, -1) if arm == "perfect" else None
+                hints = degraded_hints(trace, wl.N, float(arm[len("hints_p"):]), seed=cap)
             run.decode(record=False, steps=warmup, start=0, hints=hints[:warmup] if hints is not None else None)
             run.ctx.reset_stats()
             torch.cuda.synchronize()
@@ -279,17 +396,84 @@ def prefetch_leg(run, wl, wisp, torch, warmup=16, steps=96):
                              prefetch_copies_per_token=st["issued"] / n_tok,
                              precision=st["useful"] / st["issued"] if st["issued"] else None,
                              link_GB_per_token=(float(o["misses"].sum()) + st["issued"]) * wl.blob / n_tok / 1e9)
+            if hints is not None:
+                arms[arm]["hint_precision"] = float(arm[len("hints_p"):])
+        base = arms["off"]["tokens_per_s"]
         row = dict(cap=cap, **{a: v for a, v in arms.items()},
-                   predictor_speedup=arms["predictor"]["tokens_per_s"] / arms["off"]["tokens_per_s"],
-                   perfect_speedup=arms["perfect"]["tokens_per_s"] / arms["off"]["tokens_per_s"])
+                   speedup={a: v["tokens_per_s"] / base for a, v in arms.items() if a != "off"})
         out.append(row)
-        pr = arms["predictor"]
-        log(f"prefetch C={cap:3d}: off {arms['off']['tokens_per_s']:6.2f} tokens/s; predictor {pr['tokens_per_s']:6.2f} "
-            f"({row['predictor_speedup']:.2f}x, precision {pr['precision'] or 0:.2f}, "
-            f"{pr['prefetch_copies_per_token']:.1f} copies + {pr['demand_faults_per_token']:.1f} faults per token); "
-            f"perfect hints {arms['perfect']['tokens_per_s']:6.2f} ({row['perfect_speedup']:.2f}x)")
+        log(f"prefetch C={cap:3d}: off {base:6.2f} tokens/s; " + "; ".join(
+            f"{a} {v['tokens_per_s']:6.2f} ({v['tokens_per_s'] / base:.2f}x, precision {v['precision'] or 0:.2f}, "
+            f"{v['prefetch_copies_per_token']:.1f} copies + {v['demand_faults_per_token']:.1f} faults per token)"
+            for a, v in arms.items() if a != "off"))
     assert run.set_cap(wl.cap) == wl.cap
     return out
+
+
+# bounded decode legs of the workloads whose masters exceed the pinned memory of the test machines:
+# (workload, warmup steps, timed steps), each from cold slot tables
+PAGEABLE_LEGS = (("mixtral-8x7b-decode", 2, 6), ("deepseek-v3-16l-decode", 8, 64))
+
+
+def pageable_leg(wisp, torch, name, warmup, steps, cpu=True):
+    """Paged decode of a workload with pageable masters (every fault staged through the pinned bounce
+    ring, host pager): tokens/s over `steps` timed steps after `warmup` steps from cold tables; the
+    path roofline with the link term at the measured rate of that staged path; the expert gate/up
+    kernel's HBM rate in the timed region; and the CPU oracle on a bounded sample."""
+    from paper_2606_21868_amd.workloads import WORKLOADS
+    wl = WORKLOADS[name]
+    run = wisp.DecodeRun(wl, device=0, steps=warmup + steps, pageable=True)
+    try:
+        t0 = time.time()
+        run.generate()
+        gen_s = time.time() - t0
+        n_probe = max(1, math.ceil(2e9 / wl.blob))
+        link = run.ctx.probe_h2d(n_probe, 3)
+        assert run.set_cap(wl.cap) == wl.cap
+        run.ctx.masters_ready()
+        run.decode(record=False, steps=warmup, start=0)
+        run.ctx.reset_stats()
+        run.ctx.reset_kernel_times()
+        run.ctx.set_profiling(1 << wisp.K_FFN_GATEUP)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        out = run.decode(record=False, steps=steps, start=warmup)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t1
+        run.ctx.set_profiling(0)
+        g = run.ctx.kernel_times(wisp.K_FFN_GATEUP)
+        hits, misses = out["hits"], out["misses"]
+        n_tok = wl.T * steps
+        hbm_bytes = (float((hits + misses).sum()) + (wl.L * steps if wl.has_shared else 0)) * wl.blob + \
+            wl.N * wl.d * 4 * wl.L * steps
+        link_bytes = float(misses.sum()) * wl.blob
+        t_roof = hbm_bytes / (HBM_PEAK_GBPS * 1e9) + link_bytes / (link * 1e9)
+        gate = None
+        if g["launches"]:
+            gbps = g["bytes"] / (g["total_ms"] * 1e-3) / 1e9
+            gate = dict(bound="hbm", kernel="ffn_rows expert gate/up (W1+W3 rows" +
+                        (", fp8 E4M3 x bf16 block scales" if wl.w_dtype == wisp.FP8 else ", bf16") + "), timed region",
+                        achieved=gbps, peak=HBM_PEAK_GBPS, unit="GB/s", frac=gbps / HBM_PEAK_GBPS,
+                        launches=g["launches"], avg_launch_us=g["total_ms"] * 1e3 / g["launches"],
+                        bytes_per_launch=g["bytes"] / g["launches"])
+        res = dict(workload=wl.description, tokens_per_s=n_tok / el, ms_per_step=el / steps * 1e3, steps=steps,
+                   warmup=warmup, cap_per_layer=wl.cap, generate_s=gen_s, masters="pageable (staged through a "
+                   "pinned bounce ring)",
+                   path_roofline=dict(t_roof_s=t_roof, t_measured_s=el, frac=t_roof / el,
+                                      roofline_tokens_per_s=n_tok / t_roof, link_engine="copy_engine_staged",
+                                      link_GBps_measured=link, hbm_peak_GBps=HBM_PEAK_GBPS,
+                                      hbm_bytes_per_token=hbm_bytes / n_tok, link_bytes_per_token=link_bytes / n_tok,
+                                      faults_per_token=float(misses.sum()) / n_tok),
+                   gateup_kernel=gate)
+        log(f"{name}: {steps} steps in {el:.2f} s -> {n_tok / el:.3f} tokens/s, {t_roof / el:.3f} of the path "
+            f"roofline (staged link {link:.1f} GB/s, {float(misses.sum()) / n_tok:.1f} faults per token)"
+            + (f"; gate/up {gate['achieved']:.0f} GB/s ({gate['frac']:.3f} of HBM)" if gate else ""))
+        if cpu:
+            res["cpu_baseline"] = cpu_baseline(run, wl, warmup, max_tokens=wl.T * 2, budget_s=10.0)
+            log(f"{name}: cpu oracle {res['cpu_baseline']['value']:.4f} tokens/s ({res['cpu_baseline']['sample']})")
+        return res
+    finally:
+        run.close()
 
 
 def prefill_leg(wisp, torch, link, link_cu, passes=3):
@@ -409,6 +593,8 @@ def main():
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill leg")
     ap.add_argument("--no-sweep", action="store_true", help="skip the iso-VRAM budget sweep against static offload")
     ap.add_argument("--no-prefetch", action="store_true", help="skip the speculative-prefetch leg")
+    ap.add_argument("--no-pageable", action="store_true",
+                    help="skip the bounded Mixtral- and DeepSeek-shaped decode legs (pageable masters)")
     ap.add_argument("--no-fusion", action="store_true",
                     help="separate down and combine kernels instead of the fused down+combine (single-token steps)")
     ap.add_argument("--census-steps", type=int, default=24,
@@ -437,14 +623,19 @@ def main():
     total = warmup + steps
     log(f"workload {wl.name}: {warmup} warmup + {steps} timed steps, cap {wl.cap}")
 
-    run = wisp.DecodeRun(wl, device=0, steps=total)
+    # master sets beyond the pinned memory a process may hold on the test machines are pageable (faults
+    # staged through the bounce ring; host pager only)
+    pageable_masters = wl.L * wl.N * wl.blob > PINNED_LIMIT_BYTES
+    if pageable_masters:
+        args.pager = "host"
+    run = wisp.DecodeRun(wl, device=0, steps=total, pageable=pageable_masters)
     t0 = time.time()
     run.generate()
-    log(f"generated {wl.L * wl.N} expert blobs ({wl.L * wl.N * wl.blob / 1e9:.1f} GB pinned) and inputs in "
-        f"{time.time() - t0:.1f} s")
+    log(f"generated {wl.L * wl.N} expert blobs ({wl.L * wl.N * wl.blob / 1e9:.1f} GB "
+        f"{'pageable' if pageable_masters else 'pinned'}) and inputs in {time.time() - t0:.1f} s")
     n_probe = max(1, math.ceil(2e9 / wl.blob))
     link = run.ctx.probe_h2d(n_probe, 5)
-    link_cu = run.ctx.probe_h2d(n_probe, 5, engine=wisp.LINK_CUS)
+    link_cu = run.ctx.probe_h2d(n_probe, 5, engine=wisp.LINK_CUS) if not pageable_masters else link
     hbm_copy = measure_hbm_copy(torch, wisp)
     log(f"host->device {link:.1f} GB/s copy engine, {link_cu:.1f} GB/s compute-unit streaming (median of 5 x "
         f"{n_probe} blobs); device copy {hbm_copy:.0f} GB/s")
@@ -599,9 +790,11 @@ def main():
 
     sweep = None
     controller = None
+    configurator = None
     if not args.no_sweep and wl.name == BENCH_WORKLOAD:
         sweep = sweep_leg(run, wl, wisp, torch)
         controller = controller_leg(run, wl, wisp, torch)
+        configurator = configurator_leg(run, wl, wisp, torch, link_cu)
     prefetch = None
     if not args.no_prefetch and wl.name == BENCH_WORKLOAD:
         prefetch = prefetch_leg(run, wl, wisp, torch)
@@ -614,6 +807,10 @@ def main():
     prefill = None
     if not args.no_prefill:
         prefill = prefill_leg(wisp, torch, link, link_cu)
+    pageable = None
+    if not args.no_pageable and wl.name == BENCH_WORKLOAD:
+        pageable = {name: pageable_leg(wisp, torch, name, w, n, cpu=not args.no_cpu_baseline)
+                    for name, w, n in PAGEABLE_LEGS}
 
     result = {
         "metric": "paged MoE decode tokens/s at fixed VRAM expert budget",
@@ -640,7 +837,9 @@ def main():
         "prefill": prefill,
         "sweep": sweep,
         "controller": controller,
+        "configurator": configurator,
         "prefetch": prefetch,
+        "pageable_legs": pageable,
     }
     print(json.dumps(result), flush=True)
 

@@ -25,9 +25,12 @@ extern "C" {
  * counted at step level: the distinct experts referenced in the steps strictly between its previous
  * reference and this one.  A reference misses at cap C iff it is the first reference to its expert or
  * that distance is >= C.  This is a lower bound on Algorithm 1's misses (exact when every step has one
- * reference).  misses receives n_experts + 1 counts, C = 0 .. n_experts.  One pass, O(R log S) for R
- * references and S steps (a Fenwick tree over steps).  Host memory only. */
-wisp_status wisp_miss_curve(const int32_t* ids, int32_t steps, int32_t refs, int32_t n_experts, uint64_t* misses);
+ * reference).  misses receives n_experts + 1 counts, C = 0 .. n_experts.  misses_upper (optional, NULL
+ * to skip) receives the upper bound: a reference also counts when its distance plus the number of other
+ * experts of its previous step is >= C (those share its tick, so any of them may be evicted after it).
+ * One pass, O(R log S) for R references and S steps (a Fenwick tree over steps).  Host memory only. */
+wisp_status wisp_miss_curve(const int32_t* ids, int32_t steps, int32_t refs, int32_t n_experts, uint64_t* misses,
+                            uint64_t* misses_upper);
 
 /* MV-WSA startup configurator (Sec. 3.3 and 3.4, Eqs. 3-5). */
 typedef struct {
@@ -88,6 +91,22 @@ wisp_status wisp_kv_pool_destroy(wisp_kv_pool* pool);
  * max(old, new).  If the growing side fails, the shrunk side is grown back and WISP_E_NOMEM is
  * returned with the previous split in place.  Drains the context like wisp_set_budget. */
 wisp_status wisp_dual_resize(wisp_ctx* ctx, wisp_kv_pool* pool, int32_t cap_new, int64_t kv_blocks_new);
+
+/* The online controller of MV-WSA (Sec. 3.5 "Dynamic Dual-Resize", App. B): the caller reports the KV
+ * blocks in use after each decode step; at each drained barrier the controller takes the peak since
+ * the previous barrier as p, computes the target of the control law (wisp_resize_target, Eqs. 6-8,
+ * with its dead-zone) against the split it last applied, and, if a move is due, applies it with
+ * wisp_dual_resize.  A move that fails for lack of memory is skipped and the previous split stays
+ * (*moved_out = -1); *moved_out = 1 after a move, 0 when none was due or nothing was observed since the
+ * last barrier.  ctx and pool NULL: the decision only, nothing resized.  *peak_out receives p (-1 if
+ * nothing was observed).  Host memory only; one controller per (context, pool). */
+typedef struct wisp_controller wisp_controller;
+wisp_status wisp_controller_create(const wisp_resize_law* law, int32_t cap_now, int64_t kv_blocks_now,
+                                   wisp_controller** out);
+wisp_status wisp_controller_observe(wisp_controller* ctl, int64_t kv_blocks_in_use);
+wisp_status wisp_controller_barrier(wisp_controller* ctl, wisp_ctx* ctx, wisp_kv_pool* pool, int32_t* cap_out,
+                                    int64_t* kv_blocks_out, int32_t* moved_out, int64_t* peak_out);
+wisp_status wisp_controller_destroy(wisp_controller* ctl);
 
 #ifdef __cplusplus
 }

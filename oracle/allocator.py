@@ -93,3 +93,24 @@ def resize_target(B, a, b, kv_min, headroom, cap_min, cap_max, dead_zone, peak_b
     kappa = (B - C * a) // b
     move = abs(C - cap_now) >= dead_zone and C != cap_now
     return C, kappa, move
+
+
+def controller_replay(B, a, b, kv_min, headroom, cap_min, cap_max, dead_zone, cap0, kv0, occupancy, barrier_every):
+    """The online controller of Sec. 3.5 / App. B replayed on a KV-occupancy trace: after each decode
+    step t the blocks in use occupancy[t] are seen; after every barrier_every steps there is a drained
+    barrier, where p is the largest occupancy since the previous barrier and the law's target (with its
+    dead-zone) against the current split is applied when a move is due.  Returns one record per
+    barrier: (step, p, cap, kv_blocks, moved) with the split in place after the barrier."""
+    cap, kv = cap0, kv0
+    out = []
+    peak = None
+    for t, occ in enumerate(occupancy):
+        peak = occ if peak is None else max(peak, occ)
+        if (t + 1) % barrier_every == 0:
+            moved = 0
+            r = resize_target(B, a, b, kv_min, headroom, cap_min, cap_max, dead_zone, peak, cap)
+            if r is not None and r[2]:
+                cap, kv, moved = r[0], r[1], 1
+            out.append((t, peak, cap, kv, moved))
+            peak = None
+    return out

@@ -43,6 +43,16 @@ struct wisp_kv_pool {
   int64_t blocks = 0;               // the pool's size (<= capacity < size + kChunkBlocks)
 };
 
+// The online dual-resize controller (Sec. 3.5, App. B): the law, the split it last applied, and the
+// peak KV occupancy observed since the last drained barrier.
+struct wisp_controller {
+  wisp_resize_law law{};
+  int32_t cap = 0;
+  int64_t kv = 0;
+  int64_t peak = -1;          // -1: nothing observed since the last barrier
+  int64_t observed = 0;       // decode steps observed since the last barrier
+};
+
 namespace {
 
 constexpr int64_t kChunkBlocks = 64;
@@ -87,7 +97,8 @@ void pool_shrink(wisp_kv_pool* p, int64_t blocks) {
 
 extern "C" {
 
-wisp_status wisp_miss_curve(const int32_t* ids, int32_t steps, int32_t refs, int32_t n_experts, uint64_t* misses) {
+wisp_status wisp_miss_curve(const int32_t* ids, int32_t steps, int32_t refs, int32_t n_experts, uint64_t* misses,
+                            uint64_t* misses_upper) {
   if (!ids || !misses || steps < 0 || refs < 0 || n_experts < 1)
     return set_error(WISP_E_INVAL, "miss curve: NULL pointer or non-positive shape");
   for (int64_t i = 0; i < static_cast<int64_t>(steps) * refs; ++i)
@@ -97,8 +108,10 @@ wisp_status wisp_miss_curve(const int32_t* ids, int32_t steps, int32_t refs, int
   // steps holds one mark per expert, at the step of its latest reference; a step's distances are
   // read before its own marks move.
   std::vector<uint64_t> hist(static_cast<size_t>(n_experts) + 1, 0);
+  std::vector<uint64_t> hist_up(static_cast<size_t>(n_experts) + 1, 0);   // distance + peers
   uint64_t cold = 0;
   std::vector<int32_t> last(n_experts, -1);
+  std::vector<int32_t> step_size(static_cast<size_t>(std::max(steps, 1)), 0);   // distinct ids per step
   std::vector<int32_t> step_ids;
   Fenwick fw(static_cast<size_t>(std::max(steps, 1)));
   for (int32_t t = 0; t < steps; ++t) {
@@ -114,19 +127,25 @@ wisp_status wisp_miss_curve(const int32_t* ids, int32_t steps, int32_t refs, int
       } else {
         const int64_t dist = fw.prefix(static_cast<size_t>(t)) - fw.prefix(static_cast<size_t>(p) + 1);
         ++hist[static_cast<size_t>(std::min<int64_t>(dist, n_experts))];
+        // the other experts of step p share e's tick and may be evicted after it: the upper bound
+        const int64_t up = dist + step_size[static_cast<size_t>(p)] - 1;
+        ++hist_up[static_cast<size_t>(std::min<int64_t>(up, n_experts))];
       }
     }
+    step_size[static_cast<size_t>(t)] = static_cast<int32_t>(step_ids.size());
     for (int32_t e : step_ids) {
       if (last[e] >= 0) fw.add(static_cast<size_t>(last[e]), -1);
       fw.add(static_cast<size_t>(t), +1);
       last[e] = t;
     }
   }
-  // m(C) = cold + #{distance >= C}
-  uint64_t tail = 0;
+  // m(C) = cold + #{distance >= C}; the upper curve counts distance + peers >= C
+  uint64_t tail = 0, tail_up = 0;
   for (int32_t C = n_experts; C >= 0; --C) {
     tail += hist[C];
+    tail_up += hist_up[C];
     misses[C] = cold + tail;
+    if (misses_upper) misses_upper[C] = cold + tail_up;
   }
   return WISP_OK;
 }
@@ -261,6 +280,73 @@ wisp_status wisp_dual_resize(wisp_ctx* ctx, wisp_kv_pool* pool, int32_t cap_new,
     (void)wisp_set_budget(ctx, static_cast<uint64_t>(cap_old) * a, nullptr);
     return s;
   }
+  return WISP_OK;
+}
+
+wisp_status wisp_controller_create(const wisp_resize_law* law, int32_t cap_now, int64_t kv_blocks_now,
+                                   wisp_controller** out) {
+  if (!law || !out) return set_error(WISP_E_INVAL, "controller: NULL argument");
+  *out = nullptr;
+  int32_t c = 0, m = 0;
+  int64_t k = 0;
+  // the law must be valid (checked by evaluating it once) and the current split inside the budget
+  wisp_status s = wisp_resize_target(law, 0, cap_now, &c, &k, &m);
+  if (s != WISP_OK) return s;
+  if (cap_now < 0 || kv_blocks_now < 0 ||
+      static_cast<uint64_t>(cap_now) * law->expert_set_bytes + static_cast<uint64_t>(kv_blocks_now) *
+      law->kv_block_bytes > law->budget_bytes)
+    return set_error(WISP_E_INVAL, "controller: the current split exceeds the budget");
+  auto* ctl = new (std::nothrow) wisp_controller();
+  if (!ctl) return set_error(WISP_E_NOMEM, "controller: host allocation failed");
+  ctl->law = *law;
+  ctl->cap = cap_now;
+  ctl->kv = kv_blocks_now;
+  *out = ctl;
+  return WISP_OK;
+}
+
+wisp_status wisp_controller_observe(wisp_controller* ctl, int64_t kv_blocks_in_use) {
+  if (!ctl || kv_blocks_in_use < 0) return set_error(WISP_E_INVAL, "controller: bad observation");
+  ctl->peak = std::max(ctl->peak, kv_blocks_in_use);
+  ++ctl->observed;
+  return WISP_OK;
+}
+
+wisp_status wisp_controller_barrier(wisp_controller* ctl, wisp_ctx* ctx, wisp_kv_pool* pool, int32_t* cap_out,
+                                    int64_t* kv_blocks_out, int32_t* moved_out, int64_t* peak_out) {
+  if (!ctl) return set_error(WISP_E_INVAL, "controller: NULL controller");
+  if ((ctx == nullptr) != (pool == nullptr)) return set_error(WISP_E_INVAL, "controller: ctx and pool go together");
+  int32_t moved = 0;
+  const int64_t peak = ctl->peak;
+  if (peak >= 0) {
+    int32_t cap = 0, move = 0;
+    int64_t kv = 0;
+    wisp_status s = wisp_resize_target(&ctl->law, peak, ctl->cap, &cap, &kv, &move);
+    if (s != WISP_OK) return s;
+    if (move) {
+      s = ctx ? wisp_dual_resize(ctx, pool, cap, kv) : WISP_OK;
+      if (s == WISP_OK) {
+        ctl->cap = cap;
+        ctl->kv = kv;
+        moved = 1;
+      } else if (s == WISP_E_NOMEM) {
+        moved = -1;            // the move is skipped: the previous split stays in place (App. B)
+      } else {
+        return s;
+      }
+    }
+  }
+  ctl->peak = -1;
+  ctl->observed = 0;
+  if (cap_out) *cap_out = ctl->cap;
+  if (kv_blocks_out) *kv_blocks_out = ctl->kv;
+  if (moved_out) *moved_out = moved;
+  if (peak_out) *peak_out = peak;
+  return WISP_OK;
+}
+
+wisp_status wisp_controller_destroy(wisp_controller* ctl) {
+  delete ctl;
   return WISP_OK;
 }
 

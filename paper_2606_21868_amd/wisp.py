@@ -95,7 +95,7 @@ _SIGS = {
     "wisp_offload_step": [_P, _P, _I, _P, _P, _P, _P],
     "wisp_offload_end": [_P],
     "wisp_get_desc": [_P, ctypes.POINTER(ModelDesc)],
-    "wisp_miss_curve": [_P, _I, _I, _I, _P],
+    "wisp_miss_curve": [_P, _I, _I, _I, _P, _P],
     "wisp_mvwsa_configure": [ctypes.POINTER(MvwsaProblem), _P, _P, ctypes.POINTER(MvwsaSplit)],
     "wisp_resize_target": [ctypes.POINTER(ResizeLaw), ctypes.c_int64, _I, ctypes.POINTER(_I),
                            ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(_I)],
@@ -104,6 +104,11 @@ _SIGS = {
     "wisp_kv_pool_resize": [_P, ctypes.c_int64],
     "wisp_kv_pool_destroy": [_P],
     "wisp_dual_resize": [_P, _P, _I, ctypes.c_int64],
+    "wisp_controller_create": [ctypes.POINTER(ResizeLaw), _I, ctypes.c_int64, ctypes.POINTER(_P)],
+    "wisp_controller_observe": [_P, ctypes.c_int64],
+    "wisp_controller_barrier": [_P, _P, _P, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(_I),
+                                ctypes.POINTER(ctypes.c_int64)],
+    "wisp_controller_destroy": [_P],
     "wisp_get_stats": [_P, _I, ctypes.POINTER(PageStats)],
     "wisp_reset_stats": [_P],
     "wisp_get_cap": [_P, ctypes.POINTER(_I)],
@@ -492,15 +497,17 @@ class SlotTable:
 # ------------------------------------------------------------------------------------------------
 # Expert <-> KV allocator (wisp_mvwsa.h)
 # ------------------------------------------------------------------------------------------------
-def miss_curve(ids, n_experts):
-    """Expert miss curve m(C), C = 0..n_experts, of one layer's routing trace ids [steps, refs]."""
+def miss_curve(ids, n_experts, upper=False):
+    """Expert miss curve m(C), C = 0..n_experts, of one layer's routing trace ids [steps, refs]; with
+    upper=True also the upper-bound curve: (lower, upper)."""
     ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int32))
     if ids.ndim == 1:
         ids = ids[:, None]
     out = np.zeros(n_experts + 1, np.uint64)
-    check(lib().wisp_miss_curve(ids.ctypes.data, ids.shape[0], ids.shape[1], n_experts, out.ctypes.data),
-          "wisp_miss_curve")
-    return out
+    up = np.zeros(n_experts + 1, np.uint64) if upper else None
+    check(lib().wisp_miss_curve(ids.ctypes.data, ids.shape[0], ids.shape[1], n_experts, out.ctypes.data,
+                                up.ctypes.data if upper else None), "wisp_miss_curve")
+    return (out, up) if upper else out
 
 
 def mvwsa_configure(B, a, b, kv_min, c_exp, c_kv, m_exp, m_kv):
@@ -550,6 +557,42 @@ class KvPool:
 def dual_resize(ctx, pool, cap_new, kv_blocks_new):
     """The drained-barrier move of App. B between the expert scratch of ctx and the KV pool."""
     check(lib().wisp_dual_resize(ctx.h, pool.h, int(cap_new), int(kv_blocks_new)), "wisp_dual_resize")
+
+
+class Controller:
+    """The online dual-resize controller (wisp_controller_*): observe the KV blocks in use after each
+    decode step; barrier() at a drained barrier applies the control law to ctx and pool (or only
+    decides when both are None)."""
+
+    def __init__(self, B, a, b, kv_min, headroom, cap_min, cap_max, dead_zone, cap_now, kv_now):
+        law = ResizeLaw(int(B), int(a), int(b), int(kv_min), float(headroom), int(cap_min), int(cap_max),
+                        int(dead_zone))
+        self.h = _P()
+        check(lib().wisp_controller_create(ctypes.byref(law), int(cap_now), int(kv_now), ctypes.byref(self.h)),
+              "wisp_controller_create")
+
+    def observe(self, kv_blocks_in_use):
+        check(lib().wisp_controller_observe(self.h, int(kv_blocks_in_use)), "wisp_controller_observe")
+
+    def barrier(self, ctx=None, pool=None):
+        """Returns (cap, kv_blocks, moved, peak): the split after the barrier, 1 moved / 0 none / -1 a
+        failed move skipped, and the peak the law used (-1: nothing observed)."""
+        c, k, m, p = _I(), ctypes.c_int64(), _I(), ctypes.c_int64()
+        check(lib().wisp_controller_barrier(self.h, ctx.h if ctx is not None else None,
+                                            pool.h if pool is not None else None, ctypes.byref(c), ctypes.byref(k),
+                                            ctypes.byref(m), ctypes.byref(p)), "wisp_controller_barrier")
+        return c.value, k.value, m.value, p.value
+
+    def close(self):
+        if self.h:
+            check(lib().wisp_controller_destroy(self.h), "wisp_controller_destroy")
+            self.h = _P()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 # ------------------------------------------------------------------------------------------------

@@ -90,5 +90,59 @@ WORKLOADS = {
         route=ROUTE_SIGMOID_GROUP, budget_bytes=40_000_000_000, n_groups=8, topk_groups=4, has_shared=True),
 }
 
+def degraded_hints(idx, n_experts, precision, seed=0):
+    """Prefetch hints of a chosen precision for the speculative-prefetch experiment (Sec. 4): for each
+    (step, layer) of a routing trace idx [S, L, T, k], the distinct routed ids with a fraction
+    1 - precision of them (rounded) replaced by ids drawn without replacement from the experts that
+    step does not route to, in a seeded random order.  Returns hints [S, L, n] int32, n the largest
+    routed-set size, padded with -1.  precision 1 gives the true routing (a perfect predictor)."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    S, L = idx.shape[:2]
+    sets = [[np.unique(idx[s, l]) for l in range(L)] for s in range(S)]
+    n = max(len(r) for row in sets for r in row)
+    out = np.full((S, L, n), -1, np.int32)
+    for s in range(S):
+        for l in range(L):
+            r = sets[s][l]
+            m = int(round(len(r) * (1.0 - precision)))
+            others = np.setdiff1d(np.arange(n_experts), r)
+            m = min(m, others.size)
+            keep = rng.choice(r, size=len(r) - m, replace=False)
+            wrong = rng.choice(others, size=m, replace=False)
+            h = rng.permutation(np.concatenate([keep, wrong]))
+            out[s, l, :h.size] = h
+    return out
+
+
+KV_REGIMES = {
+    # per-session context at the start of a turn, as a fraction of a session's share of the initial KV
+    # pool, and the chance per decode step that a session's turn ends (a new one starts)
+    "tool": (0.15, 0.55, 0.08),      # short tool-call bursts: the pool is mostly idle
+    "long": (0.75, 1.00, 0.01),      # long-context turns: the pool is nearly full
+}
+
+
+def kv_occupancy_trace(regimes, pool_blocks, sessions=4, block_tokens=16, seed=0):
+    """A seeded KV-occupancy trace (blocks in use after each decode step) for the online allocator of
+    Sec. 3.5: `sessions` concurrent sessions whose contexts grow by one token per step; a turn ends with
+    the regime's probability and the next starts at a context drawn from the regime's range.  Every
+    session starts a new turn when the regime changes.  regimes: [(steps, "tool" | "long")].  Returns
+    int64 [sum of steps]."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    share = pool_blocks / sessions
+    out = []
+    for steps, kind in regimes:
+        lo, hi, p_end = KV_REGIMES[kind]
+        ctx = rng.uniform(lo, hi, sessions) * share * block_tokens          # tokens
+        for _ in range(steps):
+            ends = rng.random(sessions) < p_end
+            ctx[ends] = rng.uniform(lo, hi, int(ends.sum())) * share * block_tokens
+            ctx += 1.0
+            out.append(int(np.ceil(ctx / block_tokens).sum()))
+    return np.array(out, np.int64)
+
+
 # The benchmarked workload: the paged decode on which the decode-throughput metric is quoted.
 BENCH_WORKLOAD = "qwen3-30b-a3b-decode"

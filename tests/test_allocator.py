@@ -137,6 +137,8 @@ def test_library_miss_curve_matches_oracle(N, k, steps):
     want = A.reuse_curve(trace, N)
     got = wisp.miss_curve(trace, N)
     assert got.tolist() == want
+    lo, up = wisp.miss_curve(trace, N, upper=True)
+    assert lo.tolist() == want and up.tolist() == A.reuse_curve_upper(trace, N)
 
 
 def test_library_miss_curve_properties():
@@ -192,3 +194,39 @@ def test_library_resize_target_matches_oracle():
                 wisp.resize_target(B, a, b, kv_min, h, cmin, cmax, dz, peak, now)
             continue
         assert wisp.resize_target(B, a, b, kv_min, h, cmin, cmax, dz, peak, now) == want
+
+
+@pytest.mark.parametrize("seed,dz,every", [(0, 1, 4), (3, 2, 6), (5, 3, 8), (7, 0, 5)])
+def test_library_controller_matches_oracle_replay(seed, dz, every):
+    from paper_2606_21868_amd.workloads import kv_occupancy_trace
+    N, a, b, kv0 = 128, 28 << 20, 4 << 20, 600
+    B = 32 * a + kv0 * b
+    occ = kv_occupancy_trace([(3 * every, "tool"), (2 * every, "long"), (3 * every, "tool")], kv0, seed=seed)
+    want = A.controller_replay(B, a, b, 50, 0.2, 1, N, dz, 32, kv0, occ, every)
+    ctl = wisp.Controller(B, a, b, 50, 0.2, 1, N, dz, 32, kv0)
+    got = []
+    for s0 in range(0, occ.size, every):
+        for t in range(s0, s0 + every):
+            ctl.observe(int(occ[t]))
+        c, k, m, p = ctl.barrier()
+        got.append((s0 + every - 1, p, c, k, m))
+    assert got == want
+    assert ctl.barrier() == (want[-1][2], want[-1][3], 0, -1)       # nothing observed: no move
+    ctl.close()
+
+
+def test_library_controller_rejects_bad_arguments():
+    with pytest.raises(wisp.WispError):
+        wisp.Controller(100, 10, 1, 0, 0.2, 1, 8, 1, 20, 0)            # split beyond the budget
+    ctl = wisp.Controller(100, 10, 1, 0, 0.2, 1, 8, 1, 5, 50)
+    with pytest.raises(wisp.WispError):
+        ctl.observe(-1)
+    ctl.close()
+
+
+def test_kv_occupancy_trace_regimes():
+    from paper_2606_21868_amd.workloads import kv_occupancy_trace
+    occ = kv_occupancy_trace([(200, "tool"), (200, "long")], 1000, seed=1)
+    assert occ.shape == (400,) and occ.dtype == np.int64
+    assert occ[:200].max() < 0.7 * 1000 < occ[200:].min()
+    assert np.array_equal(occ, kv_occupancy_trace([(200, "tool"), (200, "long")], 1000, seed=1))

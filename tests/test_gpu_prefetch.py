@@ -4,7 +4,8 @@ A paged decode from a cold table with prefetch off is checked against the oracle
 outputs).  The same steps are then run again from a cold table with prefetch on:
 - PREDICTOR: each step's per-layer requests must be a valid top-`depth` of the oracle predictor's
   exact scores, replayed on the GPU's routing trace;
-- HINTS: the true routing of each step, given before it (a perfect predictor).
+- HINTS: the true routing of each step, given before it (a perfect predictor), and the same with
+  half of each step's ids replaced by experts it does not use (a predictor of precision 0.5).
 In both, the outputs must be bit-identical to the prefetch-off run (prefetch changes residency, never
 the arithmetic), and the hits, misses, prefetch copies and useful prefetches must equal the oracle's
 Algorithm 1 simulator replaying the same routing and the same prefetch requests.
@@ -18,7 +19,7 @@ import oracle
 from oracle.predictor import CoActivation
 from parity import check_run, log
 from paper_2606_21868_amd import wisp
-from paper_2606_21868_amd.workloads import WORKLOADS
+from paper_2606_21868_amd.workloads import WORKLOADS, degraded_hints
 
 torch = pytest.importorskip("torch")
 
@@ -112,6 +113,25 @@ def test_prefetch_keeps_bits_and_matches_the_oracle_replay(cap):
         assert np.array_equal(perfect["hits"], h) and np.array_equal(perfect["misses"], m)
         assert int(m.sum()) == 0 and (st["issued"], st["useful"]) == (issued, useful) and useful == issued
         log(f"  perfect hints: no demand fault, {issued} prefetch copies, all used; bits unchanged")
+
+        # hints at precision 0.5: half of each step's routed set replaced by experts it does not use
+        run.ctx.masters_ready()
+        run.ctx.reset_stats()
+        run.ctx.set_prefetch(wisp.PREFETCH_HINTS)
+        hints = degraded_hints(off["idx"], wl.N, 0.5, seed=cap)
+        half = run.decode(record=True, hints=hints, prefetch_log=True)
+        run.ctx.set_prefetch(wisp.PREFETCH_OFF)
+        assert np.array_equal(half["y"].view(np.uint32), off["y"].view(np.uint32))
+        for s in range(steps):
+            for l in range(wl.L):
+                assert sorted(half["requests"][s][l].tolist()) == sorted(int(e) for e in hints[s, l] if e >= 0)
+                assert len(set(hints[s, l].tolist()) & set(off["idx"][s, l].ravel().tolist())) == wl.k // 2
+        h, m, issued, useful = _replay(wl, cap, half["idx"], half["requests"])
+        st = run.ctx.prefetch_stats()
+        assert np.array_equal(half["hits"], h) and np.array_equal(half["misses"], m)
+        assert (st["issued"], st["useful"]) == (issued, useful) and useful < issued
+        log(f"  hints at precision 0.5: {int(m.sum())} faults + {issued} prefetch copies ({useful} used); "
+            f"bits unchanged")
     finally:
         run.close()
 
