@@ -212,13 +212,22 @@ def configurator_leg(run, wl, wisp, torch, link_cu, warmup=16, steps=96):
     run.ctx.set_pager(wisp.PAGER_DEVICE)
     rec = run.decode(record=True, steps=run.steps, start=0)
     S = run.steps
-    lo = np.zeros(wl.N + 1)
-    up = np.zeros(wl.N + 1)
-    for l in range(wl.L):
-        c_lo, c_up = wisp.miss_curve(rec["idx"][:, l].reshape(S, -1), wl.N, upper=True)
-        lo += c_lo
-        up += c_up
-    m_exp = np.round(lo / S).astype(np.uint64)                  # expert faults per decode step
+
+    def curves(n_steps):
+        """Sum over layers of the lower and upper curves of the first n_steps of the recorded routing."""
+        lo_, up_ = np.zeros(wl.N + 1), np.zeros(wl.N + 1)
+        for l in range(wl.L):
+            c_lo, c_up = wisp.miss_curve(rec["idx"][:n_steps, l].reshape(n_steps, -1), wl.N, upper=True)
+            lo_ += c_lo
+            up_ += c_up
+        return lo_, up_
+
+    lo, up = curves(S)
+    # a reference's classification depends only on earlier steps, so the faults of the window the
+    # chosen split is timed on are the curves of the longer prefix minus those of the warmup prefix
+    lo_w, up_w = [a - b for a, b in zip(curves(warmup + steps), curves(warmup))]
+    lo_warm, _ = curves(warmup)
+    m_exp = np.round((lo - lo_warm) / (S - warmup)).astype(np.uint64)   # expert faults per warm decode step
     kv_min = 4 * math.ceil(4096 / 16)
     m_kv = np.maximum(0, demand - np.arange(demand + 1)).astype(np.float64)
     c_exp = wl.blob / (link_cu * 1e9)
@@ -243,12 +252,13 @@ def configurator_leg(run, wl, wisp, torch, link_cu, warmup=16, steps=96):
                                              for c in (8, 16, 32, 64, 128, cap) if c <= wl.N}),
                recorded_cap=wl.cap, recorded_faults_per_step=float(whole / S),
                recorded_within_curves=bool(lo[wl.cap] <= whole <= up[wl.cap]),
-               chosen=dict(cap=cap, tokens_per_s=wl.T * steps / el,
+               chosen=dict(cap=cap, tokens_per_s=wl.T * steps / el, window_steps=[warmup, warmup + steps],
                            faults_per_step=float(o["misses"].sum()) / steps,
-                           curve_bounds_per_step=[float(lo[cap] / S), float(up[cap] / S)]))
+                           curve_bounds_per_step=[float(lo_w[cap] / steps), float(up_w[cap] / steps)],
+                           within_curves=bool(lo_w[cap] <= o["misses"].sum() <= up_w[cap])))
     log(f"configurator: B {B / (1 << 30):.2f} GiB -> cap {cap} / KV {res['kv_GiB']:.2f} GiB (f = {split['f']:.3f}, "
         f"floor binding {split['floor_binding']}); decode {res['chosen']['tokens_per_s']:.2f} tokens/s, "
-        f"{res['chosen']['faults_per_step']:.1f} faults per step (curve {lo[cap] / S:.1f}..{up[cap] / S:.1f})")
+        f"{res['chosen']['faults_per_step']:.1f} faults per step (curve {lo_w[cap] / steps:.1f}..{up_w[cap] / steps:.1f})")
     return res
 
 

@@ -101,7 +101,8 @@ wisp_status wisp_destroy(wisp_ctx* ctx);
 wisp_status wisp_expert_host_ptr(wisp_ctx* ctx, int32_t layer, int32_t expert, void** ptr, uint64_t* bytes);
 
 /* Declare the masters final: copies the shared experts to their fixed device slab and drops every
- * resident expert so later faults re-read the masters.  Synchronous. */
+ * resident expert so later faults re-read the masters: every layer's slot table restarts cold (all
+ * slots empty, LRU clock at 0).  Synchronous. */
 wisp_status wisp_masters_ready(wisp_ctx* ctx);
 
 /* Router weights of `layer`: device pointer to W_r [N, d] fp32 row-major, caller-owned, valid
@@ -275,6 +276,14 @@ wisp_status wisp_probe_mfma(int32_t launches, double* tflops);
 /* Decode n fp8 E4M3 codes to fp32 on the device with the same conversion the FFN kernels use
  * (for checking the hardware conversion against the format definition). */
 wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n, void* stream);
+
+/* Hazard check for tests (host pager): with on != 0, every slot chosen as a victim is overwritten
+ * with 0xFF bytes (NaN in every weight format, and in the fp8 block scales) on the side stream right
+ * after the stream's write-after-read wait on the layer's last FFN, before the fill copies the
+ * master in (faults, chunked unions and speculative prefetch alike).  Outputs stay exact exactly when
+ * every FFN read of a slot is ordered after its fill and every fill after the slot's last read
+ * (Sec. 3.2, the exactness invariant).  Costs one memset per fault. */
+wisp_status wisp_debug_poison_victims(wisp_ctx* ctx, int32_t on);
 
 /* Fault injection for tests of the transactional resize: the next `n`-th device slot allocation
  * (counting from 1, across later wisp_set_budget calls) fails as if out of memory.  0 = off. */

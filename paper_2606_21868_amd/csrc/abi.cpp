@@ -143,6 +143,7 @@ struct wisp_ctx {
   } off;
   int32_t fail_alloc_at = 0;
   int32_t alloc_counter = 0;
+  bool poison = false;               // debug: victim slots overwritten with NaN bytes before each fill
   // device pager (WISP_PAGER_DEVICE): the slot tables in HBM are authoritative while it is on
   int32_t pager = WISP_PAGER_HOST;
   int32_t dev_cap = 0;               // C the device arrays are sized for
@@ -156,6 +157,8 @@ struct wisp_ctx {
   uint32_t* h_stats = nullptr;       // pinned copy
   bool fusion = true;                // fused decode kernels (route + page; down + combine)
   uint32_t* d_arrive = nullptr;      // route + page: logit rows completed in the running launch
+  uint64_t* d_logit_tags = nullptr;  // [4][N] tagged logit words of the one-launch router kernels
+  uint32_t logit_tag = 0;            // tag of the last such launch (never 0)
   // speculative prefetch inside wisp_decode_step (host pager)
   int32_t pf_mode = WISP_PREFETCH_OFF;
   wisp_predictor* pf_pred = nullptr;
@@ -224,6 +227,12 @@ void harvest(wisp_ctx* c, bool wait) {
     c->ev_pool.push_back(p.b);
   }
   c->timed.resize(keep);
+}
+
+// The tag of the next one-launch router kernel: a sequence number that skips 0 (the words start at 0).
+uint32_t next_logit_tag(wisp_ctx* c) {
+  if (++c->logit_tag == 0) ++c->logit_tag;
+  return c->logit_tag;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -323,6 +332,7 @@ void free_ctx(wisp_ctx* c) {
     if (p) hipFree(p);
   if (c->h_stats) hipHostFree(c->h_stats);
   if (c->d_arrive) hipFree(c->d_arrive);
+  if (c->d_logit_tags) hipFree(c->d_logit_tags);
   delete c;
 }
 
@@ -459,6 +469,18 @@ wisp_status fill_slots(wisp_ctx* c, int32_t layer, const std::vector<std::pair<i
   return WISP_OK;
 }
 
+// Debug hazard check: after the side stream's write-after-read wait, fill each victim slot with 0xFF
+// bytes (NaN in fp32, bf16 and E4M3, and in the bf16 block scales) before its copy.  A read of a slot
+// that is not ordered after its fill, or a fill not ordered after the slot's last read, then shows up
+// as NaN in the outputs instead of as plausible stale weights.
+wisp_status poison_slots(wisp_ctx* c, int32_t layer, const std::vector<std::pair<int32_t, int32_t>>& fills) {
+  if (!c->poison) return WISP_OK;
+  LayerState& L = c->layers[layer];
+  for (const auto& f : fills)
+    WISP_HIP(hipMemsetAsync(L.slot_mem[f.second], 0xFF, c->blob.bytes, c->side), "hipMemsetAsync(poison)");
+  return WISP_OK;
+}
+
 wisp_status issue_fills(wisp_ctx* c, int32_t layer, size_t ci) {
   LayerState& L = c->layers[layer];
   const ChunkPlan& cp = L.plan.chunks[ci];
@@ -474,7 +496,9 @@ wisp_status issue_fills(wisp_ctx* c, int32_t layer, size_t ci) {
   for (size_t i = 0; i < cp.experts.size(); ++i)
     if (cp.fault[i]) fills.push_back({cp.experts[i], cp.slots[i]});
   const bool batch = L.T >= kGroupedMinTokens && grouped_supported(c->shape, c->desc.has_shared);
-  wisp_status s = fill_slots(c, layer, fills, batch);
+  wisp_status s = poison_slots(c, layer, fills);
+  if (s != WISP_OK) return s;
+  s = fill_slots(c, layer, fills, batch);
   if (s != WISP_OK) return s;
   if (tm.stop) WISP_HIP(hipEventRecord(tm.stop, c->side), "hipEventRecord");
   timing_end(c, tm, WISP_K_H2D_FILL, static_cast<uint64_t>(cp.n_faults) * c->blob.bytes);
@@ -549,7 +573,9 @@ wisp_status prefetch_layer(wisp_ctx* c, int32_t layer, const int32_t* ids, int32
   if (L.use_ev_recorded) WISP_HIP(hipStreamWaitEvent(c->side, L.use_ev, 0), "hipStreamWaitEvent(use)");
   LaunchTiming tm = timing_begin(c, WISP_K_H2D_FILL);
   if (tm.start) WISP_HIP(hipEventRecord(tm.start, c->side), "hipEventRecord");
-  wisp_status s = fill_slots(c, layer, fills, false);
+  wisp_status s = poison_slots(c, layer, fills);
+  if (s != WISP_OK) return s;
+  s = fill_slots(c, layer, fills, false);
   if (s != WISP_OK) return s;
   for (const auto& f : fills) {
     L.pf_inflight.push_back(f.first);
@@ -696,6 +722,10 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   if (hipMalloc(&p, 256) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
   c->d_arrive = static_cast<uint32_t*>(p);
   if (hipMemset(c->d_arrive, 0, 256) != hipSuccess) return bail(WISP_E_HIP, "hipMemset(counter)");
+  if (hipMalloc(&p, sizeof(uint64_t) * 4 * N) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
+  c->d_logit_tags = static_cast<uint64_t*>(p);
+  if (hipMemset(c->d_logit_tags, 0, sizeof(uint64_t) * 4 * N) != hipSuccess)
+    return bail(WISP_E_HIP, "hipMemset(logit tags)");
 
   c->pair_order.resize(static_cast<size_t>(T) * k);
   *out = c;
@@ -939,7 +969,8 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
   if (ctx->fusion && T <= 4) {
     // logits and selection in one launch (the workgroup completing the logits selects)
     LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
-    WISP_HIP(launch_route_select(L.wr, x_dev, d.x_dtype, d.d_model, ctx->logits, ctx->d_arrive, T, d.n_experts,
+    WISP_HIP(launch_route_select(L.wr, x_dev, d.x_dtype, d.d_model, ctx->d_logit_tags, next_logit_tag(ctx),
+                                 ctx->d_arrive, T, d.n_experts,
                                  d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev, w_dev,
                                  publish ? ctx->idx_tagged : nullptr, seq, st, t1),
              "router logits + select launch");
@@ -1279,7 +1310,8 @@ wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_
       const uint64_t* slot_l = ctx->d_slot_ptr + static_cast<size_t>(l) * C;
       if (ctx->fusion) {
         LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
-        WISP_HIP(launch_route_page(L.wr, xl, d.x_dtype, d.d_model, ctx->logits, ctx->d_arrive, T, d.n_experts, d.top_k,
+        WISP_HIP(launch_route_page(L.wr, xl, d.x_dtype, d.d_model, ctx->d_logit_tags, next_logit_tag(ctx),
+                                   ctx->d_arrive, T, d.n_experts, d.top_k,
                                    d.route, d.n_groups, d.topk_groups, il, wl, pi_l, pinv_l, tau_l, ctx->d_clock + l, C,
                                    slot_l, ctx->masters[l], ctx->master_stride, L.shared_dev, d.has_shared,
                                    ctx->d_plan, ctx->d_stats + 2 * l, sm, t1),
@@ -1819,6 +1851,13 @@ wisp_status wisp_probe_mfma(int32_t launches, double* tflops) {
 wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n, void* stream) {
   if (!codes_dev || !out_dev || n < 0) return fail(WISP_E_INVAL, "bad argument");
   WISP_HIP(launch_decode_fp8(codes_dev, out_dev, n, static_cast<hipStream_t>(stream)), "decode launch");
+  return WISP_OK;
+}
+
+wisp_status wisp_debug_poison_victims(wisp_ctx* ctx, int32_t on) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  ctx->poison = on != 0;
   return WISP_OK;
 }
 

@@ -79,8 +79,10 @@ __device__ __forceinline__ void tile_of(const GroupedBatch& gb, int n_ctiles, in
 // off[e] + (earlier pairs of e in earlier waves) + (earlier pairs of e in this wave).
 __global__ void __launch_bounds__(1024) permute_pairs_kernel(const int32_t* __restrict__ idx, int P, int N,
                                                              int32_t* __restrict__ perm) {
+  constexpr int kBatch = 8;            // chunks of 64 pairs whose ids a wave loads before using any
   __shared__ int32_t cnt[16][256];
   __shared__ int32_t base[257];
+  __shared__ int32_t wsum[4];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   for (int i = tid; i < 16 * 256; i += 1024) (&cnt[0][0])[i] = 0;
   __syncthreads();
@@ -88,25 +90,37 @@ __global__ void __launch_bounds__(1024) permute_pairs_kernel(const int32_t* __re
   const int p0 = wave * seg, p1 = min(P, p0 + seg);
   const uint64_t below = (1ull << lane) - 1ull;
   for (int pass = 0; pass < 2; ++pass) {
-    for (int c0 = p0; c0 < p1; c0 += 64) {
-      const int p = c0 + lane;
-      const bool valid = p < p1;
-      const int e = valid ? idx[p] : 0;
-      uint64_t same = __ballot(valid);
+    for (int cb = p0; cb < p1; cb += 64 * kBatch) {
+      int ev[kBatch];
 #pragma unroll
-      for (int b = 0; b < 8; ++b) {
-        const bool bit = (e >> b) & 1;
-        const uint64_t m = __ballot(bit);
-        same &= bit ? m : ~m;
+      for (int q = 0; q < kBatch; ++q) {   // the loads of kBatch chunks go out together
+        const int p = cb + q * 64 + lane;
+        ev[q] = p < p1 ? idx[p] : 0;
       }
-      if (valid) {
-        const int before = cnt[wave][e];
-        if (pass == 1) perm[base[e] + before + __popcll(same & below)] = p;
-        if ((same & below) == 0) cnt[wave][e] = before + __popcll(same);
+#pragma unroll
+      for (int q = 0; q < kBatch; ++q) {
+        const int c0 = cb + q * 64;
+        if (c0 >= p1) break;               // uniform across the wave
+        const int p = c0 + lane;
+        const bool valid = p < p1;
+        const int e = ev[q];
+        uint64_t same = __ballot(valid);
+#pragma unroll
+        for (int bi = 0; bi < 8; ++bi) {
+          const bool bit = (e >> bi) & 1;
+          const uint64_t m = __ballot(bit);
+          same &= bit ? m : ~m;
+        }
+        if (valid) {
+          const int before = cnt[wave][e];
+          if (pass == 1) perm[base[e] + before + __popcll(same & below)] = p;
+          if ((same & below) == 0) cnt[wave][e] = before + __popcll(same);
+        }
       }
     }
     __syncthreads();
     if (pass == 0) {
+      // per expert: the waves' counts to exclusive offsets inside the expert, and its total
       if (tid < N) {
         int run = 0;
         for (int w = 0; w < 16; ++w) {
@@ -117,14 +131,24 @@ __global__ void __launch_bounds__(1024) permute_pairs_kernel(const int32_t* __re
         base[tid] = run;
       }
       __syncthreads();
-      if (tid == 0) {
-        int run = 0;
-        for (int e = 0; e < N; ++e) {
-          const int c = base[e];
-          base[e] = run;
-          run += c;
+      // experts' totals to exclusive offsets: an inclusive scan per wave (threads 0..255), then the
+      // totals of the waves before; base[N] is the number of pairs
+      int v = 0, x = 0;
+      if (tid < 256) {
+        v = tid < N ? base[tid] : 0;
+        x = v;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const int y = __shfl_up(x, off, 64);
+          if (lane >= off) x += y;
         }
-        base[N] = run;
+        if (lane == 63) wsum[wave] = x;
+      }
+      __syncthreads();
+      if (tid < 256) {
+        for (int w = 0; w < wave; ++w) x += wsum[w];
+        if (tid < N) base[tid] = x - v;
+        if (tid == 255) base[N] = x;
       }
       __syncthreads();
     }

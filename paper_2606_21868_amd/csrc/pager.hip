@@ -90,15 +90,16 @@ __device__ __forceinline__ void store_table(PagerShared& sh, int N, int C, const
 
 // Selection, Algorithm 1 and the launch plan for one layer-step, by one workgroup whose table is in
 // sh (load_table) and whose threads have not yet synchronised since.
-template <bool COHERENT>
+template <bool TAGGED>
 __device__ __forceinline__ void select_and_page(
-    PagerShared& sh, const float* __restrict__ logits, int T, int N, int k, int route, int n_groups, int topk_groups,
+    PagerShared& sh, const void* __restrict__ logits, uint32_t tag, int T, int N, int k, int route, int n_groups,
+    int topk_groups,
     int32_t* __restrict__ idx, float* __restrict__ w, int32_t* __restrict__ pi, int32_t* __restrict__ pinv,
     uint64_t* __restrict__ tau, uint64_t* __restrict__ clock, int C, const uint8_t* master_base,
     uint64_t master_stride, const uint8_t* shared_dev, int has_shared, FfnBatch* __restrict__ plan,
     uint32_t* __restrict__ stats) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  select_tokens<COHERENT>(logits, 0, T, N, k, route, n_groups, topk_groups, sh.s);   // ends with a barrier
+  select_tokens<TAGGED>(logits, tag, 0, T, N, k, route, n_groups, topk_groups, sh.s);   // ends with a barrier
   if (wave < T && lane < k) {
     idx[wave * k + lane] = sh.s.sel[wave][lane];
     w[wave * k + lane] = sh.s.gate[wave][lane];
@@ -208,17 +209,18 @@ __global__ void __launch_bounds__(256) select_page_kernel(
     FfnBatch* __restrict__ plan, uint32_t* __restrict__ stats) {
   __shared__ PagerShared sh;
   load_table(sh, N, C, pi, pinv, tau, clock, slot_ptr);
-  select_and_page<false>(sh, logits, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
+  select_and_page<false>(sh, logits, 0, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
                          master_base, master_stride, shared_dev, has_shared, plan, stats);
 }
 
 // Router logits, selection and Algorithm 1 of one layer-step in one launch.  Workgroup e computes
-// logit row e (router_row, as the router kernel does), publishes it at device scope and counts
-// itself in *arrive; the workgroup whose arrival is the N-th resets the counter and runs the
-// selection and the pager on the complete logits.  No workgroup waits for another.
+// logit row e (router_row, as the router kernel does), publishes it as tagged words (tag_logit, one
+// atomic store each) and counts itself in *arrive; the workgroup whose arrival is the N-th resets the
+// counter and runs the selection and the pager on the complete logits, reading each word until it
+// carries this launch's tag.  No workgroup waits for another's progress.
 template <int XT>
 __global__ void __launch_bounds__(256) route_page_kernel(
-    const float* __restrict__ wr, const void* __restrict__ x, int d, float* __restrict__ logits,
+    const float* __restrict__ wr, const void* __restrict__ x, int d, uint64_t* __restrict__ logits, uint32_t tag,
     uint32_t* __restrict__ arrive, int T, int N, int k, int route, int n_groups, int topk_groups,
     int32_t* __restrict__ idx, float* __restrict__ w, int32_t* __restrict__ pi, int32_t* __restrict__ pinv,
     uint64_t* __restrict__ tau, uint64_t* __restrict__ clock, int C, const uint64_t* __restrict__ slot_ptr,
@@ -234,28 +236,25 @@ __global__ void __launch_bounds__(256) route_page_kernel(
   const TableRegs tab = load_table_regs(N, C, pi, pinv, tau, clock, slot_ptr);
   const float z = router_row<XT>(wr, x, 0, T, d, e, part);
   if (static_cast<int>(threadIdx.x) < T)
-    __hip_atomic_store(logits + static_cast<size_t>(threadIdx.x) * N + e, z, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  // The storing threads (t < T <= 4) are in wave 0 with thread 0; the barrier orders their stores
-  // before thread 0's arrival, whose release at agent scope publishes the row to every workgroup of
-  // the device that acquires the count.
+    __hip_atomic_store(logits + static_cast<size_t>(threadIdx.x) * N + e, tag_logit(tag, z), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (threadIdx.x == 0) {
-    const uint32_t before = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t before = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     last = before + 1 == static_cast<uint32_t>(N);
     if (last) __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
   if (!last) return;
-  // every thread of the last workgroup: its later loads see all N published rows
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   store_table(sh, N, C, tab);   // read after select_tokens' first barrier
-  select_and_page<true>(sh, logits, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
+  select_and_page<true>(sh, logits, tag, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
                         master_base, master_stride, shared_dev, has_shared, plan, stats);
 }
 
 }  // namespace
 
-hipError_t launch_route_page(const float* wr, const void* x, int x_dtype, int d, float* logits, uint32_t* arrive, int T,
+hipError_t launch_route_page(const float* wr, const void* x, int x_dtype, int d, uint64_t* logits, uint32_t tag,
+                             uint32_t* arrive, int T,
                              int N, int k, int route, int n_groups, int topk_groups, int32_t* idx, float* w,
                              int32_t* pi, int32_t* pinv, uint64_t* tau, uint64_t* clock, int C,
                              const uint64_t* slot_ptr, const uint8_t* master_base, uint64_t master_stride,
@@ -266,11 +265,11 @@ hipError_t launch_route_page(const float* wr, const void* x, int x_dtype, int d,
     return hipErrorInvalidValue;
   if (x_dtype == DT_F32)
     hipExtLaunchKernelGGL(route_page_kernel<DT_F32>, dim3(N), dim3(256), 0, st, tm.start, tm.stop, 0, wr, x, d, logits,
-                          arrive, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C, slot_ptr,
+                          tag, arrive, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C, slot_ptr,
                           master_base, master_stride, shared_dev, has_shared, plan, stats);
   else
     hipExtLaunchKernelGGL(route_page_kernel<DT_BF16>, dim3(N), dim3(256), 0, st, tm.start, tm.stop, 0, wr, x, d,
-                          logits, arrive, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
+                          logits, tag, arrive, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
                           slot_ptr, master_base, master_stride, shared_dev, has_shared, plan, stats);
   return hipGetLastError();
 }

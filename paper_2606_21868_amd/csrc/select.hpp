@@ -36,23 +36,46 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 
 __device__ __forceinline__ float sel_sigmoid(float z) { return 1.0f / (1.0f + __expf(-z)); }
 
+// A logit published by another workgroup of the running kernel: one 64-bit word, the launch's tag
+// above the fp32 bits, written by a single atomic store.
+__device__ __forceinline__ uint64_t tag_logit(uint32_t tag, float z) {
+  return (static_cast<uint64_t>(tag) << 32) | __float_as_uint(z);
+}
+
+// Spins (bounded) until the word carries `tag`.  Atomic accesses to one location are coherent, so once
+// the publishing workgroup's store is visible the word holds this launch's logit; every publisher has
+// issued its store before it counted itself, so the wait is short.  After kTagSpins polls the word is
+// used as it is (a bound that a store already issued never reaches).
+constexpr int kTagSpins = 1 << 22;
+__device__ __forceinline__ float read_tagged_logit(const uint64_t* p, uint32_t tag) {
+  uint64_t v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (int i = 0; static_cast<uint32_t>(v >> 32) != tag && i < kTagSpins; ++i) {
+    __builtin_amdgcn_s_sleep(1);
+    v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  return __uint_as_float(static_cast<uint32_t>(v));
+}
+
 // Tokens t0 .. t0+3 (those < T) of logits [T, N]; all 256 threads must call it.  Thread e owns
 // expert e of every token (N <= 256).  A key packs the order-preserving bits of the logit above
 // 255 - id, so (logit desc, id asc) is plain unsigned order and every allowed key is distinct:
-// the rank of an expert is the number of larger keys.  COHERENT: the logits were written by other
-// workgroups of the running kernel, so they are read at device scope.
-template <bool COHERENT = false>
-__device__ __forceinline__ void select_tokens(const float* __restrict__ logits, int t0, int T, int N, int k, int route,
-                                              int n_groups, int topk_groups, SelectShared& sh) {
+// the rank of an expert is the number of larger keys.  TAGGED: the logits are 64-bit tagged words
+// published by other workgroups of the running kernel (tag_logit), read until they carry `tag`;
+// otherwise plain fp32 written by an earlier kernel.
+template <bool TAGGED = false>
+__device__ __forceinline__ void select_tokens(const void* __restrict__ logits, uint32_t tag, int t0, int T, int N,
+                                              int k, int route, int n_groups, int topk_groups, SelectShared& sh) {
   const int tid = threadIdx.x;
   const int nt = min(4, T - t0);
   const int e = tid;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     if (t >= nt) break;
-    const float* zp = logits + static_cast<size_t>(t0 + t) * N + e;
+    const size_t at = static_cast<size_t>(t0 + t) * N + e;
     float z = 0.f;
-    if (e < N) z = COHERENT ? __hip_atomic_load(zp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : *zp;
+    if (e < N)
+      z = TAGGED ? read_tagged_logit(static_cast<const uint64_t*>(logits) + at, tag)
+                 : static_cast<const float*>(logits)[at];
     sh.z[t][e] = z;
     sh.key[t][e] = e < N ? (static_cast<uint64_t>(order_key(z)) << 32) | static_cast<uint32_t>(255 - e) : 0ull;
   }

@@ -13,10 +13,14 @@ SlotTable::SlotTable(int32_t n_experts, int32_t cap)
   cand_.reserve(cap);
 }
 
+// A cold table: every slot empty and the clock back at 0, as before the first step.  (A clock left
+// running would give a prefetch before the first step a tick above the empty slots' 0, where a
+// cold table gives it 0: the victim order of the next step would then differ.)
 void SlotTable::clear() {
   std::fill(pi_.begin(), pi_.end(), -1);
   std::fill(pinv_.begin(), pinv_.end(), -1);
   std::fill(tau_.begin(), tau_.end(), 0);
+  clock_ = 0;
 }
 
 void SlotTable::export_state(int32_t* pi, int32_t* pinv, uint64_t* tau, uint64_t* clock) const {

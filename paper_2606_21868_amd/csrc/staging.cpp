@@ -29,8 +29,14 @@ hipError_t BounceRing::init(int threads) {
 }
 
 hipError_t BounceRing::copy_to_device(void* dst, const uint8_t* src, size_t bytes, hipStream_t st) {
-  for (size_t off = 0; off < bytes; off += kPieceBytes) {
-    const size_t n = std::min(kPieceBytes, bytes - off);
+  // the link is idle when no earlier piece's copy is still pending: then it waits for this copy's
+  // first host copy, which is kept small; behind pending copies full pieces keep it busy
+  bool idle = true;
+  for (int i = 0; i < kBuffers && idle; ++i)
+    if (used_[i] && hipEventQuery(ev_[i]) != hipSuccess) idle = false;
+  size_t piece = idle ? kFirstPieceBytes : kPieceBytes;
+  for (size_t off = 0; off < bytes; off += piece, piece = std::min(kPieceBytes, 2 * piece)) {
+    const size_t n = std::min(piece, bytes - off);
     const int b = next_;
     next_ = (next_ + 1) % kBuffers;
     if (used_[b]) {

@@ -5,7 +5,9 @@
 // ordinary pageable memory, and each copy goes piece by piece through pinned bounce buffers:
 // host threads copy a piece into a free buffer, a DMA copy on the stream moves it to the device,
 // and an event recorded after it frees the buffer again.  The host copy of the next piece overlaps
-// the DMA of the previous ones.
+// the DMA of the previous ones.  A copy that finds the link idle starts with a small piece and
+// doubles it up to the buffer size: the link waits for the host copy of the first piece only, so
+// that piece is kept short.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -19,7 +21,8 @@ namespace wisp {
 
 class BounceRing {
  public:
-  static constexpr size_t kPieceBytes = 32ull << 20;
+  static constexpr size_t kPieceBytes = 32ull << 20;        // buffer size, the largest piece
+  static constexpr size_t kFirstPieceBytes = 4ull << 20;     // the first piece of a copy from idle
   static constexpr int kBuffers = 4;
   BounceRing() = default;
   ~BounceRing();

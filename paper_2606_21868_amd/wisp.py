@@ -126,6 +126,7 @@ _SIGS = {
     "wisp_probe_mfma": [_I, ctypes.POINTER(ctypes.c_double)],
     "wisp_decode_fp8": [_P, _P, _I, _P],
     "wisp_debug_fail_slot_alloc": [_P, _I],
+    "wisp_debug_poison_victims": [_P, _I],
     "wisp_predictor_create": [_I, _I, _I, ctypes.c_double, ctypes.POINTER(_P)],
     "wisp_predictor_destroy": [_P],
     "wisp_predictor_shape": [_P, ctypes.POINTER(_I), ctypes.POINTER(_I)],
@@ -342,6 +343,10 @@ class Context:
         else:
             check(lib().wisp_probe_h2d_engine(self.h, count, reps, engine, ctypes.byref(g)), "wisp_probe_h2d_engine")
         return g.value
+
+    def debug_poison_victims(self, on):
+        """Overwrite every victim slot with NaN bytes after its write-after-read wait, before its fill."""
+        check(lib().wisp_debug_poison_victims(self.h, int(bool(on))), "wisp_debug_poison_victims")
 
     def debug_fail_slot_alloc(self, n):
         check(lib().wisp_debug_fail_slot_alloc(self.h, n), "wisp_debug_fail_slot_alloc")

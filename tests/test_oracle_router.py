@@ -15,8 +15,8 @@ import oracle
 def test_bf16_decoder_all_codes():
     codes = np.arange(65536, dtype=np.uint32).astype(np.uint16)
     ref = torch.from_numpy(codes.view(np.int16)).view(torch.bfloat16).double().numpy()
-    got = np.array([oracle.bf16_value(c) for c in codes[::7]])
-    r = ref[::7]
+    got = np.array([oracle.bf16_value(c) for c in codes])
+    r = ref
     both_nan = np.isnan(got) & np.isnan(r)
     assert np.array_equal(got[~both_nan], r[~both_nan])
     assert np.array_equal(np.isnan(got), np.isnan(r))
