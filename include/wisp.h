@@ -277,6 +277,25 @@ wisp_status wisp_probe_mfma(int32_t launches, double* tflops);
  * (for checking the hardware conversion against the format definition). */
 wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n, void* stream);
 
+/* Router scoring and top-k for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the selection of wisp_route_topk
+ * without a context.  Routes T tokens x_dev [T, d] (x_dtype WISP_F32 or WISP_BF16) with router weights
+ * w_r_dev [N, d] fp32 row-major into idx_dev [T, k] int32 and w_dev [T, k] fp32 on `stream`, ranks
+ * ordered (score desc, expert id asc), route / n_groups / topk_groups as in wisp_model_desc.  It runs
+ * the same kernels as wisp_route_topk with fusion on (one launch for T <= 4, logits then selection
+ * above), so ids and gates are bit-identical to it; nothing is published to the host.
+ * Allocates nothing: its scratch (the logits and an arrival counter) is a fixed device array of
+ * 256 + 8192 + 4 * WISP_NOALLOC_MAX_LOGITS bytes that each device the library runs on holds until the process
+ * ends; its address is looked up on the first call on a device (which also clears the counter and the
+ * tag words with a kernel on `stream`).  Every call on a device shares that array: calls that overlap on one device
+ * (other streams, other threads) race and must be serialised by the caller.  WISP_E_INVAL when
+ * T * N > WISP_NOALLOC_MAX_LOGITS, for a null pointer or an unsupported shape (more than 8 tokens need
+ * d a multiple of 32); validation happens before any GPU call. */
+#define WISP_NOALLOC_MAX_LOGITS 524288
+wisp_status wisp_route_topk_noalloc(const float* w_r_dev, const void* x_dev, int32_t x_dtype, int32_t T, int32_t N,
+                                    int32_t d, int32_t k, int32_t route, int32_t n_groups, int32_t topk_groups,
+                                    int32_t* idx_dev, float* w_dev, void* stream);
+
 /* Hazard check for tests (host pager): with on != 0, every slot chosen as a victim is overwritten
  * with 0xFF bytes (NaN in every weight format, and in the fp8 block scales) on the side stream right
  * after the stream's write-after-read wait on the layer's last FFN, before the fill copies the

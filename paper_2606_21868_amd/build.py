@@ -28,7 +28,7 @@ HIP_FLAGS = [
 ]
 
 HIP_SOURCES = ["abi.cpp", "slot_table.cpp", "staging.cpp", "copy_pool.cpp", "mvwsa.cpp", "predictor.cpp", "router.hip", "expert_ffn.hip", "combine.hip", "probe.hip", "fill.hip",
-               "pager.hip", "grouped_gemm.hip"]
+               "pager.hip", "grouped_gemm.hip", "noalloc.cpp"]
 
 
 def _run(cmd):

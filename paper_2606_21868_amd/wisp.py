@@ -127,6 +127,7 @@ _SIGS = {
     "wisp_decode_fp8": [_P, _P, _I, _P],
     "wisp_debug_fail_slot_alloc": [_P, _I],
     "wisp_debug_poison_victims": [_P, _I],
+    "wisp_route_topk_noalloc": [_P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P],
     "wisp_predictor_create": [_I, _I, _I, ctypes.c_double, ctypes.POINTER(_P)],
     "wisp_predictor_destroy": [_P],
     "wisp_predictor_shape": [_P, ctypes.POINTER(_I), ctypes.POINTER(_I)],
@@ -435,6 +436,17 @@ def probe_mfma(launches):
 
 def hbm_copy(src, dst, nbytes, stream=None):
     check(lib().wisp_hbm_copy(_ptr(src), _ptr(dst), int(nbytes), _stream(stream)), "wisp_hbm_copy")
+
+
+NOALLOC_MAX_LOGITS = 524288
+
+
+def route_topk_noalloc(wr, x, x_dtype, T, N, d, k, route, n_groups, topk_groups, idx, w, stream=None):
+    """Route T tokens without a context and without allocating (wisp_route_topk_noalloc): the
+    kernels' scratch is the library's fixed device array, shared by every call on the device."""
+    check(lib().wisp_route_topk_noalloc(_ptr(wr), _ptr(x), int(x_dtype), int(T), int(N), int(d), int(k), int(route),
+                                        int(n_groups), int(topk_groups), _ptr(idx), _ptr(w), _stream(stream)),
+          "wisp_route_topk_noalloc")
 
 
 def decode_fp8(codes_dev, out_dev, n, stream=None):
