@@ -52,8 +52,12 @@ HBM_PEAK_GBPS = 8000.0
 PINNED_LIMIT_BYTES = 60e9           # pinned host memory one process may hold on the test machines (65 GiB)
 MFMA_BF16_PEAK_TFLOPS = 2500.0      # dense bf16 matrix-core peak of the MI355X
 PREFILL_WORKLOAD = "qwen3-30b-a3b-prefill"
-TRAFFIC_SUMMARIES = {k: os.path.join(ROOT, "profiles", f"{k}_qwen3-30b-a3b-decode_hbm_traffic.txt")
-                     for k in ("ffn_gateup",)}
+# committed PMC traffic summaries of a kernel class on a workload (their source hash must still match)
+TRAFFIC_SUMMARIES = {
+    ("qwen3-30b-a3b-decode", "ffn_gateup"): os.path.join(ROOT, "profiles", "ffn_gateup_qwen3-30b-a3b-decode_hbm_traffic.txt"),
+    ("deepseek-v3-16l-decode", "ffn_gateup"): os.path.join(ROOT, "profiles",
+                                                           "ffn_gateup_fp8_deepseek-v3-16l-decode_profile.txt"),
+}
 FFN_SOURCE = os.path.join(ROOT, "paper_2606_21868_amd", "csrc", "expert_ffn.hip")
 
 
@@ -85,8 +89,8 @@ def measured_traffic(workload, kname):
     (scaled by the copy-kernel calibration it records), or None when there is none for this workload and
     kernel or the kernel source has changed since the counters were taken."""
     import hashlib
-    summary = TRAFFIC_SUMMARIES.get(kname)
-    if workload != "qwen3-30b-a3b-decode" or summary is None or not os.path.exists(summary):
+    summary = TRAFFIC_SUMMARIES.get((workload, kname))
+    if summary is None or not os.path.exists(summary):
         return None
     fields = {}
     for line in open(summary):
@@ -461,11 +465,13 @@ def pageable_leg(wisp, torch, name, warmup, steps, cpu=True):
         gate = None
         if g["launches"]:
             gbps = g["bytes"] / (g["total_ms"] * 1e-3) / 1e9
+            tr = measured_traffic(wl.name, "ffn_gateup")
             gate = dict(bound="hbm", kernel="ffn_rows expert gate/up (W1+W3 rows" +
                         (", fp8 E4M3 x bf16 block scales" if wl.w_dtype == wisp.FP8 else ", bf16") + "), timed region",
                         achieved=gbps, peak=HBM_PEAK_GBPS, unit="GB/s", frac=gbps / HBM_PEAK_GBPS,
                         launches=g["launches"], avg_launch_us=g["total_ms"] * 1e3 / g["launches"],
-                        bytes_per_launch=g["bytes"] / g["launches"])
+                        bytes_per_launch=g["bytes"] / g["launches"], traffic=tr["bytes_per_launch"] if tr else None,
+                        traffic_detail=tr)
         res = dict(workload=wl.description, tokens_per_s=n_tok / el, ms_per_step=el / steps * 1e3, steps=steps,
                    warmup=warmup, cap_per_layer=wl.cap, generate_s=gen_s, masters="pageable (staged through a "
                    "pinned bounce ring)",
@@ -771,7 +777,8 @@ def main():
             tr = measured_traffic(wl.name, "ffn_gateup")
             roof = dict(bound="hbm", achieved=g["GBps"], peak=HBM_PEAK_GBPS, unit="GB/s", frac=g["GBps"] / HBM_PEAK_GBPS,
                         traffic=tr["bytes_per_launch"] if tr else None,
-                        traffic_detail=tr, kernel="ffn_rows<bf16,bf16,gate/up> expert GEMV (W1+W3 rows), host-pager pass",
+                        traffic_detail=tr, kernel=f"expert gate/up GEMV (W1+W3 rows, {DTYPE_NAMES[wl.w_dtype]} weights), "
+                                                  f"host-pager pass",
                         avg_launch_us=g["avg_us"], bytes_per_launch=g["bytes_per_launch"], launches=g["launches"])
             # what a plain streaming read of the same bytes per launch takes on this GPU: the floor of
             # any kernel that must read them in one launch of this size
