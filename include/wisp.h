@@ -284,8 +284,9 @@ wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n,
  * ordered (score desc, expert id asc), route / n_groups / topk_groups as in wisp_model_desc.  It runs
  * the same kernels as wisp_route_topk with fusion on (one launch for T <= 4, logits then selection
  * above), so ids and gates are bit-identical to it; nothing is published to the host.
- * Allocates nothing: its scratch (the logits and an arrival counter) is a fixed device array of
- * 256 + 8192 + 4 * WISP_NOALLOC_MAX_LOGITS bytes that each device the library runs on holds until the process
+ * Allocates nothing: its scratch (the logits, kept for token batches as up to eight partial sums over
+ * column slices, and an arrival counter) is a fixed device array of
+ * 256 + 8192 + 32 * WISP_NOALLOC_MAX_LOGITS bytes that each device the library runs on holds until the process
  * ends; its address is looked up on the first call on a device (which also clears the counter and the
  * tag words with a kernel on `stream`).  Every call on a device shares that array: calls that overlap on one device
  * (other streams, other threads) race and must be serialised by the caller.  WISP_E_INVAL when

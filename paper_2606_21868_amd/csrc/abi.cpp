@@ -117,6 +117,7 @@ struct wisp_ctx {
   int32_t* ids_up = nullptr;         // pinned staging of the ids for the upload
   int32_t* d_ids = nullptr;          // [max_tokens * k]
   int32_t* d_perm = nullptr;         // [max_tokens * k]
+  int32_t* d_perm_counts = nullptr;  // [segments of the pairs][N] scratch of the permutation
   hipEvent_t ids_ev = nullptr;       // the last upload has been read
   bool ids_ev_recorded = false;
   // the permutation of a token batch, computed from the device ids right after routing (while the
@@ -323,6 +324,7 @@ void free_ctx(wisp_ctx* c) {
   if (c->ids_up) hipHostFree(c->ids_up);
   if (c->d_ids) hipFree(c->d_ids);
   if (c->d_perm) hipFree(c->d_perm);
+  if (c->d_perm_counts) hipFree(c->d_perm_counts);
   if (c->ids_ev) hipEventDestroy(c->ids_ev);
   if (c->perm_ev) hipEventDestroy(c->perm_ev);
   if (c->perm_use_ev) hipEventDestroy(c->perm_use_ev);
@@ -694,7 +696,8 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess)
     return bail(WISP_E_HIP, "hipStreamCreateWithFlags failed");
   void* p = nullptr;
-  if (hipMalloc(&p, sizeof(float) * static_cast<size_t>(T) * N) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
+  if (hipMalloc(&p, sizeof(float) * kRouterMaxSplit * static_cast<size_t>(T) * N) != hipSuccess)
+    return bail(WISP_E_NOMEM, "scratch");
   c->logits = static_cast<float*>(p);
   const size_t rows = static_cast<size_t>(T) * (k + 1);
   if (hipMalloc(&c->h, rows * desc->d_ff * c->h_elem()) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
@@ -712,6 +715,9 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   c->d_ids = static_cast<int32_t*>(p);
   if (hipMalloc(&p, pairs_bytes) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
   c->d_perm = static_cast<int32_t*>(p);
+  if (hipMalloc(&p, sizeof(int32_t) * static_cast<size_t>(permute_segments(T * k)) * N) != hipSuccess)
+    return bail(WISP_E_NOMEM, "scratch");
+  c->d_perm_counts = static_cast<int32_t*>(p);
   if (hipEventCreateWithFlags(&c->ids_ev, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c->perm_ev, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c->perm_use_ev, hipEventDisableTiming) != hipSuccess)
@@ -978,13 +984,14 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
                static_cast<uint64_t>(d.n_experts) * d.d_model * 4 + static_cast<uint64_t>(T) * d.d_model * ctx->x_elem());
   } else {
     LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_LOGITS);
-    WISP_HIP(launch_router_logits(L.wr, x_dev, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, st, t1),
+    int n_split = 1;
+    WISP_HIP(launch_router_logits(L.wr, x_dev, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, &n_split, st, t1),
              "router logits launch");
     timing_end(ctx, t1, WISP_K_ROUTER_LOGITS,
                static_cast<uint64_t>(d.n_experts) * d.d_model * 4 +
                    static_cast<uint64_t>(T) * d.d_model * ctx->x_elem() + static_cast<uint64_t>(T) * d.n_experts * 4);
     LaunchTiming t2 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
-    WISP_HIP(launch_router_select(ctx->logits, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev,
+    WISP_HIP(launch_router_select(ctx->logits, n_split, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev,
                                   w_dev, publish ? ctx->idx_tagged : nullptr, seq, st, t2),
              "router select launch");
     timing_end(ctx, t2, WISP_K_ROUTER_SELECT,
@@ -999,7 +1006,7 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
       ctx->perm_layer = -1;
       if (ctx->perm_use_recorded) WISP_HIP(hipStreamWaitEvent(st, ctx->perm_use_ev, 0), "hipStreamWaitEvent(perm use)");
       LaunchTiming tp = timing_begin(ctx, WISP_K_PERMUTE);
-      WISP_HIP(launch_permute_pairs(idx_dev, n, d.n_experts, ctx->d_perm, st, tp), "permute launch");
+      WISP_HIP(launch_permute_pairs(idx_dev, n, d.n_experts, ctx->d_perm, ctx->d_perm_counts, st, tp), "permute launch");
       timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(n) * 8);
       WISP_HIP(hipEventRecord(ctx->perm_ev, st), "hipEventRecord(perm)");
       ctx->perm_ev_recorded = true;
@@ -1146,7 +1153,7 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
       WISP_HIP(hipEventRecord(ctx->ids_ev, sm), "hipEventRecord(ids)");
       ctx->ids_ev_recorded = true;
       LaunchTiming tp = timing_begin(ctx, WISP_K_PERMUTE);
-      WISP_HIP(launch_permute_pairs(ctx->d_ids, n_pairs, N, ctx->d_perm, sm, tp), "permute launch");
+      WISP_HIP(launch_permute_pairs(ctx->d_ids, n_pairs, N, ctx->d_perm, ctx->d_perm_counts, sm, tp), "permute launch");
       timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(n_pairs) * 8);
     }
   }
@@ -1319,7 +1326,8 @@ wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_
         timing_end(ctx, t1, WISP_K_ROUTER_SELECT, static_cast<uint64_t>(d.n_experts) * d.d_model * 4);
       } else {
         LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_LOGITS);
-        WISP_HIP(launch_router_logits(L.wr, xl, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, sm, t1),
+        int n_split = 1;   // decode sizes: one slice (the device pager's selection reads plain logits)
+        WISP_HIP(launch_router_logits(L.wr, xl, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, &n_split, sm, t1),
                  "router logits launch");
         timing_end(ctx, t1, WISP_K_ROUTER_LOGITS, static_cast<uint64_t>(d.n_experts) * d.d_model * 4);
         LaunchTiming t2 = timing_begin(ctx, WISP_K_ROUTER_SELECT);

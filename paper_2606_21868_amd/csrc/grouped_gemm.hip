@@ -72,87 +72,93 @@ __device__ __forceinline__ void tile_of(const GroupedBatch& gb, int n_ctiles, in
   mt = local - ct * n_mt;
 }
 
-// Stable counting sort of the pairs p = t*k + j by expert id idx[p] (one workgroup of 16 waves).
-// Wave w owns a contiguous segment of pairs.  Pass 1 counts each expert per wave (lanes with equal
-// ids find each other through eight ballots over the id bits); the counts are scanned over waves
-// and then over experts; pass 2 repeats the walk and writes every pair to
-// off[e] + (earlier pairs of e in earlier waves) + (earlier pairs of e in this wave).
-__global__ void __launch_bounds__(1024) permute_pairs_kernel(const int32_t* __restrict__ idx, int P, int N,
-                                                             int32_t* __restrict__ perm) {
-  constexpr int kBatch = 8;            // chunks of 64 pairs whose ids a wave loads before using any
-  __shared__ int32_t cnt[16][256];
-  __shared__ int32_t base[257];
-  __shared__ int32_t wsum[4];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  for (int i = tid; i < 16 * 256; i += 1024) (&cnt[0][0])[i] = 0;
+// Stable counting sort of the pairs p = t*k + j by expert id idx[p], in two launches over segments of
+// kPermSeg pairs: permute_count_kernel counts each expert in each segment; permute_scatter_kernel (a
+// workgroup of 16 waves per segment, 64 pairs per wave) places every pair at
+//   (pairs of smaller experts) + (pairs of its expert in earlier segments)
+//   + (pairs of its expert in earlier waves of its segment) + (earlier lanes of its wave with that expert),
+// the last found by matching lanes with equal ids through eight ballots over the id bits.  The result
+// is the unique stable order: the pairs of each expert in ascending pair order.
+constexpr int kPermSeg = 1024;
+
+__global__ void __launch_bounds__(256) permute_count_kernel(const int32_t* __restrict__ idx, int P, int N,
+                                                            int32_t* __restrict__ counts) {
+  __shared__ int32_t h[256];
+  const int tid = threadIdx.x, seg = blockIdx.x;
+  h[tid] = 0;
   __syncthreads();
-  const int seg = (P + 15) / 16;
-  const int p0 = wave * seg, p1 = min(P, p0 + seg);
-  const uint64_t below = (1ull << lane) - 1ull;
-  for (int pass = 0; pass < 2; ++pass) {
-    for (int cb = p0; cb < p1; cb += 64 * kBatch) {
-      int ev[kBatch];
+  const int p0 = seg * kPermSeg;
+  int ev[kPermSeg / 256];
 #pragma unroll
-      for (int q = 0; q < kBatch; ++q) {   // the loads of kBatch chunks go out together
-        const int p = cb + q * 64 + lane;
-        ev[q] = p < p1 ? idx[p] : 0;
-      }
+  for (int i = 0; i < kPermSeg / 256; ++i) {   // the loads go out together
+    const int p = p0 + i * 256 + tid;
+    ev[i] = p < P ? idx[p] : -1;
+  }
 #pragma unroll
-      for (int q = 0; q < kBatch; ++q) {
-        const int c0 = cb + q * 64;
-        if (c0 >= p1) break;               // uniform across the wave
-        const int p = c0 + lane;
-        const bool valid = p < p1;
-        const int e = ev[q];
-        uint64_t same = __ballot(valid);
-#pragma unroll
-        for (int bi = 0; bi < 8; ++bi) {
-          const bool bit = (e >> bi) & 1;
-          const uint64_t m = __ballot(bit);
-          same &= bit ? m : ~m;
-        }
-        if (valid) {
-          const int before = cnt[wave][e];
-          if (pass == 1) perm[base[e] + before + __popcll(same & below)] = p;
-          if ((same & below) == 0) cnt[wave][e] = before + __popcll(same);
-        }
-      }
-    }
-    __syncthreads();
-    if (pass == 0) {
-      // per expert: the waves' counts to exclusive offsets inside the expert, and its total
-      if (tid < N) {
-        int run = 0;
-        for (int w = 0; w < 16; ++w) {
-          const int c = cnt[w][tid];
-          cnt[w][tid] = run;
-          run += c;
-        }
-        base[tid] = run;
-      }
-      __syncthreads();
-      // experts' totals to exclusive offsets: an inclusive scan per wave (threads 0..255), then the
-      // totals of the waves before; base[N] is the number of pairs
-      int v = 0, x = 0;
-      if (tid < 256) {
-        v = tid < N ? base[tid] : 0;
-        x = v;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-          const int y = __shfl_up(x, off, 64);
-          if (lane >= off) x += y;
-        }
-        if (lane == 63) wsum[wave] = x;
-      }
-      __syncthreads();
-      if (tid < 256) {
-        for (int w = 0; w < wave; ++w) x += wsum[w];
-        if (tid < N) base[tid] = x - v;
-        if (tid == 255) base[N] = x;
-      }
-      __syncthreads();
+  for (int i = 0; i < kPermSeg / 256; ++i)
+    if (ev[i] >= 0) atomicAdd(&h[ev[i]], 1);
+  __syncthreads();
+  if (tid < N) counts[seg * N + tid] = h[tid];
+}
+
+__global__ void __launch_bounds__(1024) permute_scatter_kernel(const int32_t* __restrict__ idx, int P, int N,
+                                                               const int32_t* __restrict__ counts, int n_seg,
+                                                               int32_t* __restrict__ perm) {
+  __shared__ int32_t cnt[16][256];
+  __shared__ int32_t base[256];
+  __shared__ int32_t wsum[4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, seg = blockIdx.x;
+  const int p = seg * kPermSeg + wave * 64 + lane;
+  const bool valid = p < P;
+  const int e = valid ? idx[p] : 0;
+  for (int i = tid; i < 16 * 256; i += 1024) (&cnt[0][0])[i] = 0;
+  // per expert: all its pairs (for the offsets) and those in earlier segments
+  int tot = 0, before = 0;
+  if (tid < N) {
+    for (int q = 0; q < n_seg; ++q) {
+      const int c = counts[q * N + tid];
+      tot += c;
+      before += q < seg ? c : 0;
     }
   }
+  // exclusive scan of the totals over experts: an inclusive scan per wave (threads 0..255), then the
+  // totals of the waves before
+  int x = tot;
+  if (tid < 256) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(x, off, 64);
+      if (lane >= off) x += y;
+    }
+    if (lane == 63) wsum[wave] = x;
+  }
+  __syncthreads();
+  if (tid < 256) {
+    for (int w = 0; w < wave; ++w) x += wsum[w];
+    base[tid] = x - tot + before;
+  }
+  // lanes of this wave with the same expert, and the rank among them
+  uint64_t same = __ballot(valid);
+#pragma unroll
+  for (int bi = 0; bi < 8; ++bi) {
+    const bool bit = (e >> bi) & 1;
+    const uint64_t m = __ballot(bit);
+    same &= bit ? m : ~m;
+  }
+  const uint64_t below = (1ull << lane) - 1ull;
+  if (valid && (same & below) == 0) cnt[wave][e] = __popcll(same);
+  __syncthreads();
+  // per expert: the counts of the waves to exclusive offsets inside the segment
+  if (tid < N) {
+    int run = 0;
+    for (int w = 0; w < 16; ++w) {
+      const int c = cnt[w][tid];
+      cnt[w][tid] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+  if (valid) perm[base[e] + cnt[wave][e] + __popcll(same & below)] = p;
 }
 
 // One K stage of a 64-row A tile and a 128-row B tile through LDS.  A thread loads 16-byte pieces
@@ -377,12 +383,19 @@ bool offsets_fit(const FfnShape& s, int n_tok, int k) {
 }
 }  // namespace
 
-hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t* perm, hipStream_t st,
+int permute_segments(int n_pairs) { return (n_pairs + kPermSeg - 1) / kPermSeg; }
+
+hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t* perm, int32_t* counts, hipStream_t st,
                                 const LaunchTiming& tm) {
   if (n_pairs <= 0) return hipSuccess;
   if (N < 1 || N > 256) return hipErrorInvalidValue;
-  hipExtLaunchKernelGGL(permute_pairs_kernel, dim3(1), dim3(1024), 0, st, tm.start, tm.stop, 0, idx, n_pairs, N,
-                        perm);
+  const int n_seg = permute_segments(n_pairs);
+  hipExtLaunchKernelGGL(permute_count_kernel, dim3(n_seg), dim3(256), 0, st, tm.start, nullptr, 0, idx, n_pairs, N,
+                        counts);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipExtLaunchKernelGGL(permute_scatter_kernel, dim3(n_seg), dim3(1024), 0, st, nullptr, tm.stop, 0, idx, n_pairs, N,
+                        counts, n_seg, perm);
   return hipGetLastError();
 }
 

@@ -107,7 +107,9 @@ struct GroupedBatch {
 bool grouped_supported(const FfnShape& s, int has_shared);
 int grouped_row_tiles(int rows);
 // perm[off_e + i] = the i-th pair (ascending) routed to expert e; off_e = pairs of experts < e.
-hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t* perm, hipStream_t st,
+// counts: device scratch of permute_segments(n_pairs) * N int32.
+int permute_segments(int n_pairs);
+hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t* perm, int32_t* counts, hipStream_t st,
                                 const LaunchTiming& tm);
 // hs[row] = bf16(silu(W1 x[t]) * (W3 x[t])) for every row of the batch's experts (row in sorted order);
 // x holds n_tok token rows, hs n_tok * k pair rows.
@@ -117,9 +119,12 @@ hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const
 hipError_t launch_grouped_down(const GroupedBatch& b, const FfnShape& s, const void* hs, int n_tok, const int32_t* perm,
                                int k, float* buf, hipStream_t st, const LaunchTiming& tm);
 
-// Router: logits[t, e] = W_r[e] . x[t] (fp32 accumulate).
+// Router: logits[t, e] = W_r[e] . x[t] (fp32 accumulate), written as *n_split partial sums over column
+// slices (slice s at logits + s * T * N; 1 for decode sizes, at most kRouterMaxSplit), which the
+// selection adds in slice order.  logits must hold kRouterMaxSplit * T * N floats.
+constexpr int kRouterMaxSplit = 8;
 hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int T, int N, int d, float* logits,
-                                hipStream_t st, const LaunchTiming& tm);
+                                int* n_split, hipStream_t st, const LaunchTiming& tm);
 // Router selection: idx/w [T, k] by routing variant.  If idx_host is given, entry t*k+j of it (in
 // host-coherent memory) also receives (seq << 32 | id) as one 64-bit store.
 // Decode (T <= 4): router logits and selection in one launch (the workgroup completing the logits
@@ -131,9 +136,9 @@ hipError_t launch_route_select(const float* wr, const void* x, int x_dtype, int 
                                uint32_t* arrive, int T, int N, int k, int route, int n_groups, int topk_groups,
                                int32_t* idx, float* w, uint64_t* idx_host, uint32_t seq, hipStream_t st,
                                const LaunchTiming& tm);
-hipError_t launch_router_select(const float* logits, int T, int N, int k, int route, int n_groups, int topk_groups,
-                                int32_t* idx, float* w, uint64_t* idx_host, uint32_t seq, hipStream_t st,
-                                const LaunchTiming& tm);
+hipError_t launch_router_select(const float* logits, int n_split, int T, int N, int k, int route, int n_groups,
+                                int topk_groups, int32_t* idx, float* w, uint64_t* idx_host, uint32_t seq,
+                                hipStream_t st, const LaunchTiming& tm);
 
 // Device pager: selection of T <= 4 tokens + Algorithm 1 on the layer's slot table in HBM + the
 // launch plan of the layer's FFN (one workgroup).  Requires T * k <= C.

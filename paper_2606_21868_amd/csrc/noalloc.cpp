@@ -1,7 +1,8 @@
 // wisp_route_topk_noalloc: router scoring and top-k without a context and without allocating.
 //
 // The router kernels need device scratch beyond their inputs and outputs: the logits [T, N] fp32
-// and, for the one-launch path of up to four tokens, the tagged logit words and the arrival counter
+// (up to kRouterMaxSplit partial sums of them for token batches) and, for the one-launch path of up
+// to four tokens, the tagged logit words and the arrival counter
 // of the workgroups that publish logit rows.  Here that scratch is the file-scope array `scratch`
 // below, of a fixed size, held by every device the library runs on until the process ends.  Host code never passes the
 // array's name to a kernel (in host code it names a host-side stand-in); it passes the device
@@ -20,7 +21,8 @@ namespace {
 
 constexpr size_t kCounterBytes = 256;                       // arrival counter, own 256-byte line
 constexpr size_t kTagBytes = 4 * 256 * 8;                   // tagged logit words of the one-launch path
-constexpr size_t kLogitBytes = WISP_NOALLOC_MAX_LOGITS * 4;  // logits [T, N] fp32 of the two-launch path
+// logits [T, N] fp32 of the two-launch path, as up to kRouterMaxSplit partial sums
+constexpr size_t kLogitBytes = static_cast<size_t>(wisp::kRouterMaxSplit) * WISP_NOALLOC_MAX_LOGITS * 4;
 constexpr size_t kScratchBytes = kCounterBytes + kTagBytes + kLogitBytes;
 constexpr int kMaxDevices = 64;
 
@@ -103,9 +105,10 @@ extern "C" wisp_status wisp_route_topk_noalloc(const float* w_r_dev, const void*
     e = wisp::launch_route_select(w_r_dev, x_dev, x_dtype, d, tagged, tag, arrive, T, N, k, route, n_groups,
                                   topk_groups, idx_dev, w_dev, nullptr, 0, st, wisp::LaunchTiming{});
   } else {
-    e = wisp::launch_router_logits(w_r_dev, x_dev, x_dtype, T, N, d, logits, st, wisp::LaunchTiming{});
+    int n_split = 1;
+    e = wisp::launch_router_logits(w_r_dev, x_dev, x_dtype, T, N, d, logits, &n_split, st, wisp::LaunchTiming{});
     if (e == hipSuccess)
-      e = wisp::launch_router_select(logits, T, N, k, route, n_groups, topk_groups, idx_dev, w_dev, nullptr, 0, st,
+      e = wisp::launch_router_select(logits, n_split, T, N, k, route, n_groups, topk_groups, idx_dev, w_dev, nullptr, 0, st,
                                      wisp::LaunchTiming{});
   }
   if (e != hipSuccess) return set_error(WISP_E_HIP, std::string("router launch: ") + hipGetErrorString(e));

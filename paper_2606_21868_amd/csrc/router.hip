@@ -2,8 +2,9 @@
 //
 // router_logits: z[t, e] = W_r[e] . x[t] in fp32.  Decode sizes (T <= 8): one workgroup per
 //   expert row, so the fp32 router matrix is read by N workgroups at once (one HBM round trip);
-//   token batches: fp32 matrix cores (a 16-token x 16-row block per workgroup) when N is a
-//   multiple of 16 and d of 64, else a workgroup per 16 tokens with LDS-staged slices of W_r.
+//   token batches: fp32 matrix cores (64 tokens against all router rows over a slice of the columns
+//   per workgroup, slices summed by the selection) when N is a multiple of 16, else a workgroup per
+//   16 tokens with LDS-staged slices of W_r.
 // router_select: top-k selection and gates (select.hpp), optionally publishing the ids to the
 //   host pager through host-coherent memory.
 #include <hip/hip_ext.h>
@@ -87,59 +88,105 @@ __global__ void __launch_bounds__(256) router_logits_tiled_kernel(const float* _
   }
 }
 
-// Token-batch logits on the fp32 matrix cores (v_mfma_f32_16x16x4_f32).  A workgroup computes a
-// 16-token x 16-row block; its four waves take one quarter of the columns each and their partial
-// sums are added in wave order through LDS.  W_r stays fp32 and x is widened exactly, so the
-// products are those of the FMA kernels and only the summation order differs.  Lane l owns token
-// l%16 and router row l%16; for each 16-column step it reads columns 4(l/16) .. +3 of both (one 8-
-// or 16-byte load each, issued a step ahead) for four MFMA steps, which keeps the column index of a
-// lane's A and B operands equal, as the product requires.  Output lane l: tokens 4(l/16) .. +3, row l%16.
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
-template <int XT>
-__global__ void __launch_bounds__(256) router_logits_mfma_kernel(const float* __restrict__ wr,
-                                                                 const void* __restrict__ x, int T, int N, int d,
-                                                                 float* __restrict__ logits) {
-  __shared__ f32x4_t part[3][64];
+
+// Token-batch logits with the router matrix read once per 64 tokens: a workgroup computes 64 tokens
+// against all N router rows over one of n_split slices of the columns (grid: token blocks x slices),
+// on the fp32 matrix cores (v_mfma_f32_16x16x4_f32).  Wave w takes the 16-row blocks b = w, w + 4,
+// ... of W_r and all four 16-token blocks; per 16-column step lane l (r = l % 16, g = l / 16) holds
+// columns 4g .. 4g + 3 of token r of each token block and of row r of each row block, one step ahead
+// of the matrix-core work.  The slice's sums go to partial[slice][token][row]; the selection adds the
+// slices in order.  (W_r is re-read T / 64 times instead of T / 16 times by 16 x 16 blocks.)
+template <int XT, int RB>
+__global__ void __launch_bounds__(256) router_logits_split_kernel(const float* __restrict__ wr,
+                                                                  const void* __restrict__ x, int T, int N, int d,
+                                                                  int ks, float* __restrict__ partial) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int t0 = blockIdx.x * 16, e0 = blockIdx.y * 16;
   const int r = lane & 15, g = lane >> 4;
-  const bool tok_ok = t0 + r < T;
-  const int kq = d / 4;                         // columns per wave (d % 64 == 0)
-  const int kbeg = wave * kq;
-  const float* wrow = wr + static_cast<size_t>(e0 + r) * d + kbeg + 4 * g;
-  const size_t xoff = static_cast<size_t>(tok_ok ? t0 + r : 0) * d + kbeg + 4 * g;
-  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-  float4 w = *reinterpret_cast<const float4*>(wrow);
-  float4 v = tok_ok ? load_x4<XT>(x, xoff) : make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int k0 = 0; k0 < kq; k0 += 16) {
-    float4 wn = w, vn = v;
-    if (k0 + 16 < kq) {
-      wn = *reinterpret_cast<const float4*>(wrow + k0 + 16);
-      if (tok_ok) vn = load_x4<XT>(x, xoff + k0 + 16);
-    }
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(v.x, w.x, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(v.y, w.y, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(v.z, w.z, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(v.w, w.w, acc, 0, 0, 0);
-    w = wn;
-    v = vn;
+  const int t0 = blockIdx.x * 64, q = blockIdx.y, kbeg = q * ks;
+  const int nb = N / 16;
+  const float* wrow[RB];
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    const int blk = min(wave + 4 * b, nb - 1);   // a block past N repeats the last (never stored)
+    wrow[b] = wr + static_cast<size_t>(16 * blk + r) * d + kbeg + 4 * g;
   }
-  if (wave > 0) part[wave - 1][lane] = acc;
-  __syncthreads();
-  if (wave == 0) {
+  size_t xoff[4];
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
-      const f32x4_t p = part[q][lane];
-      acc[0] += p[0];
-      acc[1] += p[1];
-      acc[2] += p[2];
-      acc[3] += p[3];
-    }
+  for (int tb = 0; tb < 4; ++tb) {
+    const int t = t0 + 16 * tb + r;
+    xoff[tb] = static_cast<size_t>(t < T ? t : 0) * d + kbeg + 4 * g;
+  }
+  f32x4_t acc[4][RB];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int t = t0 + 4 * g + q;
-      if (t < T) logits[static_cast<size_t>(t) * N + e0 + r] = acc[q];
+  for (int tb = 0; tb < 4; ++tb)
+#pragma unroll
+    for (int b = 0; b < RB; ++b) acc[tb][b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // operands of PF 16-column steps in flight (one wave per SIMD: the loads of a step are issued PF
+  // steps before its matrix-core work); step j lives in ring slot j % PF.  The loads are unconditional
+  // (a token past T reads token 0's row, never stored) and the inputs stay raw until used, so no load
+  // waits for another.
+  constexpr int PF = 4;
+  constexpr int XW = XT == DT_F32 ? 4 : 2;   // 32-bit words of four inputs
+  float4 w[PF][RB];
+  uint32_t v[PF][4][XW];
+  auto load = [&](int slot, int k0) {
+#pragma unroll
+    for (int b = 0; b < RB; ++b) w[slot][b] = *reinterpret_cast<const float4*>(wrow[b] + k0);
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+      if constexpr (XT == DT_F32) {
+        const uint4 q4 = *reinterpret_cast<const uint4*>(static_cast<const float*>(x) + xoff[tb] + k0);
+        v[slot][tb][0] = q4.x; v[slot][tb][1] = q4.y; v[slot][tb][2] = q4.z; v[slot][tb][3] = q4.w;
+      } else {
+        const uint2 q2 = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(x) + xoff[tb] + k0);
+        v[slot][tb][0] = q2.x; v[slot][tb][1] = q2.y;
+      }
     }
+  };
+  // input c (0..3) of token block tb in slot `slot`, widened exactly to fp32
+  auto xin = [&](int slot, int tb, int c) -> float {
+    if constexpr (XT == DT_F32) return __uint_as_float(v[slot][tb][c]);
+    const uint32_t q = v[slot][tb][c >> 1];
+    return __uint_as_float((c & 1) ? (q & 0xFFFF0000u) : (q << 16));
+  };
+  // one column of the quad at a time over all 4 x RB accumulators, so that consecutive matrix-core
+  // instructions never wait on each other's result (each accumulator still takes its columns in order)
+  auto mma = [&](int slot) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb)
+#pragma unroll
+        for (int b = 0; b < RB; ++b) {
+          const float wc = c == 0 ? w[slot][b].x : c == 1 ? w[slot][b].y : c == 2 ? w[slot][b].z : w[slot][b].w;
+          acc[tb][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(xin(slot, tb, c), wc, acc[tb][b], 0, 0, 0);
+        }
+  };
+  const int steps = ks / 16;   // a multiple of PF or below it (ks = d / n_split, d % 16 == 0)
+#pragma unroll
+  for (int j = 0; j < PF; ++j)
+    if (j < steps) load(j, 16 * j);
+  for (int j0 = 0; j0 < steps; j0 += PF) {
+#pragma unroll
+    for (int j = 0; j < PF; ++j) {
+      if (j0 + j >= steps) break;
+      mma(j);
+      if (j0 + j + PF < steps) load(j, 16 * (j0 + j + PF));
+    }
+  }
+  float* out = partial + static_cast<size_t>(q) * T * N;
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    const int blk = wave + 4 * b;
+    if (blk >= nb) break;
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = t0 + 16 * tb + 4 * g + i;
+        if (t < T) out[static_cast<size_t>(t) * N + 16 * blk + r] = acc[tb][b][i];
+      }
   }
 }
 
@@ -147,12 +194,13 @@ __global__ void __launch_bounds__(256) router_logits_mfma_kernel(const float* __
 // token blockIdx.x * 4 + w.  The indices can also be published to host-coherent memory as 64-bit
 // (seq << 32 | id) words: the host knows an entry is current from its tag alone, so it needs no
 // copy, event or fence to read them.
-__global__ void __launch_bounds__(256) router_select_kernel(const float* __restrict__ logits, int T, int N, int k,
-                                                            int route, int n_groups, int topk_groups,
+__global__ void __launch_bounds__(256) router_select_kernel(const float* __restrict__ logits, int n_split, int T,
+                                                            int N, int k, int route, int n_groups, int topk_groups,
                                                             int32_t* __restrict__ idx, float* __restrict__ w,
                                                             uint64_t* __restrict__ idx_host, uint32_t seq) {
   __shared__ SelectShared sh;
-  select_tokens(logits, 0, blockIdx.x * 4, T, N, k, route, n_groups, topk_groups, sh);
+  select_tokens(logits, 0, blockIdx.x * 4, T, N, k, route, n_groups, topk_groups, sh, n_split,
+                static_cast<size_t>(T) * N);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + wave;
   if (t < T && lane < k) {
@@ -226,7 +274,8 @@ hipError_t launch_route_select(const float* wr, const void* x, int x_dtype, int 
 }
 
 hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int T, int N, int d, float* logits,
-                                hipStream_t st, const LaunchTiming& tm) {
+                                int* n_split, hipStream_t st, const LaunchTiming& tm) {
+  *n_split = 1;
   if (T <= 0) return hipSuccess;
   if (d % 4 != 0) return hipErrorInvalidValue;
   if (T <= 8) {
@@ -239,14 +288,26 @@ hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int
                             d, logits);
     return hipGetLastError();
   }
-  if (N % 16 == 0 && d % 64 == 0) {
-    dim3 grid((T + 15) / 16, N / 16), block(256);
+  if (N % 16 == 0 && N <= 256 && d % 16 == 0) {
+    // enough (token block, column slice) workgroups to cover the chip, at most kRouterMaxSplit slices
+    const int tiles = (T + 63) / 64;
+    int S = 1;
+    while (2 * S <= kRouterMaxSplit && tiles * S < 256 && d % (32 * S) == 0 &&
+           ((d / (2 * S)) / 16 % 4 == 0 || (d / (2 * S)) / 16 < 4))
+      S *= 2;
+    *n_split = S;
+    dim3 grid(tiles, S), block(256);
+    const int ks = d / S;
+    using K = void (*)(const float*, const void*, int, int, int, int, float*);
+    K kern = nullptr;
+    const int rb = (N / 16 + 3) / 4;
     if (x_dtype == DT_F32)
-      hipExtLaunchKernelGGL(router_logits_mfma_kernel<DT_F32>, grid, block, 0, st, tm.start, tm.stop, 0, wr, x, T, N,
-                            d, logits);
+      kern = rb == 1 ? &router_logits_split_kernel<DT_F32, 1> : rb == 2 ? &router_logits_split_kernel<DT_F32, 2>
+           : rb == 3 ? &router_logits_split_kernel<DT_F32, 3> : &router_logits_split_kernel<DT_F32, 4>;
     else
-      hipExtLaunchKernelGGL(router_logits_mfma_kernel<DT_BF16>, grid, block, 0, st, tm.start, tm.stop, 0, wr, x, T,
-                            N, d, logits);
+      kern = rb == 1 ? &router_logits_split_kernel<DT_BF16, 1> : rb == 2 ? &router_logits_split_kernel<DT_BF16, 2>
+           : rb == 3 ? &router_logits_split_kernel<DT_BF16, 3> : &router_logits_split_kernel<DT_BF16, 4>;
+    hipExtLaunchKernelGGL(kern, grid, block, 0, st, tm.start, tm.stop, 0, wr, x, T, N, d, ks, logits);
     return hipGetLastError();
   }
   if (d % 32 == 0 && N <= 256) {
@@ -272,15 +333,16 @@ hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_router_select(const float* logits, int T, int N, int k, int route, int n_groups, int topk_groups,
-                                int32_t* idx, float* w, uint64_t* idx_host, uint32_t seq, hipStream_t st,
-                                const LaunchTiming& tm) {
+hipError_t launch_router_select(const float* logits, int n_split, int T, int N, int k, int route, int n_groups,
+                                int topk_groups, int32_t* idx, float* w, uint64_t* idx_host, uint32_t seq,
+                                hipStream_t st, const LaunchTiming& tm) {
   if (T <= 0) return hipSuccess;
   if (N > 256 || k > 8 || k < 1 || (route == R_SIGMOID_GROUP && (n_groups > 32 || N % n_groups != 0)))
     return hipErrorInvalidValue;
   dim3 grid((T + 3) / 4), block(256);
-  hipExtLaunchKernelGGL(router_select_kernel, grid, block, 0, st, tm.start, tm.stop, 0, logits, T, N, k, route,
-                        n_groups, topk_groups, idx, w, idx_host, seq);
+  if (n_split < 1 || n_split > kRouterMaxSplit) return hipErrorInvalidValue;
+  hipExtLaunchKernelGGL(router_select_kernel, grid, block, 0, st, tm.start, tm.stop, 0, logits, n_split, T, N, k,
+                        route, n_groups, topk_groups, idx, w, idx_host, seq);
   return hipGetLastError();
 }
 

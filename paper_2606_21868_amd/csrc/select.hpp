@@ -19,6 +19,8 @@ namespace wisp {
 
 enum { R_SOFTMAX_RENORM = 0, R_TOPK_SOFTMAX = 1, R_SIGMOID_GROUP = 2 };
 
+constexpr int kSelectMaxSplit = 8;   // partial sums of a logit the selection adds (kRouterMaxSplit)
+
 struct SelectShared {
   uint64_t key[4][256];   // (order-preserving logit << 32 | 255 - id), 0 = not allowed
   float z[4][256];
@@ -61,10 +63,12 @@ __device__ __forceinline__ float read_tagged_logit(const uint64_t* p, uint32_t t
 // 255 - id, so (logit desc, id asc) is plain unsigned order and every allowed key is distinct:
 // the rank of an expert is the number of larger keys.  TAGGED: the logits are 64-bit tagged words
 // published by other workgroups of the running kernel (tag_logit), read until they carry `tag`;
-// otherwise plain fp32 written by an earlier kernel.
+// otherwise plain fp32 written by an earlier kernel, as n_split partial sums (split s at s * split_stride
+// floats), added in split order.
 template <bool TAGGED = false>
 __device__ __forceinline__ void select_tokens(const void* __restrict__ logits, uint32_t tag, int t0, int T, int N,
-                                              int k, int route, int n_groups, int topk_groups, SelectShared& sh) {
+                                              int k, int route, int n_groups, int topk_groups, SelectShared& sh,
+                                              int n_split = 1, size_t split_stride = 0) {
   const int tid = threadIdx.x;
   const int nt = min(4, T - t0);
   const int e = tid;
@@ -73,9 +77,21 @@ __device__ __forceinline__ void select_tokens(const void* __restrict__ logits, u
     if (t >= nt) break;
     const size_t at = static_cast<size_t>(t0 + t) * N + e;
     float z = 0.f;
-    if (e < N)
-      z = TAGGED ? read_tagged_logit(static_cast<const uint64_t*>(logits) + at, tag)
-                 : static_cast<const float*>(logits)[at];
+    if (e < N) {
+      if (TAGGED) {
+        z = read_tagged_logit(static_cast<const uint64_t*>(logits) + at, tag);
+      } else {
+        // the slices' loads go out together, then they are added in slice order
+        const float* f = static_cast<const float*>(logits);
+        float part[kSelectMaxSplit];
+#pragma unroll
+        for (int q = 0; q < kSelectMaxSplit; ++q) part[q] = q < n_split ? f[q * split_stride + at] : 0.f;
+        z = part[0];
+#pragma unroll
+        for (int q = 1; q < kSelectMaxSplit; ++q)
+          if (q < n_split) z += part[q];
+      }
+    }
     sh.z[t][e] = z;
     sh.key[t][e] = e < N ? (static_cast<uint64_t>(order_key(z)) << 32) | static_cast<uint32_t>(255 - e) : 0ull;
   }
