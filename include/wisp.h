@@ -215,10 +215,10 @@ wisp_status wisp_read_slot(wisp_ctx* ctx, int32_t layer, int32_t slot, void* dst
 /* Fused decode kernels (on by default).  (1) A layer-step of one token with bf16 weights whose
  * union fits the cap runs the down projection of all its experts and the gate-weighted combine in
  * one launch (the per-expert outputs stay on chip) instead of a down launch per expert group and a
- * combine launch.  (2) The device pager computes the router logits and, in the workgroup that
- * completes them, the selection and Algorithm 1 in one launch instead of two.  (3) wisp_route_topk
- * (and the host pager's decode step) computes the logits of up to four tokens and, in the workgroup
- * that completes them, their selection in one launch instead of two.  Every logit, row,
+ * combine launch.  (2) The device pager computes the router logits and, in its first workgroup once
+ * every logit row is published, the selection and Algorithm 1 in one launch instead of two.  (3)
+ * wisp_route_topk (and the host pager's decode step) computes the logits of up to four tokens and, in
+ * its first workgroup once every row is published, their selection in one launch instead of two.  Every logit, row,
  * decision and sum is computed by the same operations in the same order either way, so routing,
  * paging and outputs are bit-identical.  on = 0 selects the separate kernels (for comparison).
  * WISP_E_STATE while a page-in is pending. */
@@ -284,14 +284,14 @@ wisp_status wisp_decode_fp8(const uint8_t* codes_dev, float* out_dev, int32_t n,
  * ordered (score desc, expert id asc), route / n_groups / topk_groups as in wisp_model_desc.  It runs
  * the same kernels as wisp_route_topk with fusion on (one launch for T <= 4, logits then selection
  * above), so ids and gates are bit-identical to it; nothing is published to the host.
- * Allocates nothing: its scratch (the logits, kept for token batches as up to eight partial sums over
- * column slices, and an arrival counter) is a fixed device array of
- * 256 + 8192 + 32 * WISP_NOALLOC_MAX_LOGITS bytes that each device the library runs on holds until the process
- * ends; its address is looked up on the first call on a device (which also clears the counter and the
- * tag words with a kernel on `stream`).  Every call on a device shares that array: calls that overlap on one device
+ * Allocates nothing: its scratch (the tagged logit words of the one-launch path, and the logits, kept
+ * for token batches as up to eight partial sums over column slices) is a fixed device array of
+ * 8192 + 32 * WISP_NOALLOC_MAX_LOGITS bytes that each device the library runs on holds until the process
+ * ends; its address is looked up on the first call on a device (which also clears the tag words with a
+ * kernel on `stream`).  Every call on a device shares that array: calls that overlap on one device
  * (other streams, other threads) race and must be serialised by the caller.  WISP_E_INVAL when
  * T * N > WISP_NOALLOC_MAX_LOGITS, for a null pointer or an unsupported shape (more than 8 tokens need
- * d a multiple of 32); validation happens before any GPU call. */
+ * N and d multiples of 16, or d a multiple of 32); validation happens before any GPU call. */
 #define WISP_NOALLOC_MAX_LOGITS 524288
 wisp_status wisp_route_topk_noalloc(const float* w_r_dev, const void* x_dev, int32_t x_dtype, int32_t T, int32_t N,
                                     int32_t d, int32_t k, int32_t route, int32_t n_groups, int32_t topk_groups,

@@ -157,7 +157,6 @@ struct wisp_ctx {
   uint32_t* d_stats = nullptr;       // [L][2] hits, misses of the current step
   uint32_t* h_stats = nullptr;       // pinned copy
   bool fusion = true;                // fused decode kernels (route + page; down + combine)
-  uint32_t* d_arrive = nullptr;      // route + page: logit rows completed in the running launch
   uint64_t* d_logit_tags = nullptr;  // [4][N] tagged logit words of the one-launch router kernels
   uint32_t logit_tag = 0;            // tag of the last such launch (never 0)
   // speculative prefetch inside wisp_decode_step (host pager)
@@ -333,7 +332,6 @@ void free_ctx(wisp_ctx* c) {
                   static_cast<void*>(c->d_stats)})
     if (p) hipFree(p);
   if (c->h_stats) hipHostFree(c->h_stats);
-  if (c->d_arrive) hipFree(c->d_arrive);
   if (c->d_logit_tags) hipFree(c->d_logit_tags);
   delete c;
 }
@@ -725,9 +723,6 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   c->e_cnt.assign(N, 0);
   c->e_off.assign(N + 1, 0);
   c->pf_mark.assign(N, 0);
-  if (hipMalloc(&p, 256) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
-  c->d_arrive = static_cast<uint32_t*>(p);
-  if (hipMemset(c->d_arrive, 0, 256) != hipSuccess) return bail(WISP_E_HIP, "hipMemset(counter)");
   if (hipMalloc(&p, sizeof(uint64_t) * 4 * N) != hipSuccess) return bail(WISP_E_NOMEM, "scratch");
   c->d_logit_tags = static_cast<uint64_t*>(p);
   if (hipMemset(c->d_logit_tags, 0, sizeof(uint64_t) * 4 * N) != hipSuccess)
@@ -973,10 +968,10 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
   const bool publish = idx_host != nullptr;
   const uint32_t seq = publish ? ++ctx->route_seq : 0;
   if (ctx->fusion && T <= 4) {
-    // logits and selection in one launch (the workgroup completing the logits selects)
+    // logits and selection in one launch (the first workgroup selects once every row is published)
     LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
     WISP_HIP(launch_route_select(L.wr, x_dev, d.x_dtype, d.d_model, ctx->d_logit_tags, next_logit_tag(ctx),
-                                 ctx->d_arrive, T, d.n_experts,
+                                 T, d.n_experts,
                                  d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev, w_dev,
                                  publish ? ctx->idx_tagged : nullptr, seq, st, t1),
              "router logits + select launch");
@@ -1318,7 +1313,7 @@ wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_
       if (ctx->fusion) {
         LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
         WISP_HIP(launch_route_page(L.wr, xl, d.x_dtype, d.d_model, ctx->d_logit_tags, next_logit_tag(ctx),
-                                   ctx->d_arrive, T, d.n_experts, d.top_k,
+                                   T, d.n_experts, d.top_k,
                                    d.route, d.n_groups, d.topk_groups, il, wl, pi_l, pinv_l, tau_l, ctx->d_clock + l, C,
                                    slot_l, ctx->masters[l], ctx->master_stride, L.shared_dev, d.has_shared,
                                    ctx->d_plan, ctx->d_stats + 2 * l, sm, t1),

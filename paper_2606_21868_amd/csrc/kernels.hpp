@@ -127,13 +127,13 @@ hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int
                                 int* n_split, hipStream_t st, const LaunchTiming& tm);
 // Router selection: idx/w [T, k] by routing variant.  If idx_host is given, entry t*k+j of it (in
 // host-coherent memory) also receives (seq << 32 | id) as one 64-bit store.
-// Decode (T <= 4): router logits and selection in one launch (the workgroup completing the logits
-// selects); the same ids, gates and tagged ids as launch_router_logits + launch_router_select.  *arrive
-// is a device counter that must be 0 and is left 0.  logits: [T, N] 64-bit words (at least 4 x N)
-// where the rows are published tagged with `tag`, which must differ from the tag of the launch that
-// last wrote them (a per-launch sequence number, never 0; the words start at 0).
+// Decode (T <= 4): router logits and selection in one launch (workgroup 0 selects once every row is
+// published); the same ids, gates and tagged ids as launch_router_logits + launch_router_select.
+// logits: [T, N] 64-bit words (at least 4 x N) where the rows are published tagged with `tag`, which
+// must differ from the tag of the launch that last wrote them (a per-launch sequence number, never 0;
+// the words start at 0).
 hipError_t launch_route_select(const float* wr, const void* x, int x_dtype, int d, uint64_t* logits, uint32_t tag,
-                               uint32_t* arrive, int T, int N, int k, int route, int n_groups, int topk_groups,
+                               int T, int N, int k, int route, int n_groups, int topk_groups,
                                int32_t* idx, float* w, uint64_t* idx_host, uint32_t seq, hipStream_t st,
                                const LaunchTiming& tm);
 hipError_t launch_router_select(const float* logits, int n_split, int T, int N, int k, int route, int n_groups,
@@ -149,12 +149,10 @@ hipError_t launch_select_page(const float* logits, int T, int N, int k, int rout
                               hipStream_t st, const LaunchTiming& tm);
 
 // Device pager, fused: the router logits of T <= 4 tokens (one workgroup per expert row, as
-// launch_router_logits) and, in the workgroup that completes them, launch_select_page's work.
-// `arrive` is a zero-initialised device counter used by one stream; the kernel leaves it zero.  logits
-// and tag as for launch_route_select.
+// launch_router_logits) and, in workgroup 0 once every row is published, launch_select_page's work.
+// logits and tag as for launch_route_select.
 hipError_t launch_route_page(const float* wr, const void* x, int x_dtype, int d, uint64_t* logits, uint32_t tag,
-                             uint32_t* arrive, int T,
-                             int N, int k, int route, int n_groups, int topk_groups, int32_t* idx, float* w,
+                             int T, int N, int k, int route, int n_groups, int topk_groups, int32_t* idx, float* w,
                              int32_t* pi, int32_t* pinv, uint64_t* tau, uint64_t* clock, int C,
                              const uint64_t* slot_ptr, const uint8_t* master_base, uint64_t master_stride,
                              const uint8_t* shared_dev, int has_shared, FfnBatch* plan, uint32_t* stats,

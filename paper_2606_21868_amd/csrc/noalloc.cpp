@@ -2,10 +2,9 @@
 //
 // The router kernels need device scratch beyond their inputs and outputs: the logits [T, N] fp32
 // (up to kRouterMaxSplit partial sums of them for token batches) and, for the one-launch path of up
-// to four tokens, the tagged logit words and the arrival counter
-// of the workgroups that publish logit rows.  Here that scratch is the file-scope array `scratch`
-// below, of a fixed size, held by every device the library runs on until the process ends.  Host code never passes the
-// array's name to a kernel (in host code it names a host-side stand-in); it passes the device
+// to four tokens, the tagged logit words of the workgroups that publish logit rows.  Here that
+// scratch is the file-scope array `scratch` below, of a fixed size, held by every device the library
+// runs on until the process ends.  Host code never passes the array's name to a kernel (in host code it names a host-side stand-in); it passes the device
 // address hipGetSymbolAddress returns for the current device, looked up once per device.
 #include <hip/hip_runtime.h>
 
@@ -19,11 +18,10 @@
 
 namespace {
 
-constexpr size_t kCounterBytes = 256;                       // arrival counter, own 256-byte line
 constexpr size_t kTagBytes = 4 * 256 * 8;                   // tagged logit words of the one-launch path
 // logits [T, N] fp32 of the two-launch path, as up to kRouterMaxSplit partial sums
 constexpr size_t kLogitBytes = static_cast<size_t>(wisp::kRouterMaxSplit) * WISP_NOALLOC_MAX_LOGITS * 4;
-constexpr size_t kScratchBytes = kCounterBytes + kTagBytes + kLogitBytes;
+constexpr size_t kScratchBytes = kTagBytes + kLogitBytes;
 constexpr int kMaxDevices = 64;
 
 static __device__ __align__(256) uint8_t scratch[kScratchBytes];
@@ -36,8 +34,8 @@ __global__ void clear_words_kernel(uint32_t* p, int n) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0u;
 }
 
-// The device address of `scratch` on the current device (looked up, and its counter and tag words
-// cleared, on the first call on that device).
+// The device address of `scratch` on the current device (looked up, and its tag words cleared, on the
+// first call on that device).
 wisp_status scratch_on_device(hipStream_t st, uint8_t** out) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
@@ -53,13 +51,12 @@ wisp_status scratch_on_device(hipStream_t st, uint8_t** out) {
       if (e != hipSuccess || !q)
         return wisp::set_error(WISP_E_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
       p = static_cast<uint8_t*>(q);
-      // the counter and the tag words must start at zero (every launch that uses the counter leaves it
-      // at zero again; tags are never 0); a kernel rather than a memset, so that a caller capturing
-      // this stream records no memset node
+      // the tag words must start at zero (tags are never 0); a kernel rather than a memset, so that a
+      // caller capturing this stream records no memset node
       hipLaunchKernelGGL(clear_words_kernel, dim3(1), dim3(256), 0, st, reinterpret_cast<uint32_t*>(p),
-                         static_cast<int>((kCounterBytes + kTagBytes) / 4));
+                         static_cast<int>(kTagBytes / 4));
       e = hipGetLastError();
-      if (e != hipSuccess) return wisp::set_error(WISP_E_HIP, std::string("counter clear: ") + hipGetErrorString(e));
+      if (e != hipSuccess) return wisp::set_error(WISP_E_HIP, std::string("tag clear: ") + hipGetErrorString(e));
       g_scratch_dev[dev].store(p, std::memory_order_release);
     }
   }
@@ -87,22 +84,21 @@ extern "C" wisp_status wisp_route_topk_noalloc(const float* w_r_dev, const void*
   if (T < 1) return set_error(WISP_E_INVAL, "T must be >= 1");
   if (static_cast<int64_t>(T) * N > WISP_NOALLOC_MAX_LOGITS)
     return set_error(WISP_E_INVAL, "T * N exceeds the static scratch of wisp_route_topk_noalloc (524288 logits)");
-  if (T > 8 && !(N % 16 == 0 && d % 64 == 0) && d % 32)
+  if (T > 8 && !(N % 16 == 0 && d % 16 == 0) && d % 32)
     return set_error(WISP_E_INVAL, "more than 8 tokens need d a multiple of 32");
   hipStream_t st = static_cast<hipStream_t>(stream);
   uint8_t* base = nullptr;
   wisp_status s = scratch_on_device(st, &base);
   if (s != WISP_OK) return s;
-  uint32_t* arrive = reinterpret_cast<uint32_t*>(base);
-  uint64_t* tagged = reinterpret_cast<uint64_t*>(base + kCounterBytes);
-  float* logits = reinterpret_cast<float*>(base + kCounterBytes + kTagBytes);
+  uint64_t* tagged = reinterpret_cast<uint64_t*>(base);
+  float* logits = reinterpret_cast<float*>(base + kTagBytes);
   hipError_t e;
   if (T <= 4) {
     int dev = 0;
     (void)hipGetDevice(&dev);
     uint32_t tag = g_tag[dev].fetch_add(1, std::memory_order_relaxed) + 1;
     if (tag == 0) tag = g_tag[dev].fetch_add(1, std::memory_order_relaxed) + 1;
-    e = wisp::launch_route_select(w_r_dev, x_dev, x_dtype, d, tagged, tag, arrive, T, N, k, route, n_groups,
+    e = wisp::launch_route_select(w_r_dev, x_dev, x_dtype, d, tagged, tag, T, N, k, route, n_groups,
                                   topk_groups, idx_dev, w_dev, nullptr, 0, st, wisp::LaunchTiming{});
   } else {
     int n_split = 1;

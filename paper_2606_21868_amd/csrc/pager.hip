@@ -213,39 +213,36 @@ __global__ void __launch_bounds__(256) select_page_kernel(
                          master_base, master_stride, shared_dev, has_shared, plan, stats);
 }
 
-// Router logits, selection and Algorithm 1 of one layer-step in one launch.  Workgroup e computes
-// logit row e (router_row, as the router kernel does), publishes it as tagged words (tag_logit, one
-// atomic store each) and counts itself in *arrive; the workgroup whose arrival is the N-th resets the
-// counter and runs the selection and the pager on the complete logits, reading each word until it
-// carries this launch's tag.  No workgroup waits for another's progress.
+// Router logits, selection and Algorithm 1 of one layer-step in one launch.  Workgroup e computes logit
+// row e (router_row, as the router kernel does) and publishes it as tagged words (tag_logit, one atomic
+// store each); workgroup 0, which has loaded the slot table into registers before its row, then runs the
+// selection and the pager on the complete logits, reading each word until it carries this launch's tag.
+// The other workgroups wait for nothing.
 template <int XT>
 __global__ void __launch_bounds__(256) route_page_kernel(
     const float* __restrict__ wr, const void* __restrict__ x, int d, uint64_t* __restrict__ logits, uint32_t tag,
-    uint32_t* __restrict__ arrive, int T, int N, int k, int route, int n_groups, int topk_groups,
+    int T, int N, int k, int route, int n_groups, int topk_groups,
     int32_t* __restrict__ idx, float* __restrict__ w, int32_t* __restrict__ pi, int32_t* __restrict__ pinv,
     uint64_t* __restrict__ tau, uint64_t* __restrict__ clock, int C, const uint64_t* __restrict__ slot_ptr,
     const uint8_t* master_base, uint64_t master_stride, const uint8_t* shared_dev, int has_shared,
     FfnBatch* __restrict__ plan, uint32_t* __restrict__ stats) {
   __shared__ PagerShared sh;
   __shared__ float part[4][4];
-  __shared__ int last;
   const int e = blockIdx.x;
-  // every workgroup loads the table into registers first (a few hundred words, mostly L2 hits), so
-  // the one that turns out to be last has it without another round trip; the row loads follow
-  // without waiting for the table
+  if (e != 0) {
+    const float z = router_row<XT>(wr, x, 0, T, d, e, part);
+    if (static_cast<int>(threadIdx.x) < T)
+      __hip_atomic_store(logits + static_cast<size_t>(threadIdx.x) * N + e, tag_logit(tag, z), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  // the table goes into registers first (its loads do not depend on the routing), the row loads follow
+  // without waiting for it
   const TableRegs tab = load_table_regs(N, C, pi, pinv, tau, clock, slot_ptr);
   const float z = router_row<XT>(wr, x, 0, T, d, e, part);
   if (static_cast<int>(threadIdx.x) < T)
     __hip_atomic_store(logits + static_cast<size_t>(threadIdx.x) * N + e, tag_logit(tag, z), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t before = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    last = before + 1 == static_cast<uint32_t>(N);
-    if (last) __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __syncthreads();
-  if (!last) return;
   store_table(sh, N, C, tab);   // read after select_tokens' first barrier
   select_and_page<true>(sh, logits, tag, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
                         master_base, master_stride, shared_dev, has_shared, plan, stats);
@@ -254,7 +251,7 @@ __global__ void __launch_bounds__(256) route_page_kernel(
 }  // namespace
 
 hipError_t launch_route_page(const float* wr, const void* x, int x_dtype, int d, uint64_t* logits, uint32_t tag,
-                             uint32_t* arrive, int T,
+                             int T,
                              int N, int k, int route, int n_groups, int topk_groups, int32_t* idx, float* w,
                              int32_t* pi, int32_t* pinv, uint64_t* tau, uint64_t* clock, int C,
                              const uint64_t* slot_ptr, const uint8_t* master_base, uint64_t master_stride,
@@ -265,11 +262,11 @@ hipError_t launch_route_page(const float* wr, const void* x, int x_dtype, int d,
     return hipErrorInvalidValue;
   if (x_dtype == DT_F32)
     hipExtLaunchKernelGGL(route_page_kernel<DT_F32>, dim3(N), dim3(256), 0, st, tm.start, tm.stop, 0, wr, x, d, logits,
-                          tag, arrive, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C, slot_ptr,
+                          tag, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C, slot_ptr,
                           master_base, master_stride, shared_dev, has_shared, plan, stats);
   else
     hipExtLaunchKernelGGL(route_page_kernel<DT_BF16>, dim3(N), dim3(256), 0, st, tm.start, tm.stop, 0, wr, x, d,
-                          logits, tag, arrive, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
+                          logits, tag, T, N, k, route, n_groups, topk_groups, idx, w, pi, pinv, tau, clock, C,
                           slot_ptr, master_base, master_stride, shared_dev, has_shared, plan, stats);
   return hipGetLastError();
 }

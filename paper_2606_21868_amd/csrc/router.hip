@@ -214,35 +214,25 @@ __global__ void __launch_bounds__(256) router_select_kernel(const float* __restr
 }
 
 // Router logits and the selection of up to four tokens in one launch (decode).  Workgroup e computes
-// logit row e (router_row: the arithmetic of router_logits_wide_kernel), publishes it as tagged words
-// (tag_logit, one atomic store each) and counts itself in *arrive; the workgroup whose arrival
-// completes the count resets the counter and selects on the complete logits, reading each word until
-// it carries this launch's tag, and writes idx, w and, if asked, the tagged ids for the host.  No
-// workgroup waits for another's progress: the count only elects the selecting workgroup, and the
-// tags (not an ordering of the counter after the stores) make it read this launch's logits.
+// logit row e (router_row: the arithmetic of router_logits_wide_kernel) and publishes it as tagged words
+// (tag_logit, one atomic store each); workgroup 0, after its own row, selects on the complete logits,
+// reading each word until it carries this launch's tag, and writes idx, w and, if asked, the tagged ids
+// for the host.  The other workgroups wait for nothing, and the tags (atomic accesses to one location
+// are coherent) make workgroup 0 read this launch's logits with no ordering between locations.
 template <int XT>
 __global__ void __launch_bounds__(256) route_select_kernel(const float* __restrict__ wr, const void* __restrict__ x,
-                                                           int d, uint64_t* __restrict__ logits, uint32_t tag,
-                                                           uint32_t* __restrict__ arrive, int T, int N, int k,
-                                                           int route, int n_groups, int topk_groups,
+                                                           int d, uint64_t* __restrict__ logits, uint32_t tag, int T,
+                                                           int N, int k, int route, int n_groups, int topk_groups,
                                                            int32_t* __restrict__ idx, float* __restrict__ w,
                                                            uint64_t* __restrict__ idx_host, uint32_t seq) {
   __shared__ SelectShared sh;
   __shared__ float part[4][4];
-  __shared__ int last;
   const int e = blockIdx.x;
   const float z = router_row<XT>(wr, x, 0, T, d, e, part);
   if (static_cast<int>(threadIdx.x) < T)
     __hip_atomic_store(logits + static_cast<size_t>(threadIdx.x) * N + e, tag_logit(tag, z), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t before = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    last = before + 1 == static_cast<uint32_t>(N);
-    if (last) __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __syncthreads();
-  if (!last) return;
+  if (e != 0) return;
   select_tokens<true>(logits, tag, 0, T, N, k, route, n_groups, topk_groups, sh);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (wave < T && lane < k) {
@@ -258,7 +248,7 @@ __global__ void __launch_bounds__(256) route_select_kernel(const float* __restri
 }  // namespace
 
 hipError_t launch_route_select(const float* wr, const void* x, int x_dtype, int d, uint64_t* logits, uint32_t tag,
-                               uint32_t* arrive, int T, int N, int k, int route, int n_groups, int topk_groups,
+                               int T, int N, int k, int route, int n_groups, int topk_groups,
                                int32_t* idx, float* w, uint64_t* idx_host, uint32_t seq, hipStream_t st,
                                const LaunchTiming& tm) {
   if (T < 1 || T > 4 || N < 1 || N > 256 || k < 1 || k > 8 || d % 4 != 0 ||
@@ -266,10 +256,10 @@ hipError_t launch_route_select(const float* wr, const void* x, int x_dtype, int 
     return hipErrorInvalidValue;
   if (x_dtype == DT_F32)
     hipExtLaunchKernelGGL(route_select_kernel<DT_F32>, dim3(N), dim3(256), 0, st, tm.start, tm.stop, 0, wr, x, d, logits,
-                          tag, arrive, T, N, k, route, n_groups, topk_groups, idx, w, idx_host, seq);
+                          tag, T, N, k, route, n_groups, topk_groups, idx, w, idx_host, seq);
   else
     hipExtLaunchKernelGGL(route_select_kernel<DT_BF16>, dim3(N), dim3(256), 0, st, tm.start, tm.stop, 0, wr, x, d,
-                          logits, tag, arrive, T, N, k, route, n_groups, topk_groups, idx, w, idx_host, seq);
+                          logits, tag, T, N, k, route, n_groups, topk_groups, idx, w, idx_host, seq);
   return hipGetLastError();
 }
 
