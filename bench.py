@@ -171,6 +171,7 @@ def sweep_leg(run, wl, wisp, torch, warmup=16, steps=96, offload_steps=3):
             faults["n"] = int(run.decode(record=False, steps=n, start=warmup)["misses"].sum())
 
         paged = timed(paged_run, steps)
+        resident = resident_roofline(run, wl, wisp, paged, warmup) if cap == wl.N else None
         run.ctx.set_pager(wisp.PAGER_HOST)
         arms = {}
         for mode, name in ((wisp.OFFLOAD_BULK, "static_offload"), (wisp.OFFLOAD_ZERO_COPY, "zero_copy_offload")):
@@ -186,10 +187,47 @@ def sweep_leg(run, wl, wisp, torch, warmup=16, steps=96, offload_steps=3):
                         speedup_vs_zero_copy=paged / zc[0],
                         bulk_offload_tokens_per_s=st[0], bulk_resident_layers=st[1],
                         speedup_vs_bulk=paged / st[0]))
+        if resident:
+            out[-1]["resident"] = resident
         log(f"sweep C={cap:3d} ({budget / 1e9:5.1f} GB): paged {paged:7.2f} tokens/s; zero-copy offload {zc[0]:7.2f} "
             f"({zc[1]} resident layers) -> {paged / zc[0]:4.1f}x; bulk offload {st[0]:7.2f} ({st[1]}) -> "
             f"{paged / st[0]:5.1f}x")
     return out
+
+
+def resident_roofline(run, wl, wisp, tokens_per_s, start, census_steps=24):
+    """Every expert resident (C = N, preloaded, device pager): the decode path is HBM-bound, with
+    T_roof = (k experts' blobs + the fp32 router matrix) per layer / 8 TB/s.  Reports that fraction and,
+    from census steps with every kernel class event-timed, each kernel's launch time and HBM rate
+    (algorithmic bytes: the router matrix for the fused router + selection + paging kernel, the k
+    experts' W1/W3 rows for gate/up, their W2 rows for down + combine)."""
+    hbm_per_token = wl.L * (wl.T * wl.k * wl.blob + wl.N * wl.d * 4)
+    roof = HBM_PEAK_GBPS * 1e9 / hbm_per_token * wl.T
+    run.ctx.reset_kernel_times()
+    run.ctx.set_profiling(True)
+    run.decode(record=False, steps=census_steps, start=start, stats=False)
+    run.ctx.set_profiling(0)
+    wbytes = 2 if wl.w_dtype == wisp.BF16 else 4
+    per_launch = {"router_select": wl.N * wl.d * 4, "ffn_gateup": wl.T * wl.k * 2 * wl.d * wl.I * wbytes,
+                  "down_combine": wl.T * wl.k * wl.d * wl.I * wbytes}
+    kern = {}
+    for kc, name in enumerate(wisp.KERNEL_CLASS_NAMES):
+        t = run.ctx.kernel_times(kc)
+        if not t["launches"]:
+            continue
+        avg_us = t["total_ms"] * 1e3 / t["launches"]
+        e = dict(launches=t["launches"], avg_us=avg_us)
+        if name in per_launch:
+            gbps = per_launch[name] / (avg_us * 1e-6) / 1e9
+            e.update(bytes_per_launch=per_launch[name], GBps=gbps, frac_of_hbm_peak=gbps / HBM_PEAK_GBPS)
+        kern["route_page" if name == "router_select" else name] = e
+    log(f"resident decode (C = N): {tokens_per_s:.0f} tokens/s = {tokens_per_s / roof:.3f} of its HBM roofline "
+        f"({roof:.0f}); " + ", ".join(f"{k} {v['avg_us']:.2f} us" + (f" ({v['frac_of_hbm_peak']:.2f} of HBM)"
+                                                                    if 'frac_of_hbm_peak' in v else "")
+                                      for k, v in kern.items()))
+    return dict(hbm_bytes_per_token=hbm_per_token, roofline_tokens_per_s=roof, frac=tokens_per_s / roof,
+                us_per_layer_step=1e6 / tokens_per_s * wl.T / wl.L, kernels=kern,
+                kernel_source="census steps after the timed ones, every kernel class event-timed")
 
 
 def configurator_leg(run, wl, wisp, torch, link_cu, warmup=16, steps=96):
