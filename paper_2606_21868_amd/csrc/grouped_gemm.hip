@@ -5,9 +5,9 @@
 // across many rows and the FFN is a set of small dense GEMMs, one per expert:
 //   H_e = silu(X_e W1_e^T) * (X_e W3_e^T)     X_e: the rows of the tokens routed to e  [n_e, d]
 //   O_e = H_e W2_e^T                                                                    [n_e, d]
-// The (token, rank) pairs are first ordered by expert (permute_pairs_kernel: a stable counting
-// sort, so expert e owns rows [off_e, off_e + n_e) of the sorted order and, inside, its pairs
-// ascend).  The GEMM kernels read the weights through the expert's slot address and gather or
+// The (token, rank) pairs are first ordered by expert (permute_count_kernel + permute_scatter_kernel:
+// a stable counting sort, so expert e owns rows [off_e, off_e + n_e) of the sorted order and, inside,
+// its pairs ascend).  The GEMM kernels read the weights through the expert's slot address and gather or
 // scatter rows through the permutation; H is kept in the sorted order (bf16, as in decode) and O
 // lands in the per-(token, rank) rows that the combine reads.
 //

@@ -45,9 +45,10 @@ __device__ __forceinline__ uint64_t tag_logit(uint32_t tag, float z) {
 }
 
 // Spins (bounded) until the word carries `tag`.  Atomic accesses to one location are coherent, so once
-// the publishing workgroup's store is visible the word holds this launch's logit; every publisher has
-// issued its store before it counted itself, so the wait is short.  After kTagSpins polls the word is
-// used as it is (a bound that a store already issued never reaches).
+// the publishing workgroup's store is visible the word holds this launch's logit.  Only the reading
+// workgroup waits; every publisher computes its row and stores it without waiting for anything, so
+// each store is issued once the publisher has been dispatched, whether or not all workgroups fit on
+// the chip at once.  After kTagSpins polls (seconds) the word is used as it is.
 constexpr int kTagSpins = 1 << 22;
 __device__ __forceinline__ float read_tagged_logit(const uint64_t* p, uint32_t tag) {
   uint64_t v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -342,7 +342,11 @@ def run_case(wl, cap, steps, sample_points=None, check_all_outputs=False, tokens
             assert np.array_equal(dev["hits"], out["hits"]) and np.array_equal(dev["misses"], out["misses"])
             assert [[run.ctx.slot_of(l, e) for e in range(wl.N)] for l in range(wl.L)] == tables
             assert np.array_equal(dev["y"].view(np.uint32), out["y"].view(np.uint32)), "device pager changed bits"
-            log("  device pager: same routing, faults, slot tables and output bits as the host pager")
+            # the device pager's gate/up launch fills the faulted slots itself (W1/W3 while computing, the
+            # rest of the blob by workgroups of its own)
+            n_dev = check_slots_hold_masters(run)
+            log(f"  device pager: same routing, faults, slot tables and output bits as the host pager; {n_dev} "
+                f"resident slots byte-equal to their masters")
         elif not (cap >= wl.T * wl.k and wl.T <= 4 and not pageable):
             with pytest.raises(wisp.WispError) as ei:
                 run.ctx.set_pager(wisp.PAGER_DEVICE)

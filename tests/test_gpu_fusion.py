@@ -10,7 +10,7 @@ be the one that ran, and the fused outputs are checked against the oracle.
 import numpy as np
 import pytest
 
-from parity import check_run, log
+from parity import check_run, check_slots_hold_masters, log
 from paper_2606_21868_amd import wisp
 from paper_2606_21868_amd.workloads import WORKLOADS
 
@@ -60,9 +60,11 @@ def test_fused_matches_separate_kernels_and_oracle(shape, cap, steps):
             assert np.array_equal(dev["idx"], sep["idx"]) and np.array_equal(dev["w"].view(np.uint32), sep["w"].view(np.uint32))
             assert np.array_equal(dev["hits"], sep["hits"]) and np.array_equal(dev["misses"], sep["misses"])
             assert np.array_equal(dev["y"].view(np.uint32), sep["y"].view(np.uint32)), "device pager: bits differ"
+            assert check_slots_hold_masters(run) > 0   # the faults' blobs filled by the device-planned gate/up
             sep_dev = _decode(run, False, wisp.PAGER_DEVICE)
             assert sep_dev["fused_launches"] == 0
             assert np.array_equal(sep_dev["y"].view(np.uint32), sep["y"].view(np.uint32))
+            assert check_slots_hold_masters(run) > 0
         assert np.array_equal(fus["idx"], sep["idx"])
         assert np.array_equal(fus["hits"], sep["hits"]) and np.array_equal(fus["misses"], sep["misses"])
         assert np.array_equal(fus["y"].view(np.uint32), sep["y"].view(np.uint32)), "fused down+combine changed bits"
