@@ -602,6 +602,22 @@ def prefill_leg(wisp, torch, link, link_cu, passes=3):
                 gms += t["total_ms"]
             kern[wisp.KERNEL_CLASS_NAMES[kc]] = e
         achieved = gflops / (gms * 1e-3) / 1e12 if gms > 0 else None
+        # what a plain streaming read of each GEMM launch's algorithmic bytes takes on this chip (fresh
+        # windows of a buffer beyond the last-level cache): the practical floor of an HBM-bound launch
+        floor = {}
+        for kc in (wisp.K_GROUPED_GATEUP, wisp.K_GROUPED_DOWN):
+            t = run.ctx.kernel_times(kc)
+            if t["launches"] and t["bytes"]:
+                nb = int(t["bytes"] // t["launches"]) // 16 * 16
+                us = wisp.probe_hbm_read(nb, 20)
+                name = wisp.KERNEL_CLASS_NAMES[kc]
+                floor[name] = dict(bytes_per_launch=nb, us_per_launch=us, GBps=nb / (us * 1e-6) / 1e9,
+                                   frac_of_peak=nb / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS,
+                                   kernel_frac_of_floor=us / kern[name]["avg_us"])
+        if floor:
+            log("prefill: plain read of the same bytes " + "; ".join(
+                f"{k} {v['bytes_per_launch'] / 1e6:.0f} MB in {v['us_per_launch']:.1f} us = {v['GBps']:.0f} GB/s "
+                f"(the GEMM at {v['kernel_frac_of_floor']:.2f} of it)" for k, v in floor.items()))
         mfma_peak = wisp.probe_mfma(10)   # the vendor's dense bf16 peak, checked on this chip
         log(f"prefill: matrix cores sustain {mfma_peak:.0f} TFLOP/s of dense bf16 on register operands "
             f"({mfma_peak / MFMA_BF16_PEAK_TFLOPS:.3f} of the 2.5 PFLOP/s peak)")
@@ -627,7 +643,10 @@ def prefill_leg(wisp, torch, link, link_cu, passes=3):
             # ridge (2.5 PFLOP/s / 8 TB/s = 312): HBM is their bound
             hbm=dict(bound="hbm", achieved=gbytes / (gms * 1e-3) / 1e9 if gms > 0 else None, peak=HBM_PEAK_GBPS,
                      unit="GB/s", frac=gbytes / (gms * 1e-3) / 1e9 / HBM_PEAK_GBPS if gms > 0 else None,
-                     kernels="grouped gate/up + down, algorithmic bytes (weights once, rows in and out)"))
+                     kernels="grouped gate/up + down, algorithmic bytes (weights once, rows in and out)",
+                     read_floor=floor,
+                     frac_of_read_floor=(sum(v["us_per_launch"] * kern[k]["launches"] for k, v in floor.items()) /
+                                         sum(kern[k]["total_ms"] * 1e3 for k in floor)) if floor else None))
     finally:
         run.close()
 

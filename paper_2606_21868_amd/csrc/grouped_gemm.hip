@@ -11,17 +11,17 @@
 // scatter rows through the permutation; H is kept in the sorted order (bf16, as in decode) and O
 // lands in the per-(token, rank) rows that the combine reads.
 //
-// Tiles: 64 rows x 64 h-columns for gate/up (the B tile holds the matching 64 rows of W1 and of
-// W3, so SwiGLU is applied in registers), 64 rows x 128 columns for down; K in stages of 64 through
-// one LDS buffer with padded rows, the next two stages loaded into registers meanwhile (k_loop
-// below), four workgroups per CU.  Four waves per
-// workgroup, each a 32-row slab of the tile on v_mfma_f32_32x32x16_bf16 (A lane l holds row l%32,
-// k 8*(l/32)..+7; B lane l holds column l%32, same k; D lane l holds column l%32, rows
-// 8*(r/4) + 4*(l/32) + r%4).  Every output element is one
-// fixed-order reduction over K, independent of where its row sits in a tile or which launch holds
-// its expert, so paged and fully resident runs give identical bits.
+// The matrix cores run v_mfma_f32_32x32x16_bf16 with the token rows as the A operand (lane l holds
+// row l%32, k 8*(l/32)..+7 of a 16-step), the weight rows as B (lane l holds weight row l%32, same k)
+// and D lane l holding column l%32, rows 8*(r/4) + 4*(l/32) + r%4.  Every output element is one
+// fixed-order reduction over K in ascending 16-steps, independent of where its row sits in a tile or
+// which launch holds its expert, so paged and fully resident runs give identical bits.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <type_traits>
+#include <utility>
 
 #include "kernels.hpp"
 
@@ -32,44 +32,12 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));   // a plain vector: stays in registers
 
-constexpr int GM = 64;          // rows (pairs) per tile
-constexpr int GN_UP = 64;       // h columns per gate/up tile
-constexpr int GN_DOWN = 128;    // output columns per down tile
-constexpr int KS_UP = 64;       // K per LDS stage, gate/up (K = d): 27 KB of LDS per workgroup
-constexpr int KS_DOWN = 64;     // K per LDS stage, down (K = I)
-constexpr int kWgsPerCu = 4;    // occupancy the kernels are compiled for (≤ 128 registers per lane)
+constexpr uint32_t kOutOfRange = 0x80000000u;   // a byte offset past every resource below 2 GiB
 
 __device__ __forceinline__ uint16_t bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
   u += 0x7FFFu + ((u >> 16) & 1u);
   return static_cast<uint16_t>(u >> 16);
-}
-
-// Tile -> (group, row tile, column tile).  Workgroups are dealt to the 8 XCDs round-robin by
-// blockIdx.x, and each XCD has its own L2; the logical tile order is remapped so that every XCD gets
-// one contiguous run of logical tiles.  Logical tiles run expert by expert, and inside an expert
-// column-tile-major: the 2-3 row tiles of a column tile are adjacent (they read the same weight rows
-// at the same time), and an expert's gathered rows (≈0.5 MB) stay in the L2 across its column
-// tiles.  Against row-tile-major order this cut the gate/up launch's fetched bytes from 1.56x to
-// 1.17x the algorithmic bytes.
-constexpr int kXcds = 8;
-__device__ __forceinline__ void tile_of(const GroupedBatch& gb, int n_ctiles, int& g, int& mt, int& ct) {
-  const int n = static_cast<int>(gridDim.x);
-  const int xcd = static_cast<int>(blockIdx.x) % kXcds, j = static_cast<int>(blockIdx.x) / kXcds;
-  const int q = n / kXcds, r = n % kXcds;
-  const int logical = xcd * q + min(xcd, r) + j;   // a bijection of [0, n)
-  const int mt_all = logical / n_ctiles;          // expert g owns logical tiles [t0, t_end) x n_ctiles
-  int lo = 0, hi = gb.n_groups - 1;   // the first group whose tiles end past mt_all
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (mt_all >= gb.tile_end[mid]) lo = mid + 1;
-    else hi = mid;
-  }
-  g = lo;
-  const int t0 = g > 0 ? gb.tile_end[g - 1] : 0, n_mt = gb.tile_end[g] - t0;
-  const int local = logical - t0 * n_ctiles;
-  ct = local / n_mt;
-  mt = local - ct * n_mt;
 }
 
 // Stable counting sort of the pairs p = t*k + j by expert id idx[p], in two launches over segments of
@@ -161,217 +129,316 @@ __global__ void __launch_bounds__(1024) permute_scatter_kernel(const int32_t* __
   if (valid) perm[base[e] + cnt[wave][e] + __popcll(same & below)] = p;
 }
 
-// One K stage of a 64-row A tile and a 128-row B tile through LDS.  A thread loads 16-byte pieces
-// of TPR-thread row segments (KS bf16 = 2*KS contiguous bytes of a row per stage: whole 128-byte
-// lines for KS = 64).  Loads are buffer loads: one uniform resource per operand (base and size in
-// scalar registers), a 32-bit byte offset per piece and the stage's K offset as the scalar offset,
-// which keeps the per-thread address state to one register per piece.  An A row past the expert's
-// rows gets an offset beyond the resource's size, and the hardware's range check returns zeros for
-// it without touching memory.  LDS holds one stage, rows padded by 16 bytes (the 16-byte reads of 16
-// consecutive rows hit distinct banks).
-template <int KS>
-struct Stage {
-  static constexpr int TPR = KS * 2 / 16;     // threads per row segment
-  static constexpr int RPI = 256 / TPR;       // rows per load instruction
-  static constexpr int AL = GM / RPI;         // A loads per thread
-  static constexpr int BL = 128 / RPI;        // B loads per thread
-  static constexpr int LDK = KS + 8;          // LDS row stride, bf16 elements
+// ------------------------------------------------------------------------------------------
+// The GEMM kernels are persistent: one 512-thread workgroup per CU walks its share of the tiles, and
+// the K stages of all its tiles form one sequence, so the loads of the next tile's first stages are
+// in flight while the current tile finishes (no pipeline start per tile).
+//
+// Weights (B operand: 128 weight rows x 64 K per stage, 16 KB) go from HBM straight into a ring of
+// kNB LDS slots by buffer-to-LDS loads (buffer_load_dwordx4 ... lds), kNB - 1 stages ahead, so the
+// bytes in flight do not occupy registers.  Inside a slot, 16-byte chunk c of weight row r sits at
+// position c ^ swz(r), which keeps the fragment reads free of bank conflicts.  The token rows (A
+// operand) are private to a wave (wave w owns rows 32 w .. 32 w + 31 of the row block): they are loaded
+// into registers in the matrix cores' operand layout, the same kNB - 1 stages ahead (the vector-memory
+// counter retires loads in issue order, so a shallower A prefetch would also retire the deeper weight
+// loads early).  A weight fragment is read from LDS by an inline ds_read (the compiler then does not
+// make the LDS reads wait for every buffer-to-LDS load in flight); the workgroup barrier is a plain
+// s_barrier after an explicit wait for this stage's loads.
+//
+// Tiles: 64 h columns (W1 and W3 rows c0 .. c0 + 63, so SwiGLU is applied in registers) for gate/up,
+// 128 output columns (W2 rows) for down, each over up to kRB = 256 rows of one expert: all of them at
+// the routing's usual ~T k / N rows per expert, so each weight byte is read once and rows are padded
+// only to the 32-row slab of a wave.
+// ------------------------------------------------------------------------------------------
+constexpr int kRB = 256;                 // rows per row block: 8 slabs of 32, one per wave
+constexpr int kGW = 8;                   // waves per workgroup
+constexpr int kKS = 64;                  // K per stage
+constexpr int kNB = 4;                   // LDS ring slots; loads run kNB - 1 stages ahead
+constexpr int kD = kNB - 1;
+constexpr int kSlot = 128 * kKS * 2;     // bytes per slot: 128 weight rows x 64 K, bf16
+constexpr int kBI = kSlot / 1024 / kGW;  // buffer-to-LDS loads per wave per stage (1 KB each)
+constexpr int kAI = kKS / 16;            // A fragment loads per wave per stage (16 B per lane each)
+constexpr int MODE_UP = 0, MODE_DN = 1;
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// s_waitcnt immediate (gfx9 encoding) that waits for vector-memory count n only: vmcnt in bits 3:0
+// and 15:14, expcnt (6:4) and lgkmcnt (11:8) left at their maximum.
+constexpr int vmcnt_only(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
+// chunk swizzle of weight row r inside a slot: rows r .. r + 7 take distinct positions for one chunk,
+// and so do the pairs (r & 1, position) of rows r .. r + 15
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// Tile T of a launch -> its expert, row block and column tile.  Tiles run expert by expert, row block
+// by row block, column tile fastest; gb.tile_end holds the cumulative row blocks per expert.
+struct Tile {
+  const uint8_t* w;
+  int rows, base, m0, c0;
 };
-
-constexpr uint32_t kOutOfRange = 0x80000000u;   // a byte offset past every resource below 2 GiB
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t operand(const void* base, uint32_t bytes) {
-  // raw (stride 0) resource over [base, base + bytes); the third word is the gfx9 data format 32
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000);
+template <int MODE>
+__device__ __forceinline__ Tile decode_tile(const GroupedBatch& gb, int T, int n_ct) {
+  const int rb_all = T / n_ct, ct = T - rb_all * n_ct;
+  int lo = 0, hi = gb.n_groups - 1;   // the first expert whose row blocks end past rb_all
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (rb_all >= gb.tile_end[mid]) lo = mid + 1;
+    else hi = mid;
+  }
+  const int rb = rb_all - (lo > 0 ? gb.tile_end[lo - 1] : 0);
+  return Tile{gb.w[lo], gb.rows[lo], gb.row_off[lo], rb * kRB, ct * (MODE == MODE_UP ? 64 : 128)};
 }
 
-template <int KS>
-__device__ __forceinline__ void stage_load(__amdgpu_buffer_rsrc_t ar, const uint32_t* a_off, __amdgpu_buffer_rsrc_t br,
-                                           const uint32_t* b_off, int kb, u32x4_t* ra, u32x4_t* rb) {
-  const int sk = __builtin_amdgcn_readfirstlane(kb * 2);   // uniform: the scalar offset, not a per-lane one
-#pragma unroll
-  for (int i = 0; i < Stage<KS>::AL; ++i) ra[i] = __builtin_amdgcn_raw_buffer_load_b128(ar, a_off[i], sk, 0);
-#pragma unroll
-  for (int i = 0; i < Stage<KS>::BL; ++i) rb[i] = __builtin_amdgcn_raw_buffer_load_b128(br, b_off[i], sk, 0);
+// Eight weight fragments of one slot (two 16-steps x four 32-column blocks), read by inline ds_reads:
+// f[kk][cb] for 16-step kk0 + kk.  IMM = the slot's byte offset + 0 (the four column blocks are 4 KB
+// apart); addr0/addr1 = the lane's offsets of its row and chunk for the two 16-steps.
+template <int IMM>
+__device__ __forceinline__ void read_frags(u32x4_t (&f)[2][4], uint32_t addr0, uint32_t addr1) {
+  asm volatile(
+      "ds_read_b128 %0, %8 offset:%10\n\t"
+      "ds_read_b128 %1, %8 offset:%11\n\t"
+      "ds_read_b128 %2, %8 offset:%12\n\t"
+      "ds_read_b128 %3, %8 offset:%13\n\t"
+      "ds_read_b128 %4, %9 offset:%10\n\t"
+      "ds_read_b128 %5, %9 offset:%11\n\t"
+      "ds_read_b128 %6, %9 offset:%12\n\t"
+      "ds_read_b128 %7, %9 offset:%13\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(f[0][0]), "=&v"(f[0][1]), "=&v"(f[0][2]), "=&v"(f[0][3]), "=&v"(f[1][0]), "=&v"(f[1][1]), "=&v"(f[1][2]),
+        "=&v"(f[1][3])
+      : "v"(addr0), "v"(addr1), "i"(IMM), "i"(IMM + 4096), "i"(IMM + 8192), "i"(IMM + 12288)
+      : "memory");
 }
 
-template <int KS>
-__device__ __forceinline__ void stage_store(uint16_t* As, uint16_t* Bs, int tr, int tq, const u32x4_t* ra,
-                                            const u32x4_t* rb) {
-  using S = Stage<KS>;
-#pragma unroll
-  for (int i = 0; i < S::AL; ++i) *reinterpret_cast<u32x4_t*>(&As[(tr + S::RPI * i) * S::LDK + tq]) = ra[i];
-#pragma unroll
-  for (int i = 0; i < S::BL; ++i) *reinterpret_cast<u32x4_t*>(&Bs[(tr + S::RPI * i) * S::LDK + tq]) = rb[i];
+// The A fragments of one stage: four 16-byte loads (the stage's four 16-steps) into registers, by
+// inline asm so that the compiler neither counts them nor waits for them: the caller waits by count
+// (every load of a stage is older than those of the stages after it) and then passes the registers
+// through pin_frags, after which the compiler reads them.
+__device__ __forceinline__ void load_a(u32x4_t (&a)[kAI], u32x4_t rs, uint32_t voff, uint32_t soff) {
+  asm volatile(
+      "buffer_load_dwordx4 %0, %4, %5, %6 offen\n\t"
+      "buffer_load_dwordx4 %1, %4, %5, %6 offen offset:32\n\t"
+      "buffer_load_dwordx4 %2, %4, %5, %6 offen offset:64\n\t"
+      "buffer_load_dwordx4 %3, %4, %5, %6 offen offset:96"
+      : "=&v"(a[0]), "=&v"(a[1]), "=&v"(a[2]), "=&v"(a[3])
+      : "v"(voff), "s"(rs), "s"(soff)
+      : "memory");
+}
+__device__ __forceinline__ void pin_frags(u32x4_t (&a)[kAI]) {
+  asm volatile("" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]));
+}
+// One int32 per lane, loaded the same way (waited for by count, then pinned).
+__device__ __forceinline__ int32_t load_i32(const int32_t* p) {
+  int32_t v;
+  asm volatile("global_load_dword %0, %1, off" : "=&v"(v) : "v"(p) : "memory");
+  return v;
+}
+__device__ __forceinline__ void pin_i32(int32_t& v) { asm volatile("" : "+v"(v)); }
+// raw buffer resource words (stride 0) over [p, p + bytes), as uniform values
+__device__ __forceinline__ u32x4_t rsrc_words(const void* p, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  u32x4_t r;
+  r.x = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a));
+  r.y = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32) & 0xFFFFu);
+  r.z = __builtin_amdgcn_readfirstlane(bytes);
+  r.w = 0x00020000u;
+  return r;
 }
 
-// The K loop of a tile (nk stages, nk even and >= 2).  LDS holds stage s while stages s + 1 and
-// s + 2 are in flight in two register sets, so a global load has two stages of MFMA work to arrive
-// in; with one stage in flight the loop waited on load latency (a stage took ≈2 µs against ≈0.3 µs
-// of matrix-core work).  A register set is stored to LDS only after its own loads, and the next
-// loads into it are issued right after the store.  Every load in the loop is unconditional and the
-// last four stages are peeled (nk = 2, SHORT, is an instantiation of its own): then each store waits only for its own set's loads (the other set's
-// six stay in flight), and the loop has one exit, so the accumulators keep one set of registers.
-// compute() runs the MFMAs of the stage in LDS.
-template <int KS, bool SHORT, typename F>
-__device__ __forceinline__ void k_loop(int nk, __amdgpu_buffer_rsrc_t ar, const uint32_t* a_off,
-                                       __amdgpu_buffer_rsrc_t br, const uint32_t* b_off, uint16_t* As, uint16_t* Bs,
-                                       int tr, int tq, F&& compute) {
-  using S = Stage<KS>;
-  u32x4_t ra0[S::AL], rb0[S::BL], ra1[S::AL], rb1[S::BL];
-  auto load0 = [&](int st) { stage_load<KS>(ar, a_off, br, b_off, st * KS, ra0, rb0); };
-  auto load1 = [&](int st) { stage_load<KS>(ar, a_off, br, b_off, st * KS, ra1, rb1); };
-  auto store0 = [&]() { __syncthreads(); stage_store<KS>(As, Bs, tr, tq, ra0, rb0); __syncthreads(); };
-  auto store1 = [&]() { __syncthreads(); stage_store<KS>(As, Bs, tr, tq, ra1, rb1); __syncthreads(); };
-  load0(0);
-  load1(1);
-  stage_store<KS>(As, Bs, tr, tq, ra0, rb0);
-  __syncthreads();
-  if constexpr (SHORT) {   // nk = 2 (a short K, such as I = 128 in the down GEMM)
-    compute();
-    store1();
-    compute();
+template <int... Us, typename F>
+__device__ __forceinline__ void ring_unroll(std::integer_sequence<int, Us...>, F&& f) {
+  (f(std::integral_constant<int, Us>{}), ...);
+}
+
+template <int MODE>
+__global__ void __launch_bounds__(512) grouped_kernel(GroupedBatch gb, const uint16_t* __restrict__ a_src,
+                                                      uint32_t a_bytes, const int32_t* __restrict__ perm, int k,
+                                                      int d, int I, void* __restrict__ out) {
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[kNB * kSlot];
+  const int K = MODE == MODE_UP ? d : I;             // reduction length
+  const int spt = K / kKS;                           // stages per tile
+  const int n_ct = MODE == MODE_UP ? I / 64 : d / 128;
+  const int n_tiles = gb.tile_end[gb.n_groups - 1] * n_ct;
+  // XCD-aware: workgroups are dealt to the 8 XCDs round-robin, and the workgroups of one XCD take
+  // consecutive logical indices, so at any time they work on consecutive tiles (the column tiles of
+  // the same one to three experts, whose token rows then stay in that XCD's L2)
+  const int G = static_cast<int>(gridDim.x);
+  const int xcd = static_cast<int>(blockIdx.x) % 8, jx = static_cast<int>(blockIdx.x) / 8;
+  const int L = xcd * (G / 8) + min(xcd, G % 8) + jx;
+  const int my_tiles = (n_tiles - L + G - 1) / G;
+  const int nq = my_tiles * spt;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, lr = lane & 31, hb = lane >> 5;
+  const uint32_t wrow = static_cast<uint32_t>(K) * 2;   // bytes per weight row
+  const uint32_t arow = static_cast<uint32_t>(K) * 2;   // bytes per A row (x: d, h: I)
+
+  // buffer-to-LDS pattern: slot position p = (wave kBI + i) 64 + lane holds chunk (p & 7) ^ swz(row)
+  // of weight row p >> 3 (gate/up: rows 0..63 are W1 rows c0.., 64..127 the W3 rows of the same columns)
+  uint32_t bpat[kBI];
+#pragma unroll
+  for (int i = 0; i < kBI; ++i) {
+    const int pp = (wave * kBI + i) * 64 + lane, r = pp >> 3, c = (pp & 7) ^ swz(r);
+    const int wr = MODE == MODE_UP ? (r < 64 ? r : I - 64 + r) : r;
+    bpat[i] = static_cast<uint32_t>(wr) * wrow + c * 16;
+  }
+  // fragment reads: lane l reads weight row 32 cb + l % 32, chunk 2 kk + l / 32 of the 16-step pair
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)ring));
+  uint32_t fo[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) fo[kk] = lds0 + lr * 128 + (((2 * kk + hb) ^ swz(lr)) << 4);
+  const u32x4_t ar = rsrc_words(a_src, a_bytes);
+  const uint32_t wbytes = static_cast<uint32_t>(I) * d * 2 * (MODE == MODE_UP ? 2 : 1);
+  const size_t woff = MODE == MODE_UP ? 0 : static_cast<size_t>(2) * I * d * 2;   // W2 follows W1, W3
+
+  // the issue cursor: the stage whose loads go out next
+  int is_tile = 0, is_s = 0;
+  __amdgpu_buffer_rsrc_t wr_rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a_src), 0, 0, 0x00020000);
+  uint32_t bvo[kBI], avo = 0;
+  // a lane's rows are read through the pair order: lane l holds the pair of row 32 wave + l % 32 of a
+  // tile (its last row where the tile has fewer), loaded a whole tile ahead of its use and waited for
+  // by count (all at once where a tile has fewer stages than the count covers)
+  const bool short_k = spt < kD + 2;
+  auto pair_of = [&](const Tile& t) __attribute__((always_inline)) -> int32_t {
+    return load_i32(perm + t.base + min(t.m0 + wave * 32 + lr, t.rows - 1));
+  };
+  int32_t pn = 0;   // gate/up: the pair of this lane's row in the issue cursor's next tile
+  auto enter_tile = [&](int i) __attribute__((always_inline)) {   // issue cursor enters its i-th tile
+    const Tile t = decode_tile<MODE>(gb, L + i * G, n_ct);
+    wr_rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(t.w + woff), 0, static_cast<int>(wbytes), 0x00020000);
+#pragma unroll
+    for (int j = 0; j < kBI; ++j) bvo[j] = bpat[j] + static_cast<uint32_t>(t.c0) * wrow;
+    const int row = t.m0 + wave * 32 + lr;
+    if constexpr (MODE == MODE_UP) {
+      if (short_k) __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+      pin_i32(pn);
+      avo = row < t.rows ? static_cast<uint32_t>(pn / k) * arow + hb * 16 : kOutOfRange;
+      if (i + 1 < my_tiles) pn = pair_of(decode_tile<MODE>(gb, L + (i + 1) * G, n_ct));
+    } else {
+      avo = row < t.rows ? static_cast<uint32_t>(t.base + row) * arow + hb * 16 : kOutOfRange;
+    }
+  };
+  u32x4_t A[kNB][kAI];
+  auto issue = [&](int slot, u32x4_t (&a)[kAI]) __attribute__((always_inline)) {   // the loads of the issue cursor's stage
+    if (is_s == 0) enter_tile(is_tile);
+    const int sk = __builtin_amdgcn_readfirstlane(is_s * kKS * 2);
+    load_a(a, ar, avo, sk);
+#pragma unroll
+    for (int j = 0; j < kBI; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr_rs, (lds_ptr_t)(ring + slot * kSlot + (wave * kBI + j) * 1024), 16,
+                                               bvo[j], sk, 0, 0);
+    if (++is_s == spt) {
+      is_s = 0;
+      ++is_tile;
+    }
+  };
+
+  // the compute cursor
+  int cs_tile = 0, cs_s = 0;
+  Tile ct = decode_tile<MODE>(gb, L, n_ct);
+  f32x16_t acc[4] = {};
+  int32_t pq = 0;   // down: the pair of this lane's row in the compute cursor's tile
+  if constexpr (MODE == MODE_UP) {
+    pn = pair_of(ct);
+    __builtin_amdgcn_s_waitcnt(vmcnt_only(0));   // nothing else is in flight yet
   } else {
-    load0(2);
-    int s = 0;
-    for (; s + 4 < nk; s += 2) {
-      compute();     // stage s
-      store1();      // stage s + 1
-      load1(s + 3);
-      compute();
-      store0();      // stage s + 2
-      load0(s + 4);
-    }
-    compute();       // stage nk - 4
-    store1();
-    load1(nk - 1);
-    compute();       // nk - 3
-    store0();
-    compute();       // nk - 2
-    store1();
-    compute();       // nk - 1
+    pq = pair_of(ct);
   }
-}
+  // Epilogue of a tile: each wave's 32 x 128 outputs (h columns for gate/up: silu(g) * u over the two
+  // gate and up blocks), one column per lane as the matrix cores leave them.
+  auto epilogue = [&]() __attribute__((always_inline)) {
+    const int n_rows = ct.rows - ct.m0 - wave * 32;   // rows of this wave's slab in the tile (may be <= 0)
+    if constexpr (MODE == MODE_UP) {
+      uint16_t* hs = static_cast<uint16_t*>(out);
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) {
+        const int col = ct.c0 + cb * 32 + lr;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int i = (r >> 2) * 8 + hb * 4 + (r & 3);
+          if (i < n_rows) {
+            const float a = acc[cb][r];
+            const float h = a / (1.0f + __expf(-a)) * acc[cb + 2][r];
+            hs[static_cast<size_t>(ct.base + ct.m0 + wave * 32 + i) * I + col] = bf16_rne(h);
+          }
+        }
+      }
+    } else {
+      float* buf = static_cast<float*>(out);
+      if (short_k) __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+      pin_i32(pq);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = (r >> 2) * 8 + hb * 4 + (r & 3);
+        const int p = __shfl(pq, i, 64);
+        if (i < n_rows) {
+          const size_t orow = static_cast<size_t>(p / k) * (k + 1) + (p % k);
+#pragma unroll
+          for (int cb = 0; cb < 4; ++cb) buf[orow * d + ct.c0 + cb * 32 + lr] = acc[cb][r];
+        }
+      }
+    }
+  };
 
-// H rows [off_g + m0, +64) x h columns [c0, +64) of one expert: silu(X W1^T) * (X W3^T) -> bf16.
-// The B tile's rows 0..63 are W1 rows c0.., rows 64..127 the W3 rows of the same columns.  x has
-// x_bytes bytes (the token rows).
-template <int KS, bool SHORT>
-__global__ void __launch_bounds__(256, kWgsPerCu) grouped_gateup_kernel(GroupedBatch gb, const uint16_t* __restrict__ x,
-                                                                         uint32_t x_bytes,
-                                                                         const int32_t* __restrict__ perm, int k, int d,
-                                                                         int I, uint16_t* __restrict__ hs) {
-  using S = Stage<KS>;
-  __shared__ __attribute__((aligned(16))) uint16_t As[GM * S::LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * GN_UP * S::LDK];
-  int g, mt, ct;
-  tile_of(gb, I / GN_UP, g, mt, ct);
-  const int rows = gb.rows[g], base = gb.row_off[g];
-  const int m0 = mt * GM, c0 = ct * GN_UP;
-  const int tid = threadIdx.x;
-  const int tr = tid / S::TPR, tq = (tid % S::TPR) * 8;
-  uint32_t a_off[S::AL];
+  // prologue: the first kD stages
 #pragma unroll
-  for (int i = 0; i < S::AL; ++i) {
-    const int r = m0 + tr + S::RPI * i;
-    a_off[i] = r < rows ? static_cast<uint32_t>(perm[base + r] / k) * d * 2 + tq * 2 : kOutOfRange;
-  }
-  uint32_t b_off[S::BL];
-#pragma unroll
-  for (int i = 0; i < S::BL; ++i) {
-    const int j = tr + S::RPI * i;     // B tile row: W1 row c0 + j, or W3 row c0 + j - 64 (W3 follows W1)
-    b_off[i] = static_cast<uint32_t>(j < GN_UP ? c0 + j : I + c0 + j - GN_UP) * d * 2 + tq * 2;
-  }
-  const __amdgpu_buffer_rsrc_t ar = operand(x, x_bytes);
-  const __amdgpu_buffer_rsrc_t br = operand(gb.w[g], static_cast<uint32_t>(2 * I) * d * 2);
-  const int wave = tid >> 6, lane = tid & 63, wm = wave >> 1, wn = wave & 1;
-  const int fr = lane & 31, fk = (lane >> 5) * 8;
-  f32x16_t accg = {}, accu = {};
-  k_loop<KS, SHORT>(d / KS, ar, a_off, br, b_off, As, Bs, tr, tq, [&]() {
-#pragma unroll
-    for (int kk = 0; kk < KS; kk += 16) {
-      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&As[(wm * 32 + fr) * S::LDK + kk + fk]);
-      const bf16x8_t bg = *reinterpret_cast<const bf16x8_t*>(&Bs[(wn * 32 + fr) * S::LDK + kk + fk]);
-      const bf16x8_t bu = *reinterpret_cast<const bf16x8_t*>(&Bs[(GN_UP + wn * 32 + fr) * S::LDK + kk + fk]);
-      accg = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bg, accg, 0, 0, 0);
-      accu = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bu, accu, 0, 0, 0);
-    }
-  });
-  const int hc = c0 + wn * 32 + fr;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int i = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-    if (m0 + i < rows) {
-      const float a = accg[r];
-      const float h = a / (1.0f + __expf(-a)) * accu[r];
-      hs[static_cast<size_t>(base + m0 + i) * I + hc] = bf16_rne(h);
-    }
-  }
-}
+  for (int u = 0; u < kD; ++u)
+    if (u < nq) issue(u, A[u]);
 
-// O rows of one expert x output columns [c0, +128): H W2^T in fp32, scattered to the rows
-// t*(k+1) + j of the pairs.  hs has hs_bytes bytes (the sorted pair rows).
-template <int KS, bool SHORT>
-__global__ void __launch_bounds__(256, kWgsPerCu) grouped_down_kernel(GroupedBatch gb, const uint16_t* __restrict__ hs,
-                                                                       uint32_t hs_bytes,
-                                                                       const int32_t* __restrict__ perm, int k, int d,
-                                                                       int I, float* __restrict__ buf) {
-  using S = Stage<KS>;
-  __shared__ __attribute__((aligned(16))) uint16_t As[GM * S::LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[GN_DOWN * S::LDK];
-  int g, mt, ct;
-  tile_of(gb, d / GN_DOWN, g, mt, ct);
-  const int rows = gb.rows[g], base = gb.row_off[g];
-  const int m0 = mt * GM, c0 = ct * GN_DOWN;
-  const int tid = threadIdx.x;
-  const int tr = tid / S::TPR, tq = (tid % S::TPR) * 8;
-  uint32_t a_off[S::AL];
+  auto step = [&](auto U_, int q) __attribute__((always_inline)) {
+    constexpr int U = decltype(U_)::value;   // q % kNB: the slot and the A register set
+    // stage q's own loads (its A fragments, then this wave's share of the slot) have landed: the
+    // operations issued after them are the loads of the kD - 1 later stages (fewer at the end of the
+    // sequence: then everything), plus, after a tile's end, its stores and pair loads (the count then
+    // waits a little longer than it must)
+    if (is_tile * spt + is_s == q + kD)
+      __builtin_amdgcn_s_waitcnt(vmcnt_only((kD - 1) * (kBI + kAI)));
+    else
+      __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+    pin_frags(A[U]);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();   // every wave's share landed; every wave is done with stage q - 1
+    asm volatile("" ::: "memory");
+    if (is_tile * spt + is_s < nq) issue((U + kD) % kNB, A[(U + kD) % kNB]);
+    if (wave * 32 < ct.rows - ct.m0) {   // the wave's slab has rows in this tile
 #pragma unroll
-  for (int i = 0; i < S::AL; ++i) {
-    const int r = m0 + tr + S::RPI * i;
-    a_off[i] = r < rows ? static_cast<uint32_t>(base + r) * I * 2 + tq * 2 : kOutOfRange;
-  }
-  uint32_t b_off[S::BL];
+      for (int h2 = 0; h2 < 2; ++h2) {
+        u32x4_t f[2][4];
+        // the slot's offset goes into the instruction's 16-bit offset field as far as it fits
+        constexpr uint32_t hi = static_cast<uint32_t>(U / 4) * 4 * kSlot;
+        read_frags<(U % 4) * kSlot>(f, fo[2 * h2] + hi, fo[2 * h2 + 1] + hi);
 #pragma unroll
-  for (int i = 0; i < S::BL; ++i) b_off[i] = static_cast<uint32_t>(c0 + tr + S::RPI * i) * I * 2 + tq * 2;
-  const __amdgpu_buffer_rsrc_t ar = operand(hs, hs_bytes);
-  const __amdgpu_buffer_rsrc_t br =
-      operand(reinterpret_cast<const uint16_t*>(gb.w[g]) + 2 * static_cast<size_t>(I) * d, static_cast<uint32_t>(I) * d * 2);
-  const int wave = tid >> 6, lane = tid & 63, wm = wave >> 1, wn = wave & 1;
-  const int fr = lane & 31, fk = (lane >> 5) * 8;
-  f32x16_t acc0 = {}, acc1 = {};
-  k_loop<KS, SHORT>(I / KS, ar, a_off, br, b_off, As, Bs, tr, tq, [&]() {
+        for (int kk = 0; kk < 2; ++kk) {
+          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, A[U][2 * h2 + kk]);
 #pragma unroll
-    for (int kk = 0; kk < KS; kk += 16) {
-      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&As[(wm * 32 + fr) * S::LDK + kk + fk]);
-      const bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(&Bs[(wn * 64 + fr) * S::LDK + kk + fk]);
-      const bf16x8_t b1 = *reinterpret_cast<const bf16x8_t*>(&Bs[(wn * 64 + 32 + fr) * S::LDK + kk + fk]);
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b0, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b1, acc1, 0, 0, 0);
+          for (int cb = 0; cb < 4; ++cb)
+            acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, f[kk][cb]), acc[cb], 0, 0, 0);
+        }
+      }
     }
-  });
-  const int oc = c0 + wn * 64 + fr;
+    if (++cs_s == spt) {
+      epilogue();
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int i = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-    if (m0 + i < rows) {
-      const int p = perm[base + m0 + i];
-      const size_t orow = static_cast<size_t>(p / k) * (k + 1) + (p % k);
-      buf[orow * d + oc] = acc0[r];
-      buf[orow * d + oc + 32] = acc1[r];
+      for (int cb = 0; cb < 4; ++cb) acc[cb] = f32x16_t{};
+      cs_s = 0;
+      if (++cs_tile < my_tiles) {
+        ct = decode_tile<MODE>(gb, L + cs_tile * G, n_ct);
+        if constexpr (MODE == MODE_DN) pq = pair_of(ct);
+      }
     }
-  }
+  };
+  // the loop is unrolled over the ring, so that slots and register sets have fixed indices
+  for (int q = 0; q < nq; q += kNB)
+    ring_unroll(std::make_integer_sequence<int, kNB>{}, [&](auto U_) __attribute__((always_inline)) {
+      if (q + decltype(U_)::value < nq) step(U_, q + decltype(U_)::value);
+    });
 }
 
 }  // namespace
 
 bool grouped_supported(const FfnShape& s, int has_shared) {
   return !has_shared && s.blob.w_dtype == DT_BF16 && s.x_dtype == DT_BF16 && s.h_dtype == DT_BF16 &&
-         s.blob.d % GN_DOWN == 0 && s.blob.I % GN_UP == 0 &&
-         s.blob.d % (2 * KS_UP) == 0 && s.blob.I % (2 * KS_DOWN) == 0;   // K loops take stages in pairs
+         s.blob.d % 128 == 0 && s.blob.I % 64 == 0;   // whole column tiles and K stages
 }
 
-int grouped_row_tiles(int rows) { return (rows + GM - 1) / GM; }
+int grouped_row_tiles(int rows) { return (rows + kRB - 1) / kRB; }
 
 namespace {
 // the buffer loads address x, h and an expert's weights by 32-bit byte offsets below kOutOfRange
@@ -379,7 +446,8 @@ bool offsets_fit(const FfnShape& s, int n_tok, int k) {
   const uint64_t lim = kOutOfRange;
   const uint64_t d = s.blob.d, I = s.blob.I;
   return n_tok >= 1 && k >= 1 && static_cast<uint64_t>(n_tok) * d * 2 < lim &&
-         static_cast<uint64_t>(n_tok) * k * I * 2 < lim && 2 * I * d * 2 < lim;
+         static_cast<uint64_t>(n_tok) * k * I * 2 < lim && 2 * I * d * 2 < lim &&
+         static_cast<uint64_t>(n_tok) * (k + 1) * d * 4 < lim;
 }
 }  // namespace
 
@@ -399,16 +467,29 @@ hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t*
   return hipGetLastError();
 }
 
+namespace {
+int compute_units() {
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        n > 0)
+      cus = n;
+    else
+      cus = 256;
+  }
+  return cus;
+}
+}  // namespace
+
 hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const void* x, int n_tok,
                                  const int32_t* perm, int k, void* hs, hipStream_t st, const LaunchTiming& tm) {
   if (b.n_groups <= 0) return hipSuccess;
   if (b.n_groups > kMaxGroups || !grouped_supported(s, 0) || !offsets_fit(s, n_tok, k)) return hipErrorInvalidValue;
-  const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.I / GN_UP);
+  const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.I / 64);
   const uint32_t x_bytes = static_cast<uint32_t>(n_tok) * s.blob.d * 2;
-  auto* kern = s.blob.d == 2 * KS_UP ? grouped_gateup_kernel<KS_UP, true> : grouped_gateup_kernel<KS_UP, false>;
-  hipExtLaunchKernelGGL(kern, dim3(tiles), dim3(256), 0, st, tm.start, tm.stop, 0, b,
-                        static_cast<const uint16_t*>(x), x_bytes, perm, k, s.blob.d, s.blob.I,
-                        static_cast<uint16_t*>(hs));
+  hipExtLaunchKernelGGL(grouped_kernel<MODE_UP>, dim3(std::min(tiles, compute_units())), dim3(512), 0, st, tm.start,
+                        tm.stop, 0, b, static_cast<const uint16_t*>(x), x_bytes, perm, k, s.blob.d, s.blob.I, hs);
   return hipGetLastError();
 }
 
@@ -416,11 +497,11 @@ hipError_t launch_grouped_down(const GroupedBatch& b, const FfnShape& s, const v
                                int k, float* buf, hipStream_t st, const LaunchTiming& tm) {
   if (b.n_groups <= 0) return hipSuccess;
   if (b.n_groups > kMaxGroups || !grouped_supported(s, 0) || !offsets_fit(s, n_tok, k)) return hipErrorInvalidValue;
-  const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.d / GN_DOWN);
+  const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.d / 128);
   const uint32_t hs_bytes = static_cast<uint32_t>(n_tok) * k * s.blob.I * 2;
-  auto* kern = s.blob.I == 2 * KS_DOWN ? grouped_down_kernel<KS_DOWN, true> : grouped_down_kernel<KS_DOWN, false>;
-  hipExtLaunchKernelGGL(kern, dim3(tiles), dim3(256), 0, st, tm.start, tm.stop, 0, b,
-                        static_cast<const uint16_t*>(hs), hs_bytes, perm, k, s.blob.d, s.blob.I, buf);
+  hipExtLaunchKernelGGL(grouped_kernel<MODE_DN>, dim3(std::min(tiles, compute_units())), dim3(512), 0, st, tm.start,
+                        tm.stop, 0, b, static_cast<const uint16_t*>(hs), hs_bytes, perm, k, s.blob.d, s.blob.I,
+                        static_cast<void*>(buf));
   return hipGetLastError();
 }
 

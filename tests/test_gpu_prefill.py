@@ -27,11 +27,20 @@ def test_prefill_qwen3_shape_reduced():
 
 
 def test_prefill_multi_tile_ragged():
-    # several 64-row tiles per expert with ragged last tiles, a ragged 16-token router tile
-    # (520 = 32 * 16 + 8), and small caps (16 experts, C = 5 -> four chunks)
+    # ~130 rows per expert (five 32-row slabs, the last ragged), K of two stages in the down GEMM (a
+    # tile shorter than the prefetch distance), a ragged 16-token router tile (520 = 32 * 16 + 8), and
+    # small caps (16 experts, C = 5 -> four chunks)
     wl = WORKLOADS["qwen3-30b-a3b-prefill"].with_(L=2, T=520, d=256, I=128, N=16, k=4)
     out = run_case(wl, 5, 1, check_all_outputs=True, expect_grouped=True)
     assert out["chunks"].min() >= 4
+
+
+def test_prefill_experts_beyond_one_row_block():
+    # ~260 rows per expert (8 experts, top-2 of 1040 tokens): an expert of more than 256 rows takes two
+    # row blocks, each reading the expert's weights
+    wl = WORKLOADS["qwen3-30b-a3b-prefill"].with_(L=2, T=1040, d=256, I=128, N=8, k=2)
+    out = run_case(wl, 3, 1, check_all_outputs=True, expect_grouped=True)
+    assert out["chunks"].min() >= 3
 
 
 def test_prefill_below_grouped_threshold():
