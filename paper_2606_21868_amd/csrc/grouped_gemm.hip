@@ -134,7 +134,7 @@ __global__ void __launch_bounds__(1024) permute_scatter_kernel(const int32_t* __
 // the K stages of all its tiles form one sequence, so the loads of the next tile's first stages are
 // in flight while the current tile finishes (no pipeline start per tile).
 //
-// Weights (B operand: 128 weight rows x 64 K per stage, 16 KB) go from HBM straight into a ring of
+// Weights (B operand: 256 weight rows x 64 K per stage, 32 KB) go from HBM straight into a ring of
 // kNB LDS slots by buffer-to-LDS loads (buffer_load_dwordx4 ... lds), kNB - 1 stages ahead, so the
 // bytes in flight do not occupy registers.  Inside a slot, 16-byte chunk c of weight row r sits at
 // position c ^ swz(r), which keeps the fragment reads free of bank conflicts.  The token rows (A
@@ -145,17 +145,20 @@ __global__ void __launch_bounds__(1024) permute_scatter_kernel(const int32_t* __
 // make the LDS reads wait for every buffer-to-LDS load in flight); the workgroup barrier is a plain
 // s_barrier after an explicit wait for this stage's loads.
 //
-// Tiles: 64 h columns (W1 and W3 rows c0 .. c0 + 63, so SwiGLU is applied in registers) for gate/up,
-// 128 output columns (W2 rows) for down, each over up to kRB = 256 rows of one expert: all of them at
+// Tiles: 128 h columns (W1 and W3 rows c0 .. c0 + 127, so SwiGLU is applied in registers) for gate/up,
+// 256 output columns (W2 rows) for down, each over up to kRB = 256 rows of one expert: all of them at
 // the routing's usual ~T k / N rows per expert, so each weight byte is read once and rows are padded
-// only to the 32-row slab of a wave.
+// only to the 32-row slab of a wave.  The wide tiles halve how often an expert's token rows are
+// re-read (once per column tile) and how many tile ends there are.
 // ------------------------------------------------------------------------------------------
 constexpr int kRB = 256;                 // rows per row block: 8 slabs of 32, one per wave
 constexpr int kGW = 8;                   // waves per workgroup
 constexpr int kKS = 64;                  // K per stage
-constexpr int kNB = 4;                   // LDS ring slots; loads run kNB - 1 stages ahead
+constexpr int kNB = 3;                   // LDS ring slots; loads run kNB - 1 stages ahead
 constexpr int kD = kNB - 1;
-constexpr int kSlot = 128 * kKS * 2;     // bytes per slot: 128 weight rows x 64 K, bf16
+constexpr int kBR = 256;                 // weight rows per tile (gate/up: 128 W1 + 128 W3 rows)
+constexpr int kCB = kBR / 32;            // 32-column blocks per tile
+constexpr int kSlot = kBR * kKS * 2;     // bytes per slot: 256 weight rows x 64 K, bf16
 constexpr int kBI = kSlot / 1024 / kGW;  // buffer-to-LDS loads per wave per stage (1 KB each)
 constexpr int kAI = kKS / 16;            // A fragment loads per wave per stage (16 B per lane each)
 constexpr int MODE_UP = 0, MODE_DN = 1;
@@ -185,27 +188,24 @@ __device__ __forceinline__ Tile decode_tile(const GroupedBatch& gb, int T, int n
     else hi = mid;
   }
   const int rb = rb_all - (lo > 0 ? gb.tile_end[lo - 1] : 0);
-  return Tile{gb.w[lo], gb.rows[lo], gb.row_off[lo], rb * kRB, ct * (MODE == MODE_UP ? 64 : 128)};
+  return Tile{gb.w[lo], gb.rows[lo], gb.row_off[lo], rb * kRB, ct * (MODE == MODE_UP ? kBR / 2 : kBR)};
 }
 
-// Eight weight fragments of one slot (two 16-steps x four 32-column blocks), read by inline ds_reads:
-// f[kk][cb] for 16-step kk0 + kk.  IMM = the slot's byte offset + 0 (the four column blocks are 4 KB
-// apart); addr0/addr1 = the lane's offsets of its row and chunk for the two 16-steps.
-template <int IMM>
-__device__ __forceinline__ void read_frags(u32x4_t (&f)[2][4], uint32_t addr0, uint32_t addr1) {
+// The eight weight fragments (32-column blocks, 4 KB apart) of one 16-step of a slot, read by inline
+// ds_reads from the lane's address in the slot.
+__device__ __forceinline__ void read_frags(u32x4_t (&f)[kCB], uint32_t addr) {
   asm volatile(
-      "ds_read_b128 %0, %8 offset:%10\n\t"
-      "ds_read_b128 %1, %8 offset:%11\n\t"
-      "ds_read_b128 %2, %8 offset:%12\n\t"
-      "ds_read_b128 %3, %8 offset:%13\n\t"
-      "ds_read_b128 %4, %9 offset:%10\n\t"
-      "ds_read_b128 %5, %9 offset:%11\n\t"
-      "ds_read_b128 %6, %9 offset:%12\n\t"
-      "ds_read_b128 %7, %9 offset:%13\n\t"
+      "ds_read_b128 %0, %8\n\t"
+      "ds_read_b128 %1, %8 offset:4096\n\t"
+      "ds_read_b128 %2, %8 offset:8192\n\t"
+      "ds_read_b128 %3, %8 offset:12288\n\t"
+      "ds_read_b128 %4, %8 offset:16384\n\t"
+      "ds_read_b128 %5, %8 offset:20480\n\t"
+      "ds_read_b128 %6, %8 offset:24576\n\t"
+      "ds_read_b128 %7, %8 offset:28672\n\t"
       "s_waitcnt lgkmcnt(0)"
-      : "=&v"(f[0][0]), "=&v"(f[0][1]), "=&v"(f[0][2]), "=&v"(f[0][3]), "=&v"(f[1][0]), "=&v"(f[1][1]), "=&v"(f[1][2]),
-        "=&v"(f[1][3])
-      : "v"(addr0), "v"(addr1), "i"(IMM), "i"(IMM + 4096), "i"(IMM + 8192), "i"(IMM + 12288)
+      : "=&v"(f[0]), "=&v"(f[1]), "=&v"(f[2]), "=&v"(f[3]), "=&v"(f[4]), "=&v"(f[5]), "=&v"(f[6]), "=&v"(f[7])
+      : "v"(addr)
       : "memory");
 }
 
@@ -256,7 +256,7 @@ __global__ void __launch_bounds__(512) grouped_kernel(GroupedBatch gb, const uin
   __shared__ __attribute__((aligned(1024))) uint8_t ring[kNB * kSlot];
   const int K = MODE == MODE_UP ? d : I;             // reduction length
   const int spt = K / kKS;                           // stages per tile
-  const int n_ct = MODE == MODE_UP ? I / 64 : d / 128;
+  const int n_ct = MODE == MODE_UP ? I / (kBR / 2) : d / kBR;
   const int n_tiles = gb.tile_end[gb.n_groups - 1] * n_ct;
   // XCD-aware: workgroups are dealt to the 8 XCDs round-robin, and the workgroups of one XCD take
   // consecutive logical indices, so at any time they work on consecutive tiles (the column tiles of
@@ -271,12 +271,13 @@ __global__ void __launch_bounds__(512) grouped_kernel(GroupedBatch gb, const uin
   const uint32_t arow = static_cast<uint32_t>(K) * 2;   // bytes per A row (x: d, h: I)
 
   // buffer-to-LDS pattern: slot position p = (wave kBI + i) 64 + lane holds chunk (p & 7) ^ swz(row)
-  // of weight row p >> 3 (gate/up: rows 0..63 are W1 rows c0.., 64..127 the W3 rows of the same columns)
+  // of weight row p >> 3 (gate/up: rows 0..127 are W1 rows c0.., 128..255 the W3 rows of the same
+  // columns)
   uint32_t bpat[kBI];
 #pragma unroll
   for (int i = 0; i < kBI; ++i) {
     const int pp = (wave * kBI + i) * 64 + lane, r = pp >> 3, c = (pp & 7) ^ swz(r);
-    const int wr = MODE == MODE_UP ? (r < 64 ? r : I - 64 + r) : r;
+    const int wr = MODE == MODE_UP ? (r < kBR / 2 ? r : I - kBR / 2 + r) : r;
     bpat[i] = static_cast<uint32_t>(wr) * wrow + c * 16;
   }
   // fragment reads: lane l reads weight row 32 cb + l % 32, chunk 2 kk + l / 32 of the 16-step pair
@@ -333,7 +334,7 @@ __global__ void __launch_bounds__(512) grouped_kernel(GroupedBatch gb, const uin
   // the compute cursor
   int cs_tile = 0, cs_s = 0;
   Tile ct = decode_tile<MODE>(gb, L, n_ct);
-  f32x16_t acc[4] = {};
+  f32x16_t acc[kCB] = {};
   int32_t pq = 0;   // down: the pair of this lane's row in the compute cursor's tile
   if constexpr (MODE == MODE_UP) {
     pn = pair_of(ct);
@@ -348,14 +349,14 @@ __global__ void __launch_bounds__(512) grouped_kernel(GroupedBatch gb, const uin
     if constexpr (MODE == MODE_UP) {
       uint16_t* hs = static_cast<uint16_t*>(out);
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
+      for (int cb = 0; cb < kCB / 2; ++cb) {
         const int col = ct.c0 + cb * 32 + lr;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int i = (r >> 2) * 8 + hb * 4 + (r & 3);
           if (i < n_rows) {
             const float a = acc[cb][r];
-            const float h = a / (1.0f + __expf(-a)) * acc[cb + 2][r];
+            const float h = a / (1.0f + __expf(-a)) * acc[cb + kCB / 2][r];
             hs[static_cast<size_t>(ct.base + ct.m0 + wave * 32 + i) * I + col] = bf16_rne(h);
           }
         }
@@ -371,7 +372,7 @@ __global__ void __launch_bounds__(512) grouped_kernel(GroupedBatch gb, const uin
         if (i < n_rows) {
           const size_t orow = static_cast<size_t>(p / k) * (k + 1) + (p % k);
 #pragma unroll
-          for (int cb = 0; cb < 4; ++cb) buf[orow * d + ct.c0 + cb * 32 + lr] = acc[cb][r];
+          for (int cb = 0; cb < kCB; ++cb) buf[orow * d + ct.c0 + cb * 32 + lr] = acc[cb][r];
         }
       }
     }
@@ -399,24 +400,19 @@ __global__ void __launch_bounds__(512) grouped_kernel(GroupedBatch gb, const uin
     if (is_tile * spt + is_s < nq) issue((U + kD) % kNB, A[(U + kD) % kNB]);
     if (wave * 32 < ct.rows - ct.m0) {   // the wave's slab has rows in this tile
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        u32x4_t f[2][4];
-        // the slot's offset goes into the instruction's 16-bit offset field as far as it fits
-        constexpr uint32_t hi = static_cast<uint32_t>(U / 4) * 4 * kSlot;
-        read_frags<(U % 4) * kSlot>(f, fo[2 * h2] + hi, fo[2 * h2 + 1] + hi);
+      for (int kk = 0; kk < 4; ++kk) {
+        u32x4_t f[kCB];
+        read_frags(f, fo[kk] + U * kSlot);
+        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, A[U][kk]);
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, A[U][2 * h2 + kk]);
-#pragma unroll
-          for (int cb = 0; cb < 4; ++cb)
-            acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, f[kk][cb]), acc[cb], 0, 0, 0);
-        }
+        for (int cb = 0; cb < kCB; ++cb)
+          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, f[cb]), acc[cb], 0, 0, 0);
       }
     }
     if (++cs_s == spt) {
       epilogue();
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) acc[cb] = f32x16_t{};
+      for (int cb = 0; cb < kCB; ++cb) acc[cb] = f32x16_t{};
       cs_s = 0;
       if (++cs_tile < my_tiles) {
         ct = decode_tile<MODE>(gb, L + cs_tile * G, n_ct);
@@ -435,7 +431,7 @@ __global__ void __launch_bounds__(512) grouped_kernel(GroupedBatch gb, const uin
 
 bool grouped_supported(const FfnShape& s, int has_shared) {
   return !has_shared && s.blob.w_dtype == DT_BF16 && s.x_dtype == DT_BF16 && s.h_dtype == DT_BF16 &&
-         s.blob.d % 128 == 0 && s.blob.I % 64 == 0;   // whole column tiles and K stages
+         s.blob.d % kBR == 0 && s.blob.I % (kBR / 2) == 0;   // whole column tiles and K stages
 }
 
 int grouped_row_tiles(int rows) { return (rows + kRB - 1) / kRB; }
@@ -486,7 +482,7 @@ hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const
                                  const int32_t* perm, int k, void* hs, hipStream_t st, const LaunchTiming& tm) {
   if (b.n_groups <= 0) return hipSuccess;
   if (b.n_groups > kMaxGroups || !grouped_supported(s, 0) || !offsets_fit(s, n_tok, k)) return hipErrorInvalidValue;
-  const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.I / 64);
+  const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.I / (kBR / 2));
   const uint32_t x_bytes = static_cast<uint32_t>(n_tok) * s.blob.d * 2;
   hipExtLaunchKernelGGL(grouped_kernel<MODE_UP>, dim3(std::min(tiles, compute_units())), dim3(512), 0, st, tm.start,
                         tm.stop, 0, b, static_cast<const uint16_t*>(x), x_bytes, perm, k, s.blob.d, s.blob.I, hs);
@@ -497,7 +493,7 @@ hipError_t launch_grouped_down(const GroupedBatch& b, const FfnShape& s, const v
                                int k, float* buf, hipStream_t st, const LaunchTiming& tm) {
   if (b.n_groups <= 0) return hipSuccess;
   if (b.n_groups > kMaxGroups || !grouped_supported(s, 0) || !offsets_fit(s, n_tok, k)) return hipErrorInvalidValue;
-  const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.d / 128);
+  const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.d / kBR);
   const uint32_t hs_bytes = static_cast<uint32_t>(n_tok) * k * s.blob.I * 2;
   hipExtLaunchKernelGGL(grouped_kernel<MODE_DN>, dim3(std::min(tiles, compute_units())), dim3(512), 0, st, tm.start,
                         tm.stop, 0, b, static_cast<const uint16_t*>(hs), hs_bytes, perm, k, s.blob.d, s.blob.I,
