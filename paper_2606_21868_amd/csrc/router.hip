@@ -164,17 +164,24 @@ __global__ void __launch_bounds__(256) router_logits_split_kernel(const float* _
         }
   };
   const int steps = ks / 16;   // a multiple of PF or below it (ks = d / n_split, d % 16 == 0)
+  // the first PF steps' loads, unconditional like every other load (a step past the slice loads the
+  // slice's last columns again, never used)
 #pragma unroll
-  for (int j = 0; j < PF; ++j)
-    if (j < steps) load(j, 16 * j);
-  for (int j0 = 0; j0 < steps; j0 += PF) {
+  for (int j = 0; j < PF; ++j) load(j, 16 * min(j, steps - 1));
+  // every step but the last PF loads the step PF ahead, with no branch around the loads (a load
+  // behind a branch makes the compiler wait for every load in flight before the next step's work)
+  int j0 = 0;
+  for (; j0 + PF < steps; j0 += PF) {
 #pragma unroll
     for (int j = 0; j < PF; ++j) {
-      if (j0 + j >= steps) break;
       mma(j);
-      if (j0 + j + PF < steps) load(j, 16 * (j0 + j + PF));
+      load(j, 16 * (j0 + j + PF));
+      __builtin_amdgcn_sched_barrier(0);   // keeps the scheduler from moving later steps above the loads
     }
   }
+#pragma unroll
+  for (int j = 0; j < PF; ++j)
+    if (j0 + j < steps) mma(j);
   float* out = partial + static_cast<size_t>(q) * T * N;
 #pragma unroll
   for (int b = 0; b < RB; ++b) {
@@ -279,10 +286,10 @@ hipError_t launch_router_logits(const float* wr, const void* x, int x_dtype, int
     return hipGetLastError();
   }
   if (N % 16 == 0 && N <= 256 && d % 16 == 0) {
-    // enough (token block, column slice) workgroups to cover the chip, at most kRouterMaxSplit slices
+    // enough (token block, column slice) workgroups to give every CU one, at most kRouterMaxSplit slices
     const int tiles = (T + 63) / 64;
     int S = 1;
-    while (2 * S <= kRouterMaxSplit && tiles * S < 256 && d % (32 * S) == 0 &&
+    while (2 * S <= kRouterMaxSplit && 2 * tiles * S <= 256 && d % (32 * S) == 0 &&
            ((d / (2 * S)) / 16 % 4 == 0 || (d / (2 * S)) / 16 < 4))
       S *= 2;
     *n_split = S;
