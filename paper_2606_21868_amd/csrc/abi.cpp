@@ -69,7 +69,8 @@ struct LayerState {
   std::vector<hipEvent_t> chunk_ev;
   bool pending = false;
   int32_t T = 0;
-  std::vector<int32_t> ids;
+  std::vector<int32_t> ids;          // the routed ids, or (from_counts) the distinct experts
+  bool from_counts = false;          // paged in from the device's per-expert pair counts
   StepPlan plan;
   std::vector<std::vector<const uint8_t*>> chunk_ptrs;
   wisp_page_stats cum{};
@@ -103,6 +104,8 @@ struct wisp_ctx {
   void* h = nullptr;
   float* buf = nullptr;
   uint64_t* idx_tagged = nullptr;    // host-coherent (seq << 32 | id) words written by the router
+  uint64_t* cnt_tagged = nullptr;    // host-coherent (seq << 32 | pairs) words, one per expert
+  std::vector<int32_t> batch_cnt;    // a token batch's pairs per expert, from cnt_tagged
   uint32_t route_seq = 0;
   int32_t profile_mask = 0;          // kernel classes timed when profiling
   std::vector<int32_t> ids_scratch;
@@ -320,6 +323,7 @@ void free_ctx(wisp_ctx* c) {
   if (c->h) hipFree(c->h);
   if (c->buf) hipFree(c->buf);
   if (c->idx_tagged) hipHostFree(c->idx_tagged);
+  if (c->cnt_tagged) hipHostFree(c->cnt_tagged);
   if (c->ids_up) hipHostFree(c->ids_up);
   if (c->d_ids) hipFree(c->d_ids);
   if (c->d_perm) hipFree(c->d_perm);
@@ -705,6 +709,11 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
     return bail(WISP_E_NOMEM, "pinned scratch");
   c->idx_tagged = static_cast<uint64_t*>(p);
   std::memset(c->idx_tagged, 0, sizeof(uint64_t) * static_cast<size_t>(T) * k);
+  if (hipHostMalloc(&p, sizeof(uint64_t) * N, hipHostMallocCoherent) != hipSuccess)
+    return bail(WISP_E_NOMEM, "pinned scratch");
+  c->cnt_tagged = static_cast<uint64_t*>(p);
+  std::memset(c->cnt_tagged, 0, sizeof(uint64_t) * N);
+  c->batch_cnt.assign(N, 0);
   c->ids_scratch.resize(static_cast<size_t>(T) * k);
   const size_t pairs_bytes = sizeof(int32_t) * static_cast<size_t>(T) * k;
   if (hipHostMalloc(&p, pairs_bytes, hipHostMallocDefault) != hipSuccess) return bail(WISP_E_NOMEM, "pinned scratch");
@@ -951,6 +960,40 @@ wisp_status wisp_set_pager(wisp_ctx* ctx, int32_t pager) {
   return WISP_OK;
 }
 
+namespace {
+// The router launches of a layer-step: logits and selection (one launch for T <= 4 with fusion on).
+// With idx_tagged, the selection also writes each id to host-coherent memory as a word tagged seq.
+wisp_status route_kernels(wisp_ctx* ctx, LayerState& L, const void* x_dev, int32_t T, int32_t* idx_dev, float* w_dev,
+                          uint64_t* idx_tagged, uint32_t seq, hipStream_t st) {
+  const auto& d = ctx->desc;
+  if (ctx->fusion && T <= 4) {
+    // logits and selection in one launch (the first workgroup selects once every row is published)
+    LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
+    WISP_HIP(launch_route_select(L.wr, x_dev, d.x_dtype, d.d_model, ctx->d_logit_tags, next_logit_tag(ctx),
+                                 T, d.n_experts,
+                                 d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev, w_dev, idx_tagged, seq, st, t1),
+             "router logits + select launch");
+    timing_end(ctx, t1, WISP_K_ROUTER_SELECT,
+               static_cast<uint64_t>(d.n_experts) * d.d_model * 4 + static_cast<uint64_t>(T) * d.d_model * ctx->x_elem());
+  } else {
+    LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_LOGITS);
+    int n_split = 1;
+    WISP_HIP(launch_router_logits(L.wr, x_dev, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, &n_split, st, t1),
+             "router logits launch");
+    timing_end(ctx, t1, WISP_K_ROUTER_LOGITS,
+               static_cast<uint64_t>(d.n_experts) * d.d_model * 4 +
+                   static_cast<uint64_t>(T) * d.d_model * ctx->x_elem() + static_cast<uint64_t>(T) * d.n_experts * 4);
+    LaunchTiming t2 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
+    WISP_HIP(launch_router_select(ctx->logits, n_split, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev,
+                                  w_dev, idx_tagged, seq, st, t2),
+             "router select launch");
+    timing_end(ctx, t2, WISP_K_ROUTER_SELECT,
+               static_cast<uint64_t>(T) * d.n_experts * 4 + static_cast<uint64_t>(T) * d.top_k * 8);
+  }
+  return WISP_OK;
+}
+}  // namespace
+
 wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int32_t T, int32_t* idx_dev,
                             float* w_dev, int32_t* idx_host, void* stream) {
   wisp_status s = check_ctx(ctx);
@@ -967,31 +1010,8 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
   // queue's start latency was ≈10 µs of every token batch's layer-step)
   const bool publish = idx_host != nullptr;
   const uint32_t seq = publish ? ++ctx->route_seq : 0;
-  if (ctx->fusion && T <= 4) {
-    // logits and selection in one launch (the first workgroup selects once every row is published)
-    LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
-    WISP_HIP(launch_route_select(L.wr, x_dev, d.x_dtype, d.d_model, ctx->d_logit_tags, next_logit_tag(ctx),
-                                 T, d.n_experts,
-                                 d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev, w_dev,
-                                 publish ? ctx->idx_tagged : nullptr, seq, st, t1),
-             "router logits + select launch");
-    timing_end(ctx, t1, WISP_K_ROUTER_SELECT,
-               static_cast<uint64_t>(d.n_experts) * d.d_model * 4 + static_cast<uint64_t>(T) * d.d_model * ctx->x_elem());
-  } else {
-    LaunchTiming t1 = timing_begin(ctx, WISP_K_ROUTER_LOGITS);
-    int n_split = 1;
-    WISP_HIP(launch_router_logits(L.wr, x_dev, d.x_dtype, T, d.n_experts, d.d_model, ctx->logits, &n_split, st, t1),
-             "router logits launch");
-    timing_end(ctx, t1, WISP_K_ROUTER_LOGITS,
-               static_cast<uint64_t>(d.n_experts) * d.d_model * 4 +
-                   static_cast<uint64_t>(T) * d.d_model * ctx->x_elem() + static_cast<uint64_t>(T) * d.n_experts * 4);
-    LaunchTiming t2 = timing_begin(ctx, WISP_K_ROUTER_SELECT);
-    WISP_HIP(launch_router_select(ctx->logits, n_split, T, d.n_experts, d.top_k, d.route, d.n_groups, d.topk_groups, idx_dev,
-                                  w_dev, publish ? ctx->idx_tagged : nullptr, seq, st, t2),
-             "router select launch");
-    timing_end(ctx, t2, WISP_K_ROUTER_SELECT,
-               static_cast<uint64_t>(T) * d.n_experts * 4 + static_cast<uint64_t>(T) * d.top_k * 8);
-  }
+  if ((s = route_kernels(ctx, L, x_dev, T, idx_dev, w_dev, publish ? ctx->idx_tagged : nullptr, seq, st)) != WISP_OK)
+    return s;
   if (publish) {
     const int n = T * d.top_k;
     // a token batch for the grouped FFN: its pairs are ordered by expert now, from the device ids,
@@ -1032,17 +1052,14 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
   return WISP_OK;
 }
 
-wisp_status wisp_page_in(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, int32_t T, wisp_page_stats* st) {
-  wisp_status s = check_ctx(ctx);
-  if (s != WISP_OK) return s;
-  if ((s = check_layer(ctx, layer)) != WISP_OK) return s;
-  if (!ids_host) return fail(WISP_E_INVAL, "ids_host is NULL");
-  if (T < 1 || T > ctx->desc.max_tokens) return fail(WISP_E_INVAL, "T out of [1, max_tokens]");
-  if (ctx->cap < 1) return fail(WISP_E_STATE, "no expert budget set");
-  if (ctx->pager == WISP_PAGER_DEVICE) return fail(WISP_E_STATE, "the device pager pages inside wisp_decode_step");
+namespace {
+// Algorithm 1 for one layer-step over the n ids (the routed ids, or the distinct experts of a token
+// batch whose counts came from the device: the step depends only on the set of ids), then the fills
+// of its first chunk.
+wisp_status page_in_ids(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, int32_t n, int32_t T, bool from_counts,
+                        wisp_page_stats* st) {
+  wisp_status s = WISP_OK;
   LayerState& L = ctx->layers[layer];
-  if (L.pending) return fail(WISP_E_STATE, "previous page-in of this layer not consumed by wisp_moe_forward");
-  const int32_t n = T * ctx->desc.top_k;
   if (!L.pf_unused.empty()) {
     // the prefetch bookkeeping indexes by id: validate first (otherwise the slot table's step validates
     // every id before it changes anything)
@@ -1060,6 +1077,7 @@ wisp_status wisp_page_in(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, 
   }
   if (!L.table->step(ids_host, n, &L.plan)) return fail(WISP_E_INVAL, "expert id out of range");
   L.ids.assign(ids_host, ids_host + n);
+  L.from_counts = from_counts;
   L.T = T;
   const size_t nch = L.plan.chunks.size();
   if ((s = ensure_events(L.fill_ev, nch)) != WISP_OK) return s;
@@ -1087,6 +1105,20 @@ wisp_status wisp_page_in(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, 
   return WISP_OK;
 }
 
+}  // namespace
+
+wisp_status wisp_page_in(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, int32_t T, wisp_page_stats* st) {
+  wisp_status s = check_ctx(ctx);
+  if (s != WISP_OK) return s;
+  if ((s = check_layer(ctx, layer)) != WISP_OK) return s;
+  if (!ids_host) return fail(WISP_E_INVAL, "ids_host is NULL");
+  if (T < 1 || T > ctx->desc.max_tokens) return fail(WISP_E_INVAL, "T out of [1, max_tokens]");
+  if (ctx->cap < 1) return fail(WISP_E_STATE, "no expert budget set");
+  if (ctx->pager == WISP_PAGER_DEVICE) return fail(WISP_E_STATE, "the device pager pages inside wisp_decode_step");
+  if (ctx->layers[layer].pending) return fail(WISP_E_STATE, "previous page-in of this layer not consumed by wisp_moe_forward");
+  return page_in_ids(ctx, layer, ids_host, T * ctx->desc.top_k, T, false, st);
+}
+
 wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, int32_t T, const float* w_dev,
                              float* y_dev, void* stream, wisp_page_stats* st) {
   wisp_status s = check_ctx(ctx);
@@ -1106,11 +1138,17 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
   // pairs per expert, and the pairs in (expert, pair) order
   std::vector<int32_t>& cnt = ctx->e_cnt;
   std::vector<int32_t>& off = ctx->e_off;
-  std::fill(cnt.begin(), cnt.end(), 0);
-  for (int32_t p = 0; p < n_pairs; ++p) ++cnt[L.ids[p]];
+  if (L.from_counts) {
+    cnt = ctx->batch_cnt;
+  } else {
+    std::fill(cnt.begin(), cnt.end(), 0);
+    for (int32_t p = 0; p < n_pairs; ++p) ++cnt[L.ids[p]];
+  }
   off[0] = 0;
   for (int e = 0; e < N; ++e) off[e + 1] = off[e] + cnt[e];
   const bool grouped = T >= kGroupedMinTokens && grouped_supported(ctx->shape, ctx->desc.has_shared);
+  if (L.from_counts && (!grouped || ctx->perm_layer != layer || ctx->perm_T != T))
+    return fail(WISP_E_STATE, "a page-in from device counts needs its layer's device permutation");
   if (!grouped) {   // the per-item launches list their pairs; the grouped ones read the device order
     std::vector<int32_t> fill(off.begin(), off.end() - 1);
     for (int32_t p = 0; p < n_pairs; ++p) ctx->pair_order[fill[L.ids[p]]++] = p;
@@ -1135,8 +1173,10 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
   }
   if (grouped) {
     // the permutation wisp_route_topk computed for this layer, if it came from the ids paged in
+    // (a page-in from counts: the counts are the permutation's own)
     const bool early = ctx->perm_layer == layer && ctx->perm_T == T &&
-                       std::memcmp(ctx->perm_ids.data(), L.ids.data(), sizeof(int32_t) * n_pairs) == 0;
+                       (L.from_counts ||
+                        std::memcmp(ctx->perm_ids.data(), L.ids.data(), sizeof(int32_t) * n_pairs) == 0);
     ctx->perm_layer = -1;   // used once; the launches below overwrite it otherwise
     if (ctx->perm_ev_recorded) WISP_HIP(hipStreamWaitEvent(sm, ctx->perm_ev, 0), "hipStreamWaitEvent(perm)");
     if (!early) {
@@ -1286,6 +1326,61 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
   return WISP_OK;
 }
 
+namespace {
+// Routing and page-in of a token batch for the grouped FFN with the ids left on the device: the
+// permutation kernel, which orders the pairs by expert right after the selection, hands every
+// expert's pair count to the host as a word tagged with this call's sequence number (host-coherent
+// memory).  The host pages in the experts with pairs (Algorithm 1 depends only on that set) and
+// sizes the grouped launches from the counts, so it reads N words instead of T * k ids and does no
+// per-pair work.
+wisp_status route_page_batch(wisp_ctx* ctx, int32_t layer, const void* x_dev, int32_t T, int32_t* idx_dev,
+                             float* w_dev, hipStream_t st, wisp_page_stats* ps) {
+  wisp_status s = WISP_OK;
+  LayerState& L = ctx->layers[layer];
+  if (!L.wr) return fail(WISP_E_STATE, "router weights not set for this layer");
+  if (L.pending) return fail(WISP_E_STATE, "previous page-in of this layer not consumed by wisp_moe_forward");
+  const auto& d = ctx->desc;
+  const int N = d.n_experts, n = T * d.top_k;
+  const uint32_t seq = ++ctx->route_seq;
+  if ((s = route_kernels(ctx, L, x_dev, T, idx_dev, w_dev, nullptr, 0, st)) != WISP_OK) return s;
+  ctx->perm_layer = -1;
+  if (ctx->perm_use_recorded) WISP_HIP(hipStreamWaitEvent(st, ctx->perm_use_ev, 0), "hipStreamWaitEvent(perm use)");
+  LaunchTiming tp = timing_begin(ctx, WISP_K_PERMUTE);
+  WISP_HIP(launch_permute_pairs(idx_dev, n, N, ctx->d_perm, ctx->d_perm_counts, st, tp, ctx->cnt_tagged, seq),
+           "permute launch");
+  timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(n) * 8);
+  WISP_HIP(hipEventRecord(ctx->perm_ev, st), "hipEventRecord(perm)");
+  ctx->perm_ev_recorded = true;
+  // spin until every count carries this call's tag
+  std::vector<int32_t>& R = ctx->ids_scratch;   // the experts with pairs, ascending
+  R.clear();
+  uint64_t spins = 0;
+  int32_t total = 0;
+  for (int e = 0; e < N; ++e) {
+    uint64_t v;
+    while (((v = __atomic_load_n(ctx->cnt_tagged + e, __ATOMIC_ACQUIRE)) >> 32) != seq) {
+      __builtin_ia32_pause();
+      if ((++spins & 0xFFFFF) == 0) {
+        hipError_t q = hipStreamQuery(st);
+        if (q != hipSuccess && q != hipErrorNotReady)
+          return fail(WISP_E_HIP, std::string("router stream: ") + hipGetErrorString(q));
+        if (q == hipSuccess && (__atomic_load_n(ctx->cnt_tagged + e, __ATOMIC_ACQUIRE) >> 32) != seq)
+          return fail(WISP_E_HIP, "permutation finished without publishing its counts");
+      }
+    }
+    const int32_t c = static_cast<int32_t>(v & 0xFFFFFFFFu);
+    ctx->batch_cnt[e] = c;
+    total += c;
+    if (c > 0) R.push_back(e);
+  }
+  if (total != n) return fail(WISP_E_HIP, "expert counts do not add up to the routed pairs");
+  ctx->perm_layer = layer;
+  ctx->perm_T = T;
+  if (ctx->profiling) harvest(ctx, false);
+  return page_in_ids(ctx, layer, R.data(), static_cast<int32_t>(R.size()), T, true, ps);
+}
+}  // namespace
+
 wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_t* idx_dev, float* w_dev,
                              float* y_dev, void* stream, wisp_page_stats* st) {
   wisp_status s = check_ctx(ctx);
@@ -1372,12 +1467,24 @@ wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_
     }
     return WISP_OK;
   }
+  // a token batch for the grouped FFN pages in from the device's per-expert counts (no prefetch
+  // bookkeeping needs its ids)
+  const bool batch_counts = T >= kGroupedMinTokens && grouped_supported(ctx->shape, d.has_shared) &&
+                            ctx->pf_mode == WISP_PREFETCH_OFF && ctx->cap >= 1;
   for (int32_t l = 0; l < d.n_layers; ++l) {
     const void* xl = static_cast<const uint8_t*>(x_dev) + l * xs;
     int32_t* il = idx_dev + static_cast<size_t>(l) * T * d.top_k;
     float* wl = w_dev + static_cast<size_t>(l) * T * d.top_k;
     float* yl = y_dev + static_cast<size_t>(l) * T * d.d_model;
     if ((s = prefetch_before_route(ctx, l)) != WISP_OK) return s;
+    if (batch_counts) {
+      if ((s = check_layer(ctx, l)) != WISP_OK) return s;
+      if ((s = route_page_batch(ctx, l, xl, T, il, wl, static_cast<hipStream_t>(stream), st ? st + l : nullptr)) !=
+          WISP_OK)
+        return s;
+      if ((s = wisp_moe_forward(ctx, l, xl, T, wl, yl, stream, nullptr)) != WISP_OK) return s;
+      continue;
+    }
     if ((s = wisp_route_topk(ctx, l, xl, T, il, wl, ctx->ids_scratch.data(), stream)) != WISP_OK) return s;
     if (ctx->pf_mode == WISP_PREFETCH_PREDICTOR &&
         (s = wisp_predictor_observe(ctx->pf_pred, l, ctx->ids_scratch.data(), T * d.top_k)) != WISP_OK)

@@ -71,7 +71,8 @@ __global__ void __launch_bounds__(256) permute_count_kernel(const int32_t* __res
 
 __global__ void __launch_bounds__(1024) permute_scatter_kernel(const int32_t* __restrict__ idx, int P, int N,
                                                                const int32_t* __restrict__ counts, int n_seg,
-                                                               int32_t* __restrict__ perm) {
+                                                               int32_t* __restrict__ perm,
+                                                               uint64_t* __restrict__ totals, uint32_t seq) {
   __shared__ int32_t cnt[16][256];
   __shared__ int32_t base[256];
   __shared__ int32_t wsum[4];
@@ -88,6 +89,11 @@ __global__ void __launch_bounds__(1024) permute_scatter_kernel(const int32_t* __
       tot += c;
       before += q < seg ? c : 0;
     }
+    // the first segment's workgroup hands every expert's pair count to the host: one word per
+    // expert with the call's sequence number above the count, by one atomic store
+    if (totals && seg == 0)
+      __hip_atomic_store(totals + tid, (static_cast<uint64_t>(seq) << 32) | static_cast<uint32_t>(tot),
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
   // exclusive scan of the totals over experts: an inclusive scan per wave (threads 0..255), then the
   // totals of the waves before
@@ -450,7 +456,7 @@ bool offsets_fit(const FfnShape& s, int n_tok, int k) {
 int permute_segments(int n_pairs) { return (n_pairs + kPermSeg - 1) / kPermSeg; }
 
 hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t* perm, int32_t* counts, hipStream_t st,
-                                const LaunchTiming& tm) {
+                                const LaunchTiming& tm, uint64_t* totals, uint32_t seq) {
   if (n_pairs <= 0) return hipSuccess;
   if (N < 1 || N > 256) return hipErrorInvalidValue;
   const int n_seg = permute_segments(n_pairs);
@@ -459,7 +465,7 @@ hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t*
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(permute_scatter_kernel, dim3(n_seg), dim3(1024), 0, st, nullptr, tm.stop, 0, idx, n_pairs, N,
-                        counts, n_seg, perm);
+                        counts, n_seg, perm, totals, seq);
   return hipGetLastError();
 }
 

@@ -107,10 +107,11 @@ struct GroupedBatch {
 bool grouped_supported(const FfnShape& s, int has_shared);
 int grouped_row_tiles(int rows);
 // perm[off_e + i] = the i-th pair (ascending) routed to expert e; off_e = pairs of experts < e.
-// counts: device scratch of permute_segments(n_pairs) * N int32.
+// counts: device scratch of permute_segments(n_pairs) * N int32.  If totals is not NULL (N words of
+// host-coherent memory), totals[e] = seq << 32 | pairs routed to e, each written by one atomic store.
 int permute_segments(int n_pairs);
 hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t* perm, int32_t* counts, hipStream_t st,
-                                const LaunchTiming& tm);
+                                const LaunchTiming& tm, uint64_t* totals = nullptr, uint32_t seq = 0);
 // hs[row] = bf16(silu(W1 x[t]) * (W3 x[t])) for every row of the batch's experts (row in sorted order);
 // x holds n_tok token rows, hs n_tok * k pair rows.
 hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const void* x, int n_tok,
