@@ -106,3 +106,39 @@ def test_prefill_layer_calls_in_any_order():
             log(f"  {order}: bit-identical to wisp_decode_step")
     finally:
         run.close()
+
+
+def test_prefill_counts_page_in_matches_ids_page_in():
+    """wisp_decode_step pages a token batch in from the device's per-expert pair counts; the public
+    route / page-in / forward sequence pages in from the routed ids.  From the same cold tables and
+    with a budget below the union (chunked Algorithm 1 steps, faults in every layer), both make the
+    same decisions (hits, misses, chunks per layer) and give the same output bits."""
+    wl = WORKLOADS["qwen3-30b-a3b-prefill"].with_(L=2, T=64, d=256, I=128, N=16, k=4)
+    log(f"[case] counts page-in against ids page-in {wl.name} L={wl.L} T={wl.T} N={wl.N} C=6")
+    run = wisp.DecodeRun(wl, device=0, steps=1)
+    try:
+        run.generate()
+        assert run.set_cap(6) == 6
+        run.ctx.masters_ready()                       # cold tables
+        ref = run.decode(record=True, steps=1)
+        assert (ref["chunks"] > 1).all() and (ref["misses"] > 0).all()
+        T, L, k = wl.T, wl.L, wl.k
+        run.ctx.masters_ready()                       # cold tables again
+        idx = torch.zeros((L, T, k), dtype=torch.int32, device=run.dev)
+        w = torch.zeros((L, T, k), dtype=torch.float32, device=run.dev)
+        y = torch.zeros((L, T, wl.d), dtype=torch.float32, device=run.dev)
+        ids = [np.zeros(T * k, np.int32) for _ in range(L)]
+        torch.cuda.synchronize(run.dev)
+        for l in range(L):
+            run.ctx.route_topk(l, run.x_dev[0, l], T, idx[l], w[l], ids[l], run.stream)
+            st = run.ctx.page_in(l, ids[l], T)
+            assert (st["hits"], st["misses"], st["chunks"]) == \
+                (ref["hits"][0, l], ref["misses"][0, l], ref["chunks"][0, l]), l
+            run.ctx.moe_forward(l, run.x_dev[0, l], T, w[l], y[l], run.stream)
+        run.stream.synchronize()
+        assert np.array_equal(idx.cpu().numpy(), ref["idx"][0])
+        assert np.array_equal(y.cpu().numpy().view(np.uint32), ref["y"][0].view(np.uint32))
+        log(f"  misses per layer {ref['misses'][0].tolist()}, chunks {ref['chunks'][0].tolist()}: same decisions and bits")
+    finally:
+        run.close()
+
