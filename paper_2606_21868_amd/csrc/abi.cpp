@@ -106,6 +106,7 @@ struct wisp_ctx {
   uint64_t* idx_tagged = nullptr;    // host-coherent (seq << 32 | id) words written by the router
   uint64_t* cnt_tagged = nullptr;    // host-coherent (seq << 32 | pairs) words, one per expert
   std::vector<int32_t> batch_cnt;    // a token batch's pairs per expert, from cnt_tagged
+  std::vector<int32_t> batch_set;    // the experts with pairs, ascending
   uint32_t route_seq = 0;
   int32_t profile_mask = 0;          // kernel classes timed when profiling
   std::vector<int32_t> ids_scratch;
@@ -714,6 +715,7 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
   c->cnt_tagged = static_cast<uint64_t*>(p);
   std::memset(c->cnt_tagged, 0, sizeof(uint64_t) * N);
   c->batch_cnt.assign(N, 0);
+  c->batch_set.reserve(N);
   c->ids_scratch.resize(static_cast<size_t>(T) * k);
   const size_t pairs_bytes = sizeof(int32_t) * static_cast<size_t>(T) * k;
   if (hipHostMalloc(&p, pairs_bytes, hipHostMallocDefault) != hipSuccess) return bail(WISP_E_NOMEM, "pinned scratch");
@@ -1352,7 +1354,7 @@ wisp_status route_page_batch(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
   WISP_HIP(hipEventRecord(ctx->perm_ev, st), "hipEventRecord(perm)");
   ctx->perm_ev_recorded = true;
   // spin until every count carries this call's tag
-  std::vector<int32_t>& R = ctx->ids_scratch;   // the experts with pairs, ascending
+  std::vector<int32_t>& R = ctx->batch_set;
   R.clear();
   uint64_t spins = 0;
   int32_t total = 0;
