@@ -1223,8 +1223,10 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
       timing_end(ctx, t1, WISP_K_GROUPED_GATEUP, ng * 2 * dI * B.elem + nrows * (B.d + B.I) * 2,
                  nrows * 2 * 2 * dI);
       LaunchTiming t2 = timing_begin(ctx, WISP_K_GROUPED_DOWN);
-      WISP_HIP(launch_grouped_down(gb, ctx->shape, ctx->h, T, ctx->d_perm, k, ctx->buf, sm, t2), "grouped down launch");
-      timing_end(ctx, t2, WISP_K_GROUPED_DOWN, ng * dI * B.elem + nrows * (B.I * 2 + B.d * 4), nrows * 2 * dI);
+      WISP_HIP(launch_grouped_down(gb, ctx->shape, ctx->h, T, ctx->d_perm, k, reinterpret_cast<uint16_t*>(ctx->buf), sm,
+                                   t2),
+               "grouped down launch");
+      timing_end(ctx, t2, WISP_K_GROUPED_DOWN, ng * dI * B.elem + nrows * (B.I * 2 + B.d * 2), nrows * 2 * dI);
     }
     return WISP_OK;
   };
@@ -1303,7 +1305,14 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
     }
     if (ci + 1 < nch) WISP_HIP(hipEventRecord(L.chunk_ev[ci], sm), "hipEventRecord(chunk)");
   }
-  if (!fused) {
+  if (grouped) {   // the grouped GEMMs leave bf16 expert outputs (no shared expert on this path)
+    LaunchTiming tc = timing_begin(ctx, WISP_K_COMBINE);
+    WISP_HIP(launch_combine_bf16(T, k, ctx->desc.d_model, w_dev, reinterpret_cast<const uint16_t*>(ctx->buf), y_dev, sm,
+                                 tc),
+             "combine launch");
+    timing_end(ctx, tc, WISP_K_COMBINE,
+               static_cast<uint64_t>(T) * ctx->desc.d_model * (2 * k + 4) + static_cast<uint64_t>(T) * k * 4);
+  } else if (!fused) {
     LaunchTiming tc = timing_begin(ctx, WISP_K_COMBINE);
     WISP_HIP(launch_combine(T, k, ctx->desc.d_model, ctx->desc.has_shared, w_dev, ctx->buf, y_dev, sm, tc),
              "combine launch");

@@ -368,7 +368,7 @@ __global__ void __launch_bounds__(512) grouped_kernel(GroupedBatch gb, const uin
         }
       }
     } else {
-      float* buf = static_cast<float*>(out);
+      uint16_t* buf = static_cast<uint16_t*>(out);
       if (short_k) __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
       pin_i32(pq);
 #pragma unroll
@@ -378,7 +378,7 @@ __global__ void __launch_bounds__(512) grouped_kernel(GroupedBatch gb, const uin
         if (i < n_rows) {
           const size_t orow = static_cast<size_t>(p / k) * (k + 1) + (p % k);
 #pragma unroll
-          for (int cb = 0; cb < kCB; ++cb) buf[orow * d + ct.c0 + cb * 32 + lr] = acc[cb][r];
+          for (int cb = 0; cb < kCB; ++cb) buf[orow * d + ct.c0 + cb * 32 + lr] = bf16_rne(acc[cb][r]);
         }
       }
     }
@@ -496,7 +496,7 @@ hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const
 }
 
 hipError_t launch_grouped_down(const GroupedBatch& b, const FfnShape& s, const void* hs, int n_tok, const int32_t* perm,
-                               int k, float* buf, hipStream_t st, const LaunchTiming& tm) {
+                               int k, uint16_t* buf, hipStream_t st, const LaunchTiming& tm) {
   if (b.n_groups <= 0) return hipSuccess;
   if (b.n_groups > kMaxGroups || !grouped_supported(s, 0) || !offsets_fit(s, n_tok, k)) return hipErrorInvalidValue;
   const int tiles = b.tile_end[b.n_groups - 1] * (s.blob.d / kBR);

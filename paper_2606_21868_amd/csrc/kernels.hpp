@@ -90,6 +90,9 @@ bool ffn_dev_supported(const FfnShape& s, int T, int k, int has_shared);
 // y[t] = sum_j w[t, j] buf[t*(k+1)+j] (j ascending) + (shared ? buf[t*(k+1)+k] : 0).
 hipError_t launch_combine(int T, int k, int d, int has_shared, const float* w, const float* buf, float* y,
                           hipStream_t st, const LaunchTiming& tm);
+// The same sum over bf16 expert outputs (the grouped GEMMs' rows; no shared expert).
+hipError_t launch_combine_bf16(int T, int k, int d, const float* w, const uint16_t* buf, float* y, hipStream_t st,
+                               const LaunchTiming& tm);
 
 // Token batches (prefill): grouped GEMMs on the matrix cores over slot-indirected experts.
 // The (token, rank) pairs p = t*k + j are ordered by expert (stable); expert g of a launch owns
@@ -116,9 +119,10 @@ hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t*
 // x holds n_tok token rows, hs n_tok * k pair rows.
 hipError_t launch_grouped_gateup(const GroupedBatch& b, const FfnShape& s, const void* x, int n_tok,
                                  const int32_t* perm, int k, void* hs, hipStream_t st, const LaunchTiming& tm);
-// buf[t*(k+1)+j] = W2 hs[row] for the pair p = t*k+j of every row.
+// buf[t*(k+1)+j] = bf16(W2 hs[row]) for the pair p = t*k+j of every row (bf16, as h is: the combine
+// reads half the bytes).
 hipError_t launch_grouped_down(const GroupedBatch& b, const FfnShape& s, const void* hs, int n_tok, const int32_t* perm,
-                               int k, float* buf, hipStream_t st, const LaunchTiming& tm);
+                               int k, uint16_t* buf, hipStream_t st, const LaunchTiming& tm);
 
 // Router: logits[t, e] = W_r[e] . x[t] (fp32 accumulate), written as *n_split partial sums over column
 // slices (slice s at logits + s * T * N; 1 for decode sizes, at most kRouterMaxSplit), which the
