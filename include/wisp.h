@@ -171,7 +171,11 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
 
 /* One decode step over all layers in order (route, page-in, forward per layer): x_dev [L, T, d],
  * idx_dev [L, T, k], w_dev [L, T, k], y_dev [L, T, d].  Layer l+1 is routed only after layer l's
- * FFN has been issued.  st (optional) receives [L] per-layer counts. */
+ * FFN has been issued.  st (optional) receives [L] per-layer counts.  With the host pager, a token
+ * batch that takes the grouped FFN (and no prefetch mode) keeps its ids on the device: the kernel
+ * that orders its pairs by expert hands each expert's pair count to the host, which pages in the
+ * set of experts with pairs (Algorithm 1 depends only on that set) and sizes the grouped launches
+ * from the counts; decisions and outputs are those of the route / page-in / forward calls. */
 wisp_status wisp_decode_step(wisp_ctx* ctx, const void* x_dev, int32_t T, int32_t* idx_dev, float* w_dev,
                              float* y_dev, void* stream, wisp_page_stats* st);
 
