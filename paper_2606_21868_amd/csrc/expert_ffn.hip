@@ -171,8 +171,9 @@ __device__ __forceinline__ void rows_body(const FfnItem& it, const uint8_t* rd, 
   // the weights, and no LDS staging or barrier is needed.  Other items stage their input rows in
   // LDS.  The multiply-add sequence is the same either way.
   constexpr int XQ = NLT > 0 ? EPL * IS / 16 : 1;          // 16-byte input chunks per weight chunk
-  const bool xreg = NLT > 0 && ntok == 1;
-  uint4 xr[NLT > 0 ? NLT * XQ : 1];
+  constexpr bool kXreg = NLT > 0 && !(WT == DT_FP8 && NLT > 4);
+  const bool xreg = kXreg && ntok == 1;
+  uint4 xr[kXreg ? NLT * XQ : 1];
   const int rbase0 = r_begin + wave * RPW;
   const uint8_t* xrow = vin + static_cast<size_t>(MODE == MODE_GATEUP ? it.tok[0] : it.out[0]) * vin_stride * IS;
   if (!xreg) {
