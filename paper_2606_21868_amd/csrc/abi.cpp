@@ -129,6 +129,7 @@ struct wisp_ctx {
   hipEvent_t perm_ev = nullptr;      // the last early permutation is done
   hipEvent_t perm_use_ev = nullptr;  // the last grouped launches that read d_perm are done
   bool perm_ev_recorded = false, perm_use_recorded = false;
+  hipStream_t perm_stream = nullptr; // the stream the last early permutation was enqueued on
   int32_t perm_layer = -1, perm_T = 0;
   std::vector<int32_t> perm_ids;     // the ids the early permutation was computed from
   std::vector<int32_t> e_cnt, e_off; // pairs per expert and their first sorted row
@@ -1027,6 +1028,7 @@ wisp_status wisp_route_topk(wisp_ctx* ctx, int32_t layer, const void* x_dev, int
       timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(n) * 8);
       WISP_HIP(hipEventRecord(ctx->perm_ev, st), "hipEventRecord(perm)");
       ctx->perm_ev_recorded = true;
+      ctx->perm_stream = st;
     }
     // spin until every entry carries this call's tag: the wait on the critical path of a layer-step
     uint64_t spins = 0;
@@ -1180,7 +1182,9 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
                        (L.from_counts ||
                         std::memcmp(ctx->perm_ids.data(), L.ids.data(), sizeof(int32_t) * n_pairs) == 0);
     ctx->perm_layer = -1;   // used once; the launches below overwrite it otherwise
-    if (ctx->perm_ev_recorded) WISP_HIP(hipStreamWaitEvent(sm, ctx->perm_ev, 0), "hipStreamWaitEvent(perm)");
+    // (on the permutation's own stream the launches below are ordered after it already)
+    if (ctx->perm_ev_recorded && !(early && sm == ctx->perm_stream))
+      WISP_HIP(hipStreamWaitEvent(sm, ctx->perm_ev, 0), "hipStreamWaitEvent(perm)");
     if (!early) {
       // the ids go to the device; the permutation kernel orders the pairs by expert there
       if (ctx->ids_ev_recorded) WISP_HIP(hipEventSynchronize(ctx->ids_ev), "hipEventSynchronize(ids)");
@@ -1362,6 +1366,7 @@ wisp_status route_page_batch(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
   timing_end(ctx, tp, WISP_K_PERMUTE, static_cast<uint64_t>(n) * 8);
   WISP_HIP(hipEventRecord(ctx->perm_ev, st), "hipEventRecord(perm)");
   ctx->perm_ev_recorded = true;
+  ctx->perm_stream = st;
   // spin until every count carries this call's tag
   std::vector<int32_t>& R = ctx->batch_set;
   R.clear();

@@ -40,9 +40,10 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
   return static_cast<uint16_t>(u >> 16);
 }
 
-// Stable counting sort of the pairs p = t*k + j by expert id idx[p], in two launches over segments of
-// kPermSeg pairs: permute_count_kernel counts each expert in each segment; permute_scatter_kernel (a
-// workgroup of 16 waves per segment, 64 pairs per wave) places every pair at
+// Stable counting sort of the pairs p = t*k + j by expert id idx[p] over segments of kPermSeg pairs:
+// the count of each expert in each segment (permute_count_kernel, or, while those counts fit in LDS,
+// every workgroup of the scatter kernel for itself from all the ids, so the sort is one launch); then
+// permute_scatter_kernel (a workgroup of 16 waves per segment, 64 pairs per wave) places every pair at
 //   (pairs of smaller experts) + (pairs of its expert in earlier segments)
 //   + (pairs of its expert in earlier waves of its segment) + (earlier lanes of its wave with that expert),
 // the last found by matching lanes with equal ids through eight ballots over the id bits.  The result
@@ -69,6 +70,9 @@ __global__ void __launch_bounds__(256) permute_count_kernel(const int32_t* __res
   if (tid < N) counts[seg * N + tid] = h[tid];
 }
 
+constexpr int kPermFusedCounts = 8192;   // segments x experts counted in LDS by the one-launch sort
+
+template <bool FUSED>
 __global__ void __launch_bounds__(1024) permute_scatter_kernel(const int32_t* __restrict__ idx, int P, int N,
                                                                const int32_t* __restrict__ counts, int n_seg,
                                                                int32_t* __restrict__ perm,
@@ -76,16 +80,34 @@ __global__ void __launch_bounds__(1024) permute_scatter_kernel(const int32_t* __
   __shared__ int32_t cnt[16][256];
   __shared__ int32_t base[256];
   __shared__ int32_t wsum[4];
+  extern __shared__ int32_t hist[];   // FUSED: [n_seg][N] counts
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, seg = blockIdx.x;
   const int p = seg * kPermSeg + wave * 64 + lane;
   const bool valid = p < P;
   const int e = valid ? idx[p] : 0;
   for (int i = tid; i < 16 * 256; i += 1024) (&cnt[0][0])[i] = 0;
+  if constexpr (FUSED) {
+    // every pair once into its segment's count of its expert (integer adds: the same counts in any order)
+    for (int i = tid; i < n_seg * N; i += 1024) hist[i] = 0;
+    __syncthreads();
+    for (int q0 = 0; q0 < P; q0 += 4 * 1024) {
+      int ev[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {   // the loads go out together
+        const int q = q0 + u * 1024 + tid;
+        ev[u] = q < P ? idx[q] : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (ev[u] >= 0) atomicAdd(&hist[((q0 + u * 1024 + tid) / kPermSeg) * N + ev[u]], 1);
+    }
+    __syncthreads();
+  }
   // per expert: all its pairs (for the offsets) and those in earlier segments
   int tot = 0, before = 0;
   if (tid < N) {
     for (int q = 0; q < n_seg; ++q) {
-      const int c = counts[q * N + tid];
+      const int c = FUSED ? hist[q * N + tid] : counts[q * N + tid];
       tot += c;
       before += q < seg ? c : 0;
     }
@@ -460,12 +482,18 @@ hipError_t launch_permute_pairs(const int32_t* idx, int n_pairs, int N, int32_t*
   if (n_pairs <= 0) return hipSuccess;
   if (N < 1 || N > 256) return hipErrorInvalidValue;
   const int n_seg = permute_segments(n_pairs);
+  if (n_seg * N <= kPermFusedCounts) {   // one launch: each workgroup counts all the ids in LDS
+    hipExtLaunchKernelGGL(permute_scatter_kernel<true>, dim3(n_seg), dim3(1024),
+                          static_cast<uint32_t>(sizeof(int32_t) * n_seg * N), st, tm.start, tm.stop, 0, idx, n_pairs,
+                          N, counts, n_seg, perm, totals, seq);
+    return hipGetLastError();
+  }
   hipExtLaunchKernelGGL(permute_count_kernel, dim3(n_seg), dim3(256), 0, st, tm.start, nullptr, 0, idx, n_pairs, N,
                         counts);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipExtLaunchKernelGGL(permute_scatter_kernel, dim3(n_seg), dim3(1024), 0, st, nullptr, tm.stop, 0, idx, n_pairs, N,
-                        counts, n_seg, perm, totals, seq);
+  hipExtLaunchKernelGGL(permute_scatter_kernel<false>, dim3(n_seg), dim3(1024), 0, st, nullptr, tm.stop, 0, idx,
+                        n_pairs, N, counts, n_seg, perm, totals, seq);
   return hipGetLastError();
 }
 
