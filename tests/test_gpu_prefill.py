@@ -43,6 +43,16 @@ def test_prefill_experts_beyond_one_row_block():
     assert out["chunks"].min() >= 3
 
 
+def test_prefill_pair_sort_in_two_launches():
+    # 4200 tokens x top-8 of 256 experts = 33,600 pairs in 33 segments: 33 x 256 segment counts exceed
+    # what the one-launch sort counts in LDS, so the counting launch runs first; ~131 rows per expert
+    wl = WORKLOADS["qwen3-30b-a3b-prefill"].with_(L=1, T=4200, d=256, I=128, N=256, k=8)
+    rng = np.random.default_rng(2)
+    tokens = np.sort(np.concatenate([[0, wl.T - 1], rng.choice(np.arange(1, wl.T - 1), 126, replace=False)]))
+    out = run_case(wl, 64, 1, sample_points=[(0, 0)], tokens=tokens, expect_grouped=True)
+    assert out["chunks"].min() >= 4
+
+
 def test_prefill_below_grouped_threshold():
     # a 12-token batch stays on the per-item GEMV path (one partial tile of the token-batch router)
     wl = WORKLOADS["qwen3-30b-a3b-prefill"].with_(L=2, T=12, d=256, I=128, N=16, k=4)
