@@ -165,7 +165,10 @@ wisp_status wisp_page_in(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, 
  * slot, then y_t = sum_j w_dev[t,j] o_tj in rank order (+ the shared expert's output).  Experts
  * that were resident start at once; faulted ones wait for their fill.  x_dev [T, d], w_dev [T, k]
  * fp32, y_dev [T, d] fp32, on `stream`.  Returns WISP_E_NOT_RESIDENT if a routed expert is not
- * resident (exactness invariant, Sec. 3.2).  st (optional) receives the step's counts. */
+ * resident (exactness invariant, Sec. 3.2).  st (optional) receives the step's counts.  Precision:
+ * fp32 accumulation; with bf16 or fp8 weights h is rounded to bf16, and token batches of 16 or more
+ * tokens on the grouped matrix-core GEMMs (bf16 weights) also round each o_tj to bf16 before the
+ * combine (single-token and small batches keep o_tj in fp32). */
 wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, int32_t T, const float* w_dev,
                              float* y_dev, void* stream, wisp_page_stats* st);
 
