@@ -214,7 +214,7 @@ void harvest(wisp_ctx* c, bool wait) {
   size_t keep = 0;
   for (size_t i = 0; i < c->timed.size(); ++i) {
     TimedPair& p = c->timed[i];
-    if (wait) hipEventSynchronize(p.b);
+    if (wait) (void)hipEventSynchronize(p.b);
     if (hipEventQuery(p.b) != hipSuccess) {
       c->timed[keep++] = p;
       continue;
@@ -286,59 +286,59 @@ wisp_status check_layer(wisp_ctx* c, int32_t l) {
 
 void free_offload(wisp_ctx* c) {
   auto& o = c->off;
-  if (c->side) hipStreamSynchronize(c->side);
+  if (c->side) (void)hipStreamSynchronize(c->side);
   for (int b = 0; b < 2; ++b) {
-    if (o.used_rec[b]) hipEventSynchronize(o.used[b]);
-    if (o.staging[b]) hipFree(o.staging[b]);
-    if (o.filled[b]) hipEventDestroy(o.filled[b]);
-    if (o.used[b]) hipEventDestroy(o.used[b]);
+    if (o.used_rec[b]) (void)hipEventSynchronize(o.used[b]);
+    if (o.staging[b]) (void)hipFree(o.staging[b]);
+    if (o.filled[b]) (void)hipEventDestroy(o.filled[b]);
+    if (o.used[b]) (void)hipEventDestroy(o.used[b]);
   }
-  if (o.resident) hipFree(o.resident);
+  if (o.resident) (void)hipFree(o.resident);
   o = wisp_ctx::Offload{};
 }
 
 void free_ctx(wisp_ctx* c) {
   if (!c) return;
   free_offload(c);
-  if (c->side) hipStreamSynchronize(c->side);
+  if (c->side) (void)hipStreamSynchronize(c->side);
   for (auto& L : c->layers) {
-    if (L.use_ev_recorded) hipEventSynchronize(L.use_ev);
+    if (L.use_ev_recorded) (void)hipEventSynchronize(L.use_ev);
   }
-  hipDeviceSynchronize();
+  (void)hipDeviceSynchronize();
   for (auto& L : c->layers) {
-    for (auto* p : L.slot_mem) if (p) hipFree(p);
-    if (L.shared_dev) hipFree(L.shared_dev);
-    if (L.use_ev) hipEventDestroy(L.use_ev);
-    if (L.pf_ev) hipEventDestroy(L.pf_ev);
-    for (auto e : L.fill_ev) hipEventDestroy(e);
-    for (auto e : L.chunk_ev) hipEventDestroy(e);
+    for (auto* p : L.slot_mem) if (p) (void)hipFree(p);
+    if (L.shared_dev) (void)hipFree(L.shared_dev);
+    if (L.use_ev) (void)hipEventDestroy(L.use_ev);
+    if (L.pf_ev) (void)hipEventDestroy(L.pf_ev);
+    for (auto e : L.fill_ev) (void)hipEventDestroy(e);
+    for (auto e : L.chunk_ev) (void)hipEventDestroy(e);
   }
   c->bounce.reset();
   for (auto* p : c->masters)
     if (p) c->pageable ? (void)munmap(p, c->master_map_bytes) : (void)hipHostFree(p);
   for (auto* p : c->shared_master)
     if (p) c->pageable ? (void)munmap(p, c->master_stride) : (void)hipHostFree(p);
-  for (auto& t : c->timed) { hipEventDestroy(t.a); hipEventDestroy(t.b); }
-  for (auto e : c->ev_pool) hipEventDestroy(e);
-  if (c->side) hipStreamDestroy(c->side);
-  if (c->logits) hipFree(c->logits);
-  if (c->h) hipFree(c->h);
-  if (c->buf) hipFree(c->buf);
-  if (c->idx_tagged) hipHostFree(c->idx_tagged);
-  if (c->cnt_tagged) hipHostFree(c->cnt_tagged);
-  if (c->ids_up) hipHostFree(c->ids_up);
-  if (c->d_ids) hipFree(c->d_ids);
-  if (c->d_perm) hipFree(c->d_perm);
-  if (c->d_perm_counts) hipFree(c->d_perm_counts);
-  if (c->ids_ev) hipEventDestroy(c->ids_ev);
-  if (c->perm_ev) hipEventDestroy(c->perm_ev);
-  if (c->perm_use_ev) hipEventDestroy(c->perm_use_ev);
+  for (auto& t : c->timed) { (void)hipEventDestroy(t.a); (void)hipEventDestroy(t.b); }
+  for (auto e : c->ev_pool) (void)hipEventDestroy(e);
+  if (c->side) (void)hipStreamDestroy(c->side);
+  if (c->logits) (void)hipFree(c->logits);
+  if (c->h) (void)hipFree(c->h);
+  if (c->buf) (void)hipFree(c->buf);
+  if (c->idx_tagged) (void)hipHostFree(c->idx_tagged);
+  if (c->cnt_tagged) (void)hipHostFree(c->cnt_tagged);
+  if (c->ids_up) (void)hipHostFree(c->ids_up);
+  if (c->d_ids) (void)hipFree(c->d_ids);
+  if (c->d_perm) (void)hipFree(c->d_perm);
+  if (c->d_perm_counts) (void)hipFree(c->d_perm_counts);
+  if (c->ids_ev) (void)hipEventDestroy(c->ids_ev);
+  if (c->perm_ev) (void)hipEventDestroy(c->perm_ev);
+  if (c->perm_use_ev) (void)hipEventDestroy(c->perm_use_ev);
   for (void* p : {static_cast<void*>(c->d_pi), static_cast<void*>(c->d_pinv), static_cast<void*>(c->d_tau),
                   static_cast<void*>(c->d_clock), static_cast<void*>(c->d_slot_ptr), static_cast<void*>(c->d_plan),
                   static_cast<void*>(c->d_stats)})
-    if (p) hipFree(p);
-  if (c->h_stats) hipHostFree(c->h_stats);
-  if (c->d_logit_tags) hipFree(c->d_logit_tags);
+    if (p) (void)hipFree(p);
+  if (c->h_stats) (void)hipHostFree(c->h_stats);
+  if (c->d_logit_tags) (void)hipFree(c->d_logit_tags);
   delete c;
 }
 
@@ -370,7 +370,7 @@ wisp_status upload_tables(wisp_ctx* c) {
   if (c->dev_cap != C) {
     for (void** p : {reinterpret_cast<void**>(&c->d_pinv), reinterpret_cast<void**>(&c->d_tau),
                      reinterpret_cast<void**>(&c->d_slot_ptr)}) {
-      if (*p) hipFree(*p);
+      if (*p) (void)hipFree(*p);
       *p = nullptr;
     }
     c->dev_cap = 0;
@@ -748,7 +748,7 @@ wisp_status wisp_create(const wisp_model_desc* desc, wisp_ctx** out) {
 
 wisp_status wisp_destroy(wisp_ctx* ctx) {
   if (!ctx) return fail(WISP_E_INVAL, "ctx is NULL");
-  hipSetDevice(ctx->device);
+  (void)hipSetDevice(ctx->device);
   free_ctx(ctx);
   return WISP_OK;
 }
@@ -828,7 +828,7 @@ static wisp_status set_budget_host(wisp_ctx* ctx, uint64_t expert_bytes, int32_t
         if (hipMalloc(&p, ctx->blob.bytes) != hipSuccess) {
           ok = false;
           why = "hipMalloc of an expert slot failed";
-          hipGetLastError();
+          (void)hipGetLastError();
           break;
         }
         fresh[l].push_back(static_cast<uint8_t*>(p));
@@ -836,7 +836,7 @@ static wisp_status set_budget_host(wisp_ctx* ctx, uint64_t expert_bytes, int32_t
     }
     if (!ok) {
       for (auto& v : fresh)
-        for (auto* p : v) hipFree(p);
+        for (auto* p : v) (void)hipFree(p);
       return fail(WISP_E_NOMEM, why + "; previous budget kept");
     }
     for (int l = 0; l < nl; ++l) {
@@ -867,7 +867,7 @@ static wisp_status set_budget_host(wisp_ctx* ctx, uint64_t expert_bytes, int32_t
         used[spare] = 1;
       }
       for (int32_t s2 = 0; s2 < old; ++s2)
-        if (!used[s2]) hipFree(L.slot_mem[s2]);
+        if (!used[s2]) (void)hipFree(L.slot_mem[s2]);
       L.slot_mem.swap(mem);
     }
   }
@@ -1844,7 +1844,7 @@ wisp_status wisp_probe_h2d_engine(wisp_ctx* ctx, int32_t count, int32_t reps, in
   void* scratch = nullptr;
   const size_t B = ctx->blob.bytes;
   if (hipMalloc(&scratch, B * count) != hipSuccess) {
-    hipGetLastError();
+    (void)hipGetLastError();
     return fail(WISP_E_NOMEM, "probe scratch allocation failed");
   }
   hipEvent_t a = nullptr, b = nullptr;
@@ -1883,9 +1883,9 @@ wisp_status wisp_probe_h2d_engine(wisp_ctx* ctx, int32_t count, int32_t reps, in
     if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
     if (e == hipSuccess) rates.push_back(static_cast<double>(B) * count / (ms * 1e-3) / 1e9);
   }
-  if (a) hipEventDestroy(a);
-  if (b) hipEventDestroy(b);
-  hipFree(scratch);
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  (void)hipFree(scratch);
   if (e != hipSuccess) return fail(WISP_E_HIP, std::string("probe: ") + hipGetErrorString(e));
   std::sort(rates.begin(), rates.end());
   *gbps = rates[rates.size() / 2];
@@ -1908,8 +1908,8 @@ wisp_status wisp_probe_hbm_read(uint64_t bytes, int32_t launches, double* us_per
   void* buf = nullptr;
   uint32_t* sink = nullptr;
   if (hipMalloc(&buf, nwin * bytes) != hipSuccess || hipMalloc(reinterpret_cast<void**>(&sink), 256) != hipSuccess) {
-    hipGetLastError();
-    if (buf) hipFree(buf);
+    (void)hipGetLastError();
+    if (buf) (void)hipFree(buf);
     return fail(WISP_E_NOMEM, "read probe allocation failed");
   }
   hipStream_t st = nullptr;
@@ -1928,12 +1928,12 @@ wisp_status wisp_probe_hbm_read(uint64_t bytes, int32_t launches, double* us_per
   if (e == hipSuccess) e = hipEventSynchronize(b);
   float ms = 0.f;
   if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
-  if (st) hipStreamSynchronize(st);
-  if (a) hipEventDestroy(a);
-  if (b) hipEventDestroy(b);
-  if (st) hipStreamDestroy(st);
-  hipFree(sink);
-  hipFree(buf);
+  if (st) (void)hipStreamSynchronize(st);
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  if (st) (void)hipStreamDestroy(st);
+  (void)hipFree(sink);
+  (void)hipFree(buf);
   if (e != hipSuccess) return fail(WISP_E_HIP, std::string("read probe: ") + hipGetErrorString(e));
   *us_per_launch = static_cast<double>(ms) * 1e3 / launches;
   return WISP_OK;
@@ -1948,7 +1948,7 @@ wisp_status wisp_probe_mfma(int32_t launches, double* tflops) {
   const int wgs = cus * 8, iters = 2048;   // eight waves per SIMD, ≈1 ms per launch
   float* sink = nullptr;
   if (hipMalloc(reinterpret_cast<void**>(&sink), 256) != hipSuccess) {
-    hipGetLastError();
+    (void)hipGetLastError();
     return fail(WISP_E_NOMEM, "probe sink allocation failed");
   }
   hipStream_t st = nullptr;
@@ -1963,11 +1963,11 @@ wisp_status wisp_probe_mfma(int32_t launches, double* tflops) {
   if (e == hipSuccess) e = hipEventSynchronize(b);
   float ms = 0.f;
   if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
-  if (st) hipStreamSynchronize(st);
-  if (a) hipEventDestroy(a);
-  if (b) hipEventDestroy(b);
-  if (st) hipStreamDestroy(st);
-  hipFree(sink);
+  if (st) (void)hipStreamSynchronize(st);
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  if (st) (void)hipStreamDestroy(st);
+  (void)hipFree(sink);
   if (e != hipSuccess) return fail(WISP_E_HIP, std::string("matrix-core probe: ") + hipGetErrorString(e));
   const double flops = static_cast<double>(launches) * wgs * 4 /* waves */ * iters * 4 /* chains */ * 2.0 * 32 * 32 * 16;
   *tflops = flops / (static_cast<double>(ms) * 1e-3) / 1e12;
