@@ -65,8 +65,9 @@ struct LayerState {
   uint8_t* shared_dev = nullptr;
   hipEvent_t use_ev = nullptr;
   bool use_ev_recorded = false;
-  std::vector<hipEvent_t> fill_ev;
-  std::vector<hipEvent_t> chunk_ev;
+  std::vector<hipEvent_t> fill_ev;   // [2 * chunk + half]: that half of the chunk's fills has landed
+  std::vector<hipEvent_t> chunk_ev;  // [2 * chunk + half]: the chunk's compute up to that half is done
+  std::vector<std::vector<uint8_t>> late;   // per chunk, per expert: a fault of the chunk's second half
   bool pending = false;
   int32_t T = 0;
   std::vector<int32_t> ids;          // the routed ids, or (from_counts) the distinct experts
@@ -487,28 +488,54 @@ wisp_status poison_slots(wisp_ctx* c, int32_t layer, const std::vector<std::pair
   return WISP_OK;
 }
 
+// The fills of chunk ci on the side stream, in two halves with an event each (fill_ev[2 ci + h]).
+// With several chunks in a layer-step, a fill waits only for the part of the previous chunk's compute
+// that read its victim slot: that chunk's hits and first half (chunk_ev[2 (ci - 1)]) or its second
+// half (chunk_ev[2 (ci - 1) + 1]).  Faults whose victim the previous chunk's second half read form
+// this chunk's second half; chunk 0 splits its faults in the middle.  The link then streams a
+// chunk's first half while the previous chunk's second half computes, instead of idling for the
+// previous chunk's whole compute.  A single chunk keeps every fault in the first half.
 wisp_status issue_fills(wisp_ctx* c, int32_t layer, size_t ci) {
   LayerState& L = c->layers[layer];
   const ChunkPlan& cp = L.plan.chunks[ci];
-  if (cp.n_faults == 0) return WISP_OK;
-  if (ci == 0) {
-    if (L.use_ev_recorded) WISP_HIP(hipStreamWaitEvent(c->side, L.use_ev, 0), "hipStreamWaitEvent(use)");
-  } else {
-    WISP_HIP(hipStreamWaitEvent(c->side, L.chunk_ev[ci - 1], 0), "hipStreamWaitEvent(chunk)");
+  const size_t nch = L.plan.chunks.size();
+  std::vector<uint8_t>& late = L.late[ci];
+  late.assign(cp.experts.size(), 0);
+  if (cp.n_faults == 0) return WISP_OK;   // nothing waits for this chunk's fill events
+  if (nch > 1 && ci == 0) {
+    int32_t nf = 0;
+    for (size_t i = 0; i < cp.experts.size(); ++i)
+      if (cp.fault[i]) late[i] = nf++ >= (cp.n_faults + 1) / 2 ? 1 : 0;
+  } else if (nch > 1) {
+    const ChunkPlan& pp = L.plan.chunks[ci - 1];
+    std::vector<uint8_t> read_late(static_cast<size_t>(c->cap), 0);
+    for (size_t i = 0; i < pp.experts.size(); ++i)
+      if (L.late[ci - 1][i]) read_late[pp.slots[i]] = 1;
+    for (size_t i = 0; i < cp.experts.size(); ++i)
+      if (cp.fault[i]) late[i] = read_late[cp.slots[i]];
   }
-  LaunchTiming tm = timing_begin(c, WISP_K_H2D_FILL);
-  if (tm.start) WISP_HIP(hipEventRecord(tm.start, c->side), "hipEventRecord");
-  std::vector<std::pair<int32_t, int32_t>> fills;
+  std::vector<std::pair<int32_t, int32_t>> fills[2];
   for (size_t i = 0; i < cp.experts.size(); ++i)
-    if (cp.fault[i]) fills.push_back({cp.experts[i], cp.slots[i]});
+    if (cp.fault[i]) fills[late[i]].push_back({cp.experts[i], cp.slots[i]});
   const bool batch = L.T >= kGroupedMinTokens && grouped_supported(c->shape, c->desc.has_shared);
-  wisp_status s = poison_slots(c, layer, fills);
-  if (s != WISP_OK) return s;
-  s = fill_slots(c, layer, fills, batch);
-  if (s != WISP_OK) return s;
-  if (tm.stop) WISP_HIP(hipEventRecord(tm.stop, c->side), "hipEventRecord");
-  timing_end(c, tm, WISP_K_H2D_FILL, static_cast<uint64_t>(cp.n_faults) * c->blob.bytes);
-  WISP_HIP(hipEventRecord(L.fill_ev[ci], c->side), "hipEventRecord(fill)");
+  for (int h = 0; h < 2; ++h) {
+    if (ci == 0) {
+      if (h == 0 && L.use_ev_recorded) WISP_HIP(hipStreamWaitEvent(c->side, L.use_ev, 0), "hipStreamWaitEvent(use)");
+    } else {
+      WISP_HIP(hipStreamWaitEvent(c->side, L.chunk_ev[2 * (ci - 1) + h], 0), "hipStreamWaitEvent(chunk)");
+    }
+    if (!fills[h].empty()) {
+      LaunchTiming tm = timing_begin(c, WISP_K_H2D_FILL);
+      if (tm.start) WISP_HIP(hipEventRecord(tm.start, c->side), "hipEventRecord");
+      wisp_status s = poison_slots(c, layer, fills[h]);
+      if (s != WISP_OK) return s;
+      s = fill_slots(c, layer, fills[h], batch);
+      if (s != WISP_OK) return s;
+      if (tm.stop) WISP_HIP(hipEventRecord(tm.stop, c->side), "hipEventRecord");
+      timing_end(c, tm, WISP_K_H2D_FILL, static_cast<uint64_t>(fills[h].size()) * c->blob.bytes);
+    }
+    WISP_HIP(hipEventRecord(L.fill_ev[2 * ci + h], c->side), "hipEventRecord(fill)");
+  }
   return WISP_OK;
 }
 
@@ -1084,8 +1111,9 @@ wisp_status page_in_ids(wisp_ctx* ctx, int32_t layer, const int32_t* ids_host, i
   L.from_counts = from_counts;
   L.T = T;
   const size_t nch = L.plan.chunks.size();
-  if ((s = ensure_events(L.fill_ev, nch)) != WISP_OK) return s;
-  if ((s = ensure_events(L.chunk_ev, nch)) != WISP_OK) return s;
+  if ((s = ensure_events(L.fill_ev, 2 * nch)) != WISP_OK) return s;
+  if ((s = ensure_events(L.chunk_ev, 2 * nch)) != WISP_OK) return s;
+  if (L.late.size() < nch) L.late.resize(nch);
   L.chunk_ptrs.assign(nch, {});
   for (size_t ci = 0; ci < nch; ++ci)
     for (int32_t sl : L.plan.chunks[ci].slots) L.chunk_ptrs[ci].push_back(L.slot_mem[sl]);
@@ -1282,19 +1310,23 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
   for (size_t ci = 0; ci < nch && !fused; ++ci) {
     const ChunkPlan& cp = L.plan.chunks[ci];
     if (ci > 0 && (s = issue_fills(ctx, layer, ci)) != WISP_OK) return s;
+    // the hits, then each half of the faults once its fills have landed (issue_fills)
     if (grouped) {
-      std::vector<std::pair<int32_t, const uint8_t*>> hits, faults;
+      std::vector<std::pair<int32_t, const uint8_t*>> hits, faults[2];
       for (size_t i = 0; i < cp.experts.size(); ++i)
-        (cp.fault[i] ? faults : hits).push_back({cp.experts[i], L.chunk_ptrs[ci][i]});
+        (cp.fault[i] ? faults[L.late[ci][i]] : hits).push_back({cp.experts[i], L.chunk_ptrs[ci][i]});
       if (!hits.empty() && (s = run_grouped(hits)) != WISP_OK) return s;
-      if (!faults.empty()) {
-        WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[ci], 0), "hipStreamWaitEvent(fill)");
-        if ((s = run_grouped(faults)) != WISP_OK) return s;
+      for (int h = 0; h < 2; ++h) {
+        if (!faults[h].empty()) {
+          WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[2 * ci + h], 0), "hipStreamWaitEvent(fill)");
+          if ((s = run_grouped(faults[h])) != WISP_OK) return s;
+        }
+        if (nch > 1) WISP_HIP(hipEventRecord(L.chunk_ev[2 * ci + h], sm), "hipEventRecord(chunk)");
       }
     } else {
-      std::vector<Work> hits, faults;
+      std::vector<Work> hits, faults[2];
       for (size_t i = 0; i < cp.experts.size(); ++i)
-        (cp.fault[i] ? faults : hits).push_back(work_of(cp.experts[i], L.chunk_ptrs[ci][i]));
+        (cp.fault[i] ? faults[L.late[ci][i]] : hits).push_back(work_of(cp.experts[i], L.chunk_ptrs[ci][i]));
       if (ci == 0 && ctx->desc.has_shared) {
         Work wk;
         wk.w = L.shared_dev;
@@ -1302,12 +1334,14 @@ wisp_status wisp_moe_forward(wisp_ctx* ctx, int32_t layer, const void* x_dev, in
         hits.push_back(std::move(wk));
       }
       if (!hits.empty() && (s = run_ffn(ctx, hits, x_dev, sm)) != WISP_OK) return s;
-      if (!faults.empty()) {
-        WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[ci], 0), "hipStreamWaitEvent(fill)");
-        if ((s = run_ffn(ctx, faults, x_dev, sm)) != WISP_OK) return s;
+      for (int h = 0; h < 2; ++h) {
+        if (!faults[h].empty()) {
+          WISP_HIP(hipStreamWaitEvent(sm, L.fill_ev[2 * ci + h], 0), "hipStreamWaitEvent(fill)");
+          if ((s = run_ffn(ctx, faults[h], x_dev, sm)) != WISP_OK) return s;
+        }
+        if (nch > 1) WISP_HIP(hipEventRecord(L.chunk_ev[2 * ci + h], sm), "hipEventRecord(chunk)");
       }
     }
-    if (ci + 1 < nch) WISP_HIP(hipEventRecord(L.chunk_ev[ci], sm), "hipEventRecord(chunk)");
   }
   if (grouped) {   // the grouped GEMMs leave bf16 expert outputs (no shared expert on this path)
     LaunchTiming tc = timing_begin(ctx, WISP_K_COMBINE);
