@@ -518,7 +518,7 @@ wisp_status issue_fills(wisp_ctx* c, int32_t layer, size_t ci) {
   for (size_t i = 0; i < cp.experts.size(); ++i)
     if (cp.fault[i]) fills[late[i]].push_back({cp.experts[i], cp.slots[i]});
   const bool batch = L.T >= kGroupedMinTokens && grouped_supported(c->shape, c->desc.has_shared);
-  for (int h = 0; h < 2; ++h) {
+  for (int h = 0; h < (nch > 1 ? 2 : 1); ++h) {   // a single chunk has one half
     if (ci == 0) {
       if (h == 0 && L.use_ev_recorded) WISP_HIP(hipStreamWaitEvent(c->side, L.use_ev, 0), "hipStreamWaitEvent(use)");
     } else {
